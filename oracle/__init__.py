@@ -1,0 +1,138 @@
+"""CPU oracle for emulated stochastic-computing matrix multiplication.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  The product library
+(``paper_2609_32922_amd``) never imports it and shares no code with it.
+
+The arithmetic lives in ``sc_oracle.c`` (plain C, OpenMP over rows, one byte per
+stream bit, float64 decode); this module only builds it with gcc and marshals
+numpy arrays through ctypes.  Each C function's header comment cites the passage
+of the paper it follows (Sec. 3.1 encoding / comparator / Eq. (1), Sec. 4.2
+boundaries and row lengths, Sec. A.1 LFSR).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sc_oracle.c")
+_LIB = os.path.join(_HERE, "libsc_oracle.so")
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile ``sc_oracle.c`` into ``libsc_oracle.so`` with gcc (OpenMP)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.run(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11",
+                        _SRC, "-o", tmp], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB)
+        i32, u32, u64, vp = ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p
+        lib.oracle_splitmix64.argtypes = [u64]
+        lib.oracle_splitmix64.restype = u64
+        lib.oracle_seed_state.argtypes = [u64, u32]
+        lib.oracle_seed_state.restype = u32
+        lib.oracle_lfsr_draws.argtypes = [u32, i32, vp]
+        lib.oracle_lfsr_draws.restype = None
+        lib.oracle_lfsr_states.argtypes = [u32, i32, vp]
+        lib.oracle_lfsr_states.restype = None
+        lib.oracle_beta_bipolar.argtypes = [i32]
+        lib.oracle_beta_bipolar.restype = i32
+        lib.oracle_beta_unipolar.argtypes = [i32]
+        lib.oracle_beta_unipolar.restype = i32
+        lib.oracle_streams.argtypes = [i32, i32, vp, i32, u64, u32, i32, vp]
+        lib.oracle_streams.restype = None
+        lib.oracle_sc_gemm.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, u64,
+                                       vp, vp, i32]
+        lib.oracle_sc_gemm.restype = ctypes.c_int
+        lib.oracle_max_threads.argtypes = []
+        lib.oracle_max_threads.restype = i32
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data) if a is not None else None
+
+
+def splitmix64(x: int) -> int:
+    return int(_load().oracle_splitmix64(ctypes.c_uint64(x & (2**64 - 1))))
+
+
+def seed_state(seed: int, op: int) -> int:
+    """Initial LFSR state of operand ``op`` (0 = A, 1 = B) for ``seed``."""
+    return int(_load().oracle_seed_state(seed, op))
+
+
+def lfsr_draws(state: int, n: int) -> np.ndarray:
+    """``n`` comparator draws (uint8) from an initial LFSR state."""
+    out = np.zeros(max(n, 1), np.uint8)
+    _load().oracle_lfsr_draws(state, n, _ptr(out))
+    return out[:n]
+
+
+def lfsr_states(state: int, n: int) -> np.ndarray:
+    out = np.zeros(max(n, 1), np.uint32)
+    _load().oracle_lfsr_states(state, n, _ptr(out))
+    return out[:n]
+
+
+def comparator_sequence(seed: int, op: int, n: int) -> np.ndarray:
+    """The comparator sequence r_0..r_{n-1} of operand ``op`` for ``seed``."""
+    return lfsr_draws(seed_state(seed, op), n)
+
+
+def beta_bipolar(q: int) -> int:
+    return int(_load().oracle_beta_bipolar(int(q)))
+
+
+def beta_unipolar(q: int) -> int:
+    return int(_load().oracle_beta_unipolar(int(q)))
+
+
+def streams(X: np.ndarray, polarity: int, seed: int, op: int, length: int) -> np.ndarray:
+    """Materialised 0/1 streams, shape (rows, K, length), uint8."""
+    X = np.ascontiguousarray(X, dtype=np.int8)
+    rows, K = X.shape
+    z = np.zeros((rows, K, max(length, 1)), np.uint8)
+    _load().oracle_streams(rows, K, _ptr(X), polarity, seed, op, length, _ptr(z))
+    return z[:, :, :length]
+
+
+def sc_gemm(A: np.ndarray, B: np.ndarray, sA: np.ndarray, sB: np.ndarray,
+            L: np.ndarray, L_max: int, polarity: int, seed: int,
+            nthreads: int = 0, want_out: bool = True):
+    """Oracle SC GEMM.  Returns ``(counts int32 MxN, out float64 MxN or None)``."""
+    A = np.ascontiguousarray(A, dtype=np.int8)
+    B = np.ascontiguousarray(B, dtype=np.int8)
+    sA = np.ascontiguousarray(sA, dtype=np.float32)
+    sB = np.ascontiguousarray(sB, dtype=np.float32)
+    L = np.ascontiguousarray(L, dtype=np.int32)
+    M, K = A.shape
+    N, K2 = B.shape
+    if K2 != K or sA.shape != (M,) or sB.shape != (N,) or L.shape != (M,):
+        raise ValueError("shape mismatch")
+    counts = np.zeros((M, N), np.int32)
+    out = np.zeros((M, N), np.float64) if want_out else None
+    rc = _load().oracle_sc_gemm(M, N, K, _ptr(A), _ptr(B), _ptr(sA), _ptr(sB), _ptr(L),
+                                int(L_max), int(polarity), ctypes.c_uint64(seed),
+                                _ptr(counts), _ptr(out), int(nthreads))
+    if rc != 0:
+        raise ValueError("oracle_sc_gemm failed with code %d" % rc)
+    return counts, out
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
