@@ -1,0 +1,158 @@
+"""Benchmark of the MI355X SC GEMM: one step = one full sc_gemm call (comparator
+sequences, row-length scheduler, marginals, stream generation into bit planes,
+packed AND+popcount GEMM and decode) over one batch of synthetic input already
+resident in HBM.
+
+Prints ONE JSON line.  ``value`` is whole-call throughput in stream-bit-ops/s
+(N * K * sum_i L_i per step / seconds per step).  ``roofline`` is for the dominant
+kernel (the packed GEMM), timed with HIP events recorded by the library around that
+kernel on the call's stream, against the integer-VALU peak for 2 instructions per
+32 bit pairs: 256 CUs x 64 lanes x 2.4 GHz x 32 / 2 = 6.29e14 bit-ops/s.
+``cpu_baseline`` times the CPU oracle on a bounded row sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "SC stream-bit-ops/sec (M·N·K·L) and % of gfx950 bitop+popcount peak"
+PEAK_BITOPS = 256 * 64 * 2.4e9 * 32 / 2          # 6.2915e14
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="vitb16_fc1_L128")
+    p.add_argument("--cpu-rows", type=int, default=0,
+                   help="rows of A for the oracle sample (0 = size it to ~15 s)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--traffic", default=None,
+                   help="JSON file with the measured HBM bytes per GEMM launch")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build runs the SC GEMM on a single "
+              "MI355X (rows shard across GPUs with no collective; see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_32922_amd as scg
+    import workloads as W
+
+    w = W.WORKLOADS[args.workload]()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    staged = []
+    for g in w.gemms:
+        t = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (g.A, g.sA, g.B, g.sB, g.L)]
+        out = torch.empty((g.batch, g.M, g.N), dtype=torch.float32, device=dev)
+        d = scg.make_desc(t[0], t[2], g.L_max, g.polarity, g.seed)
+        ws = scg.Workspace(scg.sc_gemm_workspace_size(d), dev)
+        staged.append((g, t, out, ws))
+    bitops = w.bitops()
+    nsteps = args.steps
+    ev_pairs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                 for _ in w.gemms] for _ in range(nsteps)]
+    for pairs in ev_pairs:             # create the underlying HIP events
+        for e0, e1 in pairs:
+            e0.record(stream)
+            e1.record(stream)
+    torch.cuda.synchronize()
+
+    def step(pairs=None):
+        for k, (g, t, out, ws) in enumerate(staged):
+            pe = None if pairs is None else (pairs[k][0].cuda_event, pairs[k][1].cuda_event)
+            scg.gemm(t[0], t[1], t[2], t[3], t[4], L_max=g.L_max, polarity=g.polarity,
+                     seed=g.seed, out=out, workspace=ws, stream=stream, prof_events=pe)
+
+    for _ in range(args.warmup):
+        step()
+    rc = scg.sc_gemm_status(staged[0][3].ptr, int(stream.cuda_stream))
+    if rc != 0:
+        raise SystemExit("device status error: %s" % scg.strerror(rc))
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for s in range(nsteps):
+        step(ev_pairs[s])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t0.elapsed_time(t1)
+    ms_per_step = ms_total / nsteps
+    value = bitops / (ms_per_step * 1e-3)
+
+    # dominant kernel: the packed GEMM of the largest GEMM in the workload
+    kidx = int(np.argmax([g.bitops() for g in w.gemms]))
+    gemm_ms = float(np.mean([ev_pairs[s][kidx][0].elapsed_time(ev_pairs[s][kidx][1])
+                             for s in range(nsteps)]))
+    g_dom = w.gemms[kidx]
+    achieved = g_dom.bitops() / (gemm_ms * 1e-3)
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            traffic = json.load(f).get(args.workload)
+    roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_BITOPS / 1e12,
+                "unit": "Tbitop/s", "frac": achieved / PEAK_BITOPS, "traffic": traffic,
+                "kernel": "k_gemm<bipolar>" if g_dom.polarity == 0 else "k_gemm<unipolar>",
+                "kernel_ms": gemm_ms}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, args.cpu_rows)
+
+    g0 = w.gemms[0]
+    cfg = {"workload": w.name, "gemms": [{"name": g.name, "batch": g.batch, "M": g.M, "N": g.N,
+                                          "K": g.K, "L_mean": float(g.L.mean()),
+                                          "L_max": g.L_max} for g in w.gemms],
+           "polarity": "bipolar_xnor" if g0.polarity == 0 else "unipolar_and_sign_magnitude",
+           "rng": "lfsr32", "seed": g0.seed, "bitops_per_step": bitops}
+    line = {"metric": METRIC, "value": value, "unit": "stream-bit-ops/s", "n_gpus": 1,
+            "steps": nsteps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+            "data": "synthetic", "config": cfg, "roofline": roofline, "cpu_baseline": cpu}
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(w, rows):
+    """The CPU oracle, as it stands, on the first rows of the dominant GEMM."""
+    import oracle
+    threads = min(len(os.sched_getaffinity(0)), 16)
+    g = max(w.gemms, key=lambda x: x.bitops())
+    b = 0
+    if rows <= 0:
+        # size the sample so the timed oracle run takes roughly 15 s
+        probe = 8
+        t = time.perf_counter()
+        oracle.sc_gemm(g.A[b][:probe], g.B[0 if g.B.shape[0] == 1 else b], g.sA[b][:probe],
+                       g.sB[0 if g.B.shape[0] == 1 else b], g.L[b][:probe], g.L_max, g.polarity,
+                       g.seed, nthreads=threads, want_out=True)
+        dt = time.perf_counter() - t
+        rows = int(max(probe, min(g.M, probe * 15.0 / max(dt, 1e-3))))
+    bB = 0 if g.B.shape[0] == 1 else b
+    t = time.perf_counter()
+    oracle.sc_gemm(g.A[b][:rows], g.B[bB], g.sA[b][:rows], g.sB[bB], g.L[b][:rows], g.L_max,
+                   g.polarity, g.seed, nthreads=threads, want_out=True)
+    dt = time.perf_counter() - t
+    ops = int(g.N) * int(g.K) * int(g.L[b][:rows].astype(np.int64).sum())
+    return {"value": ops / dt, "unit": "stream-bit-ops/s", "cores": threads, "kind": "oracle",
+            "seconds": dt,
+            "sample": "%s/%s rows 0..%d of %d, all %d columns, K=%d, %d stream-bit-ops "
+                      "(B streams materialised inside the timed run)"
+                      % (w.name, g.name, rows - 1, g.M, g.N, g.K, ops)}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,144 @@
+/*
+ * scgemm.h -- C ABI of the MI355X (gfx950) stochastic-computing GEMM library.
+ *
+ * Operation (paper "Precision As You Need: Stochastic Computing Is a Dense
+ * Adaptive Quantizer", Sec. 3.1 "SC matrix multiplication", Eq. (1), and Sec. 4.2
+ * "Datapath"): for each batch entry b,
+ *
+ *     out[b] (M x N) = SC estimate of  (sA . A[b]) (sB . B[b])^T
+ *
+ * where A[b] is M x K int8 and B[b] is N x K int8 (both already quantised to
+ * [-127, 127] with per-row symmetric scales sA, sB, as the paper assumes).  Every
+ * int8 value is encoded into a stream of L_i bits by a comparator against a seeded
+ * comparator sequence (Sec. 3.1 "Bitstream generation"), one sequence per operand
+ * shared by all of its elements (Sec. 4.2: the table is indexed by boundary and
+ * cycle only).  Row i of A runs L_i cycles (Sec. 3.1 "early termination", Sec. 4.2
+ * row-length vector).  Bit products are XNOR (bipolar) or AND (unipolar,
+ * sign-magnitude), counted over cycles and the inner dimension, and decoded:
+ *
+ *   bipolar   X_ij = sum_{d<K} sum_{l<L_i} XNOR(zA_idl, zB_jdl)
+ *             out_ij = sA_i sB_j 127^2 (2 X_ij / L_i - K)                 (Eq. (1))
+ *   unipolar  S_ij = c_pp + c_nn - c_pn - c_np  (signed AND counts)
+ *             out_ij = sA_i sB_j 127^2 S_ij / L_i
+ *   L_i = 0  gives out_ij = 0 and a zero count.
+ *
+ * Comparator encoding (the paper leaves the exact maps open; these are fixed here):
+ *   sequence  r_l in [0,255]: 32-bit Galois LFSR (right shift, feedback mask
+ *             0x80200003, polynomial x^32+x^22+x^2+x+1), 8 steps per draw, first
+ *             output bit most significant; initial state = upper 32 bits of
+ *             SplitMix64(2*seed + op), op 0 for A and 1 for B, 0 replaced by 1.
+ *   bipolar   z = [r_l < beta(q)],  beta(q)   = floor((256 (q+127) + 127) / 254)
+ *   unipolar  z = [r_l < beta_u(q)], beta_u(q) = floor((256 |q| + 63) / 127),
+ *             sign = (q < 0)
+ *
+ * Memory: every array pointer is a HIP DEVICE pointer; the caller owns all memory.
+ * A pointer may be NULL only when its array has no elements (e.g. A when K = 0).
+ * The library allocates nothing in sc_gemm and keeps no state between calls; all
+ * temporaries live in the caller's workspace.  Calls are asynchronous on `stream`
+ * (a hipStream_t passed as void*; NULL = the default stream).  Two calls that share
+ * one workspace must be ordered on the same stream.
+ *
+ * Errors: arguments are checked on the host before anything is enqueued and a
+ * negative SC_ERR_* code is returned; nothing is launched then.  Launch failures
+ * return SC_ERR_HIP.  Stream lengths live on the device, so their range is checked
+ * by a kernel into a status word in the workspace; rows whose L_i is outside
+ * [0, L_max] are computed as L_i = 0 and sc_gemm_status() reports
+ * SC_ERR_DEVICE_STATUS.
+ */
+#ifndef SCGEMM_H
+#define SCGEMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    SC_OK = 0,
+    SC_ERR_NULL = -1,          /* a required pointer is NULL */
+    SC_ERR_SHAPE = -2,         /* batch, M, N or K negative, or K > SC_K_LIMIT */
+    SC_ERR_LEN = -3,           /* L_max outside [1, SC_L_MAX_LIMIT] */
+    SC_ERR_POLARITY = -4,      /* polarity not one of SC_BIPOLAR_XNOR / SC_UNIPOLAR_AND_SM */
+    SC_ERR_RNG = -5,           /* rng not SC_RNG_LFSR32 */
+    SC_ERR_WORKSPACE = -6,     /* workspace NULL or smaller than sc_gemm_workspace_size() */
+    SC_ERR_HIP = -7,           /* a HIP runtime call or kernel launch failed */
+    SC_ERR_DEVICE_STATUS = -8, /* (sc_gemm_status) some L_i was outside [0, L_max] */
+    SC_ERR_STRIDE = -9         /* a row stride is smaller than the row length */
+};
+
+enum { SC_BIPOLAR_XNOR = 0, SC_UNIPOLAR_AND_SM = 1 };
+enum { SC_RNG_LFSR32 = 0 };
+
+#define SC_L_MAX_LIMIT 4096     /* largest supported stream length */
+#define SC_K_LIMIT (1 << 20)    /* largest inner dimension (counts stay exact in int32) */
+
+typedef struct sc_gemm_desc {
+    int32_t batch;              /* >= 0 independent problems */
+    int32_t M, N, K;            /* A[b] is M x K, B[b] is N x K, out[b] is M x N */
+    int64_t lda, ldb, ldo;      /* row strides in elements (>= K, >= K, >= N) */
+    int64_t strideA, strideB, strideO;   /* batch strides in elements; 0 = broadcast */
+    int64_t strideSA, strideSB;          /* batch strides of sA (M) and sB (N) */
+    int64_t strideL;                     /* batch stride of L_per_row (M) */
+    int32_t L_max;              /* 1..SC_L_MAX_LIMIT; every L_i must lie in [0, L_max] */
+    int32_t polarity;           /* SC_BIPOLAR_XNOR or SC_UNIPOLAR_AND_SM */
+    int32_t rng;                /* SC_RNG_LFSR32 */
+    int32_t reserved;           /* must be 0 */
+    uint64_t seed;              /* comparator seed; same seed => bit-identical results */
+    void *prof_event_begin;     /* optional hipEvent_t recorded just before the main */
+    void *prof_event_end;       /*   GEMM kernel and just after it (profiling); NULL = off */
+} sc_gemm_desc;
+
+/* Bytes of device workspace sc_gemm needs for `desc` (host-only, no HIP call).
+ * Returns SC_OK and writes *bytes, or a negative SC_ERR_* code for a bad desc. */
+int sc_gemm_workspace_size(const sc_gemm_desc *desc, size_t *bytes);
+
+/*
+ * The SC GEMM (Eq. (1) with per-row stream lengths).
+ *   A          int8,  A[b*strideA + i*lda + d]
+ *   sA         fp32,  sA[b*strideSA + i]       per-row scales of A
+ *   B          int8,  B[b*strideB + j*ldb + d]
+ *   sB         fp32,  sB[b*strideSB + j]       per-row scales of B
+ *   L_per_row  int32, L[b*strideL + i]         stream length of row i of A
+ *   out        fp32,  out[b*strideO + i*ldo + j]   decoded estimate (written)
+ *   counts     int32, same layout as out, NULLABLE: raw X_ij (bipolar) or S_ij
+ *              (unipolar) for bit-exact checks
+ *   workspace  device memory of at least sc_gemm_workspace_size() bytes, 256-byte
+ *              aligned; contents on entry are ignored, contents on exit are
+ *              internal (only sc_gemm_status reads them)
+ *   stream     hipStream_t or NULL
+ * Returns SC_OK once everything is enqueued (results are ready when the stream
+ * reaches that point), or a negative SC_ERR_* code.
+ */
+int sc_gemm(const sc_gemm_desc *desc,
+            const int8_t *A, const float *sA,
+            const int8_t *B, const float *sB,
+            const int32_t *L_per_row,
+            float *out, int32_t *counts,
+            void *workspace, size_t workspace_bytes,
+            void *stream);
+
+/* Synchronises `stream` and reads the device status word that the last sc_gemm on
+ * `workspace` wrote: SC_OK, or SC_ERR_DEVICE_STATUS if some L_i was out of range. */
+int sc_gemm_status(const void *workspace, void *stream);
+
+/*
+ * The comparator sequence r_0 .. r_{n-1} of operand `op` (0 = A, 1 = B) for `seed`,
+ * computed on the device exactly as sc_gemm computes it (Sec. 3.1 "Bitstream
+ * generation"; LFSR of Sec. A.1 under the reading above).  `out` is a device
+ * buffer of n bytes.  1 <= n <= SC_L_MAX_LIMIT.  Asynchronous on `stream`.
+ */
+int sc_comparator_sequence(uint64_t seed, int32_t op, int32_t n, uint8_t *out, void *stream);
+
+/* Human-readable name of a status code (static string). */
+const char *sc_strerror(int code);
+
+/* Library ABI version (major*10000 + minor*100 + patch). */
+int sc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCGEMM_H */

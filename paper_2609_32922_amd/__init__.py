@@ -1,0 +1,115 @@
+"""MI355X (gfx950) emulated stochastic-computing GEMM.
+
+The product is libscgemm.so (C ABI in include/scgemm.h, HIP kernels in csrc/).
+This package is its thin Python binding: ``_lib`` mirrors the C functions one to
+one (same names), and ``gemm`` below only shapes torch device tensors into a
+descriptor and calls ``sc_gemm``.  PyTorch supplies device memory and the stream;
+every step of the computation runs in the library's kernels, and nothing falls
+back to the CPU: without the built library every call raises.
+"""
+from __future__ import annotations
+
+from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_L_MAX_LIMIT, SC_OK,  # noqa: F401
+                   SC_RNG_LFSR32, SC_UNIPOLAR_AND_SM, ScError, ScGemmDesc, load, sc_comparator_sequence,
+                   sc_gemm, sc_gemm_status, sc_gemm_workspace_size, sc_version, strerror)
+
+__all__ = ["gemm", "make_desc", "comparator_sequence", "Workspace", "ScGemmDesc", "ScError",
+           "sc_gemm", "sc_gemm_workspace_size", "sc_gemm_status", "sc_comparator_sequence",
+           "SC_BIPOLAR_XNOR", "SC_UNIPOLAR_AND_SM"]
+
+
+def _stream_handle(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def make_desc(A, B, L_max: int, polarity: int, seed: int) -> ScGemmDesc:
+    """Descriptor for contiguous A [batch, M, K] and B [batch or 1, N, K] tensors."""
+    if A.dim() == 2:
+        A = A.unsqueeze(0)
+    if B.dim() == 2:
+        B = B.unsqueeze(0)
+    batch, M, K = A.shape
+    nb, N, K2 = B.shape
+    if K2 != K or nb not in (1, batch):
+        raise ValueError("A is [batch, M, K], B must be [batch or 1, N, K]")
+    d = ScGemmDesc()
+    d.batch, d.M, d.N, d.K = batch, M, N, K
+    d.lda, d.ldb, d.ldo = K, K, N
+    d.strideA, d.strideB, d.strideO = M * K, (N * K if nb == batch and batch > 1 else 0), M * N
+    d.strideSA, d.strideSB, d.strideL = M, (N if nb == batch and batch > 1 else 0), M
+    d.L_max, d.polarity, d.rng, d.reserved, d.seed = int(L_max), int(polarity), SC_RNG_LFSR32, 0, int(seed)
+    return d
+
+
+class Workspace:
+    """A reusable device workspace (a torch uint8 tensor, 256-byte aligned)."""
+
+    def __init__(self, nbytes: int, device="cuda"):
+        import torch
+        self.nbytes = int(nbytes)
+        self._buf = torch.empty(self.nbytes + 256, dtype=torch.uint8, device=device)
+        base = self._buf.data_ptr()
+        self.ptr = (base + 255) // 256 * 256
+
+    def ensure(self, nbytes: int):
+        if nbytes > self.nbytes:
+            self.__init__(nbytes, self._buf.device)
+        return self
+
+
+def gemm(A, sA, B, sB, L, *, L_max: int, polarity: int = SC_BIPOLAR_XNOR, seed: int = 0,
+         out=None, counts=None, want_counts: bool = False, workspace: Workspace = None,
+         stream=None, check_status: bool = False, prof_events=None):
+    """SC GEMM on torch device tensors.
+
+    A int8 [batch, M, K] (or [M, K]), sA float32 [batch, M], B int8 [batch or 1, N, K],
+    sB float32 [batch or 1, N], L int32 [batch, M].  Returns (out, counts or None).
+    """
+    import torch
+    squeeze = A.dim() == 2
+    A3 = A.unsqueeze(0) if A.dim() == 2 else A
+    B3 = B.unsqueeze(0) if B.dim() == 2 else B
+    d = make_desc(A3, B3, L_max, polarity, seed)
+    for t, name in ((A3, "A"), (B3, "B"), (sA, "sA"), (sB, "sB"), (L, "L")):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous device tensor" % name)
+    if A3.dtype != torch.int8 or B3.dtype != torch.int8 or sA.dtype != torch.float32 \
+            or sB.dtype != torch.float32 or L.dtype != torch.int32:
+        raise TypeError("dtypes: A, B int8; sA, sB float32; L int32")
+    batch, M, N = d.batch, d.M, d.N
+    if sA.numel() != batch * M or L.numel() != batch * M or sB.numel() != B3.shape[0] * N:
+        raise ValueError("scale or length vector has the wrong size")
+    if out is None:
+        out = torch.empty((batch, M, N), dtype=torch.float32, device=A.device)
+    if counts is None and want_counts:
+        counts = torch.empty((batch, M, N), dtype=torch.int32, device=A.device)
+    nbytes = sc_gemm_workspace_size(d)
+    ws = (workspace or Workspace(nbytes, A.device)).ensure(nbytes)
+    if prof_events is not None:
+        d.prof_event_begin = prof_events[0]
+        d.prof_event_end = prof_events[1]
+    sh = _stream_handle(stream)
+    rc = sc_gemm(d, A3.data_ptr(), sA.data_ptr(), B3.data_ptr(), sB.data_ptr(), L.data_ptr(),
+                 out.data_ptr(), counts.data_ptr() if counts is not None else 0, ws.ptr, ws.nbytes, sh)
+    if rc != SC_OK:
+        raise ScError(rc, "sc_gemm")
+    if check_status:
+        rc = sc_gemm_status(ws.ptr, sh)
+        if rc != SC_OK:
+            raise ScError(rc, "sc_gemm (device status)")
+    if squeeze:
+        out = out[0]
+        counts = counts[0] if counts is not None else None
+    return out, counts
+
+
+def comparator_sequence(seed: int, op: int, n: int, stream=None):
+    """Device comparator sequence r_0..r_{n-1} (uint8 tensor) of operand ``op``."""
+    import torch
+    out = torch.empty(n, dtype=torch.uint8, device="cuda")
+    rc = sc_comparator_sequence(seed, op, n, out.data_ptr(), _stream_handle(stream))
+    if rc != SC_OK:
+        raise ScError(rc, "sc_comparator_sequence")
+    return out

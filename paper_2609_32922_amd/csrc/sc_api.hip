@@ -1,0 +1,210 @@
+// Host side of libscgemm: argument checks, workspace layout and the launch sequence.
+// Every check runs before anything is enqueued; the library allocates nothing.
+#include <limits.h>
+
+#include "sc_internal.h"
+
+namespace scg {
+
+namespace {
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// checked size arithmetic: returns false on overflow of size_t
+bool mul_ok(size_t a, size_t b, size_t *r) {
+    if (a != 0 && b > SIZE_MAX / a) return false;
+    *r = a * b;
+    return true;
+}
+
+}  // namespace
+
+bool make_layout(const sc_gemm_desc &d, Layout *lay) {
+    Layout l{};
+    l.KB = (d.K + 31) / 32;
+    l.MT = (d.M + BM - 1) / BM;
+    l.NT = (d.N + BN - 1) / BN;
+    l.LBS = (int)round_up(d.L_max, LCH);
+    l.LP = (int)round_up(d.L_max, LSTEP);
+    l.nbB = (d.strideB == 0) ? 1 : d.batch;
+    if (l.nbB < 1) l.nbB = 1;
+    const bool uni = d.polarity == SC_UNIPOLAR_AND_SM;
+
+    // the status word is always the first word of the workspace
+    size_t off = 0;
+    l.off_status = off;
+    off = align256(off + 4);
+    l.off_rA = off;
+    off = align256(off + (size_t)l.LBS * 4);
+    l.off_rB = off;
+    off = align256(off + (size_t)l.LBS * 4);
+
+    // one A block per batch entry
+    const size_t rowsA = (size_t)l.MT * BM;
+    size_t a = 0, sz;
+    l.off_perm = a;
+    a = align256(a + rowsA * 4);
+    l.off_Ls = a;
+    a = align256(a + rowsA * 4);
+    l.off_RA = a;
+    a = align256(a + rowsA * 4);
+    l.off_tileL = a;
+    a = align256(a + (size_t)l.MT * 4);
+    l.off_tileOff = a;
+    a = align256(a + (size_t)l.MT * 8);
+    l.off_Ap = a;
+    if (!mul_ok(rowsA * (size_t)l.KB, (size_t)l.LP * 4, &sz)) return false;
+    a = align256(a + sz);
+    l.off_SA = a;
+    if (uni) a = align256(a + rowsA * (size_t)l.KB * 4);
+    l.stride_batchA = a;
+    const size_t baseA = off;
+    size_t totA;
+    if (!mul_ok(a, (size_t)(d.batch > 0 ? d.batch : 0), &totA)) return false;
+    off += totA;
+
+    // one B block per distinct B batch entry
+    const size_t rowsB = (size_t)l.NT * BN;
+    size_t bb = 0;
+    l.off_Bp = bb;
+    if (!mul_ok(rowsB * (size_t)l.KB, (size_t)l.LBS * 4, &sz)) return false;
+    bb = align256(bb + sz);
+    l.off_SB = bb;
+    if (uni) bb = align256(bb + rowsB * (size_t)l.KB * 4);
+    l.off_RB = bb;
+    if (!uni) bb = align256(bb + (size_t)d.N * (size_t)(d.L_max + 1) * 4);
+    l.stride_batchB = bb;
+    const size_t baseB = off;
+    size_t totB;
+    if (!mul_ok(bb, (size_t)l.nbB, &totB)) return false;
+    off += totB;
+
+    // make every offset absolute for batch entry 0
+    l.off_perm += baseA;
+    l.off_Ls += baseA;
+    l.off_RA += baseA;
+    l.off_tileL += baseA;
+    l.off_tileOff += baseA;
+    l.off_Ap += baseA;
+    l.off_SA += baseA;
+    l.off_Bp += baseB;
+    l.off_SB += baseB;
+    l.off_RB += baseB;
+    l.total = off;
+    *lay = l;
+    return true;
+}
+
+static int check_desc(const sc_gemm_desc *d) {
+    if (d == nullptr) return SC_ERR_NULL;
+    if (d->batch < 0 || d->M < 0 || d->N < 0 || d->K < 0 || d->K > SC_K_LIMIT) return SC_ERR_SHAPE;
+    if (d->L_max < 1 || d->L_max > SC_L_MAX_LIMIT) return SC_ERR_LEN;
+    // counts 2*X and K*L must stay exact in int32
+    if ((int64_t)d->K * d->L_max > (1ll << 29)) return SC_ERR_SHAPE;
+    if (d->polarity != SC_BIPOLAR_XNOR && d->polarity != SC_UNIPOLAR_AND_SM) return SC_ERR_POLARITY;
+    if (d->rng != SC_RNG_LFSR32 || d->reserved != 0) return SC_ERR_RNG;
+    if (d->lda < d->K || d->ldb < d->K || d->ldo < d->N) return SC_ERR_STRIDE;
+    if (d->strideA < 0 || d->strideB < 0 || d->strideO < 0 || d->strideSA < 0 || d->strideSB < 0 ||
+        d->strideL < 0)
+        return SC_ERR_STRIDE;
+    // distinct batch entries must not overlap in the output
+    if (d->batch > 1 && d->M > 0 && d->N > 0 && d->strideO < (int64_t)(d->M - 1) * d->ldo + d->N)
+        return SC_ERR_STRIDE;
+    return SC_OK;
+}
+
+}  // namespace scg
+
+using namespace scg;
+
+extern "C" {
+
+int sc_version(void) { return 10000; }
+
+const char *sc_strerror(int code) {
+    switch (code) {
+        case SC_OK: return "SC_OK";
+        case SC_ERR_NULL: return "SC_ERR_NULL: a required pointer is NULL";
+        case SC_ERR_SHAPE: return "SC_ERR_SHAPE: bad batch/M/N/K (or K*L_max too large)";
+        case SC_ERR_LEN: return "SC_ERR_LEN: L_max outside [1, SC_L_MAX_LIMIT]";
+        case SC_ERR_POLARITY: return "SC_ERR_POLARITY: unknown polarity";
+        case SC_ERR_RNG: return "SC_ERR_RNG: unknown rng (or reserved field not 0)";
+        case SC_ERR_WORKSPACE: return "SC_ERR_WORKSPACE: workspace missing or too small";
+        case SC_ERR_HIP: return "SC_ERR_HIP: a HIP call or kernel launch failed";
+        case SC_ERR_DEVICE_STATUS: return "SC_ERR_DEVICE_STATUS: some L_i outside [0, L_max]";
+        case SC_ERR_STRIDE: return "SC_ERR_STRIDE: a stride is too small or negative";
+        default: return "unknown status code";
+    }
+}
+
+int sc_gemm_workspace_size(const sc_gemm_desc *desc, size_t *bytes) {
+    if (bytes == nullptr) return SC_ERR_NULL;
+    const int rc = check_desc(desc);
+    if (rc != SC_OK) return rc;
+    Layout lay;
+    if (!make_layout(*desc, &lay)) return SC_ERR_SHAPE;
+    *bytes = lay.total;
+    return SC_OK;
+}
+
+int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const int8_t *B,
+            const float *sB, const int32_t *L_per_row, float *out, int32_t *counts, void *workspace,
+            size_t workspace_bytes, void *stream) {
+    const int rc = check_desc(desc);
+    if (rc != SC_OK) return rc;
+    const sc_gemm_desc &d = *desc;
+    // a pointer may be NULL only when the array it points to has no elements
+    const bool anyM = d.batch > 0 && d.M > 0, anyN = d.batch > 0 && d.N > 0;
+    if ((anyM && d.K > 0 && A == nullptr) || (anyN && d.K > 0 && B == nullptr) ||
+        (anyM && (sA == nullptr || L_per_row == nullptr)) || (anyN && sB == nullptr) ||
+        (anyM && anyN && out == nullptr))
+        return SC_ERR_NULL;
+    Layout lay;
+    if (!make_layout(d, &lay)) return SC_ERR_SHAPE;
+    if (workspace == nullptr || workspace_bytes < lay.total ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return SC_ERR_WORKSPACE;
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
+
+    hipError_t e = launch_draws(d.seed, lay.LBS, reinterpret_cast<uint32_t *>(ws + lay.off_rA),
+                                reinterpret_cast<uint32_t *>(ws + lay.off_rB), nullptr, -1,
+                                reinterpret_cast<uint32_t *>(ws + lay.off_status), st);
+    if (e != hipSuccess) return SC_ERR_HIP;
+    if (d.batch == 0 || d.M == 0 || d.N == 0) return SC_OK;
+
+    if ((e = launch_schedule(d, lay, L_per_row, ws, st)) != hipSuccess) return SC_ERR_HIP;
+    if (d.polarity == SC_BIPOLAR_XNOR &&
+        (e = launch_marginals(d, lay, A, B, ws, st)) != hipSuccess)
+        return SC_ERR_HIP;
+    if ((e = launch_planes(d, lay, A, B, ws, st)) != hipSuccess) return SC_ERR_HIP;
+    if (d.prof_event_begin != nullptr &&
+        hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_begin), st) != hipSuccess)
+        return SC_ERR_HIP;
+    if ((e = launch_gemm(d, lay, sA, sB, out, counts, ws, st)) != hipSuccess) return SC_ERR_HIP;
+    if (d.prof_event_end != nullptr &&
+        hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_end), st) != hipSuccess)
+        return SC_ERR_HIP;
+    return SC_OK;
+}
+
+int sc_gemm_status(const void *workspace, void *stream) {
+    if (workspace == nullptr) return SC_ERR_NULL;
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    if (hipStreamSynchronize(st) != hipSuccess) return SC_ERR_HIP;
+    uint32_t word = 0;
+    if (hipMemcpy(&word, workspace, sizeof(word), hipMemcpyDeviceToHost) != hipSuccess)
+        return SC_ERR_HIP;
+    return (word & STATUS_BAD_LENGTH) ? SC_ERR_DEVICE_STATUS : SC_OK;
+}
+
+int sc_comparator_sequence(uint64_t seed, int32_t op, int32_t n, uint8_t *out, void *stream) {
+    if (out == nullptr) return SC_ERR_NULL;
+    if (op != 0 && op != 1) return SC_ERR_RNG;
+    if (n < 1 || n > SC_L_MAX_LIMIT) return SC_ERR_LEN;
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    if (launch_draws(seed, n, nullptr, nullptr, out, op, nullptr, st) != hipSuccess) return SC_ERR_HIP;
+    return SC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,69 @@
+// Internal definitions shared by the kernels and the host API of libscgemm.
+//
+// Data layout in device memory (all inside the caller's workspace):
+//
+//   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
+//   status     one uint32 (bit 0: some L_i out of range)
+//   per batch entry b of A (batch entries):
+//     perm[MT*BM]      sorted position -> original row (or -1 for padding)
+//     Ls[MT*BM]        stream length at each sorted position
+//     RA[MT*BM]        row marginal  sum_d sum_{l<L} zA   (bipolar)
+//     tileL[MT]        cycles the GEMM runs for row tile t (max L in tile, padded to 4)
+//     tileOff[MT]      word offset of tile t's planes inside Ap
+//     Ap               bit planes of A: for tile t, words [KB][tileL[t]][BM]
+//     SA               sign planes of A (unipolar): [MT][KB][BM]
+//   per batch entry of B (1 if B is broadcast, else batch entries):
+//     Bp               bit planes of B: [NT][KB][LBS][BN]
+//     SB               sign planes of B (unipolar): [NT][KB][BN]
+//     RB               prefix marginals RB[j][L] = sum_d sum_{l<L} zB, L = 0..L_max
+//
+// A "bit plane" word packs 32 consecutive inner-dimension elements d = 32*kb .. 32*kb+31
+// of one row at one cycle l: bit t = z[row][32*kb + t][l].
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/scgemm.h"
+
+namespace scg {
+
+constexpr int BM = 128;          // rows of A per GEMM tile
+constexpr int BN = 128;          // rows of B per GEMM tile
+constexpr int LSTEP = 4;         // GEMM cycle loop granularity (tile lengths padded to it)
+constexpr int LCH = 32;          // cycles per LDS stage and per plane-generation block
+constexpr uint32_t STATUS_BAD_LENGTH = 1u;
+
+__host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+struct Layout {
+    int KB;            // words per cycle per row = ceil(K/32)
+    int MT, NT;        // row tiles of A and B
+    int LBS;           // cycle stride of B planes and length of draw arrays (L_max rounded to LCH)
+    int LP;            // L_max rounded up to LSTEP
+    int nbB;           // batch entries of B planes (1 when B is broadcast)
+    size_t off_rA, off_rB, off_status;
+    size_t off_perm, off_Ls, off_RA, off_tileL, off_tileOff, off_Ap, off_SA;
+    size_t stride_batchA;          // bytes per A batch entry block
+    size_t off_Bp, off_SB, off_RB;
+    size_t stride_batchB;          // bytes per B batch entry block
+    size_t total;
+};
+
+// Host-side layout computation (no HIP calls).  Returns false on overflow.
+bool make_layout(const sc_gemm_desc &d, Layout *lay);
+
+// Kernel launchers (sc_kernels.hip).  All return hipSuccess or the launch error.
+hipError_t launch_draws(uint64_t seed, int n, uint32_t *rA, uint32_t *rB, uint8_t *bytes_out,
+                        int op_only, uint32_t *status, hipStream_t st);
+hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L,
+                           uint8_t *ws, hipStream_t st);
+hipError_t launch_marginals(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,
+                            const int8_t *B, uint8_t *ws, hipStream_t st);
+hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,
+                         const int8_t *B, uint8_t *ws, hipStream_t st);
+hipError_t launch_gemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
+                       float *out, int32_t *counts, uint8_t *ws, hipStream_t st);
+
+}  // namespace scg

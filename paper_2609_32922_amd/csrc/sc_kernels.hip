@@ -1,0 +1,620 @@
+// HIP kernels of libscgemm for gfx950 (MI355X): emulated stochastic-computing GEMM.
+//
+// Pipeline of one sc_gemm call (all on the caller's stream):
+//   k_draws      comparator sequences r^A, r^B (Sec. 3.1 "Bitstream generation",
+//                LFSR of Sec. A.1) -- one lane per cycle via LFSR jump-ahead
+//   k_schedule   per-row length scheduler: validates L_i, counting-sorts rows by L
+//                (descending) so that a 128-row tile runs for the longest length it
+//                holds (Sec. 4.2: "row i stops at l_i"; Sec. 4.1 cost ~ sum of l_i)
+//   k_marginals  bipolar only: RA_i = sum_d sum_{l<L_i} zA and RB_j(L) for all L
+//   k_planes     comparator stream generation into packed bit planes (one word =
+//                32 inner-dimension elements at one cycle); 64 lanes compare one
+//                row's 64 elements against r_l in one v_cmp, the wave ballot is the
+//                packed word
+//   k_gemm       tiled AND/bitop3 + popcount over (d, l), int32 accumulators, and the
+//                Eq. (1) decode epilogue in the original row order
+//
+// Bipolar XNOR counts use the bitwise identity XNOR(a,b) = 1 - a - b + 2ab summed
+// over the valid cycles, X_ij = K L_i - RA_i - RB_j(L_i) + 2 AND_ij, so the hot loop
+// is one AND and one popcount per 32 bit pairs and A's planes can be zero beyond L_i.
+// Unipolar sign-magnitude counts use popc((a & b) ^ sigma) with sigma = signA ^ signB
+// per 32 elements, which equals the signed AND count plus popc(sigma) per cycle.
+#include "sc_internal.h"
+
+namespace scg {
+
+// ----------------------------------------------------------------------------
+// comparator sequence
+// ----------------------------------------------------------------------------
+constexpr uint32_t kFeedback = 0x80200003u;   // x^32+x^22+x^2+x+1, Galois right-shift taps
+constexpr uint32_t kPolyLow = 0x00400007u;    // the same polynomial minus x^32
+
+constexpr uint32_t lfsr_step_ce(uint32_t s) { return (s >> 1) ^ ((s & 1u) ? kFeedback : 0u); }
+
+// kJump.v[l] is the register state after 8*l steps from state 1.  A right-shift step
+// multiplies the state polynomial by x^{-1} modulo p(x), so the state after 8*l steps
+// from S_0 is S_0 * kJump.v[l] mod p(x): every cycle's draw is computed independently.
+struct JumpTable {
+    uint32_t v[SC_L_MAX_LIMIT];
+};
+constexpr JumpTable make_jump_table() {
+    JumpTable t{};
+    uint32_t s = 1u;
+    for (int l = 0; l < SC_L_MAX_LIMIT; ++l) {
+        t.v[l] = s;
+        for (int k = 0; k < 8; ++k) s = lfsr_step_ce(s);
+    }
+    return t;
+}
+__constant__ JumpTable kJump = make_jump_table();
+
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+    uint64_t z = x + 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// Product of two polynomials of degree < 32 modulo p(x), Horner from the top bit.
+__device__ __forceinline__ uint32_t gf2_mulmod(uint32_t a, uint32_t b) {
+    uint32_t acc = 0;
+#pragma unroll
+    for (int k = 31; k >= 0; --k) {
+        acc = (acc << 1) ^ ((acc >> 31) ? kPolyLow : 0u);
+        acc ^= ((a >> k) & 1u) ? b : 0u;
+    }
+    return acc;
+}
+
+__global__ __launch_bounds__(256) void k_draws(uint64_t seed, int n, uint32_t *rA, uint32_t *rB,
+                                               uint8_t *bytes_out, int op_only, uint32_t *status) {
+    const int l = blockIdx.x * blockDim.x + threadIdx.x;
+    const int op = op_only >= 0 ? op_only : (int)blockIdx.y;
+    if (status != nullptr && l == 0 && blockIdx.y == 0) *status = 0u;
+    if (l >= n) return;
+    uint32_t s0 = (uint32_t)(splitmix64(2ull * seed + (uint64_t)op) >> 32);
+    if (s0 == 0u) s0 = 1u;
+    uint32_t s = gf2_mulmod(s0, kJump.v[l]);
+    uint32_t v = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        v = (v << 1) | (s & 1u);
+        s = (s >> 1) ^ ((s & 1u) ? kFeedback : 0u);
+    }
+    if (bytes_out != nullptr)
+        bytes_out[l] = (uint8_t)v;
+    else
+        (op == 0 ? rA : rB)[l] = v;
+}
+
+hipError_t launch_draws(uint64_t seed, int n, uint32_t *rA, uint32_t *rB, uint8_t *bytes_out,
+                        int op_only, uint32_t *status, hipStream_t st) {
+    dim3 grid((unsigned)((n + 255) / 256), op_only >= 0 ? 1u : 2u);
+    hipLaunchKernelGGL(k_draws, grid, dim3(256), 0, st, seed, n, rA, rB, bytes_out, op_only, status);
+    return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+// helpers
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ int beta_bipolar(int q) { return (256 * (q + 127) + 127) / 254; }
+__device__ __forceinline__ int beta_unipolar(int q) {
+    const int a = q < 0 ? -q : q;
+    return (256 * a + 63) / 127;
+}
+
+__device__ __forceinline__ int wave_uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// v_writelane_b32 through the compiler intrinsic (not inline asm), so that the backend
+// sees the instruction and inserts the wait states it needs after the v_cmp that
+// produced the lane value in VCC.
+__device__ int writelane_i32(int value, int lane, int old) __asm("llvm.amdgcn.writelane.i32");
+
+// Inclusive scan across a 64-lane wave.
+__device__ __forceinline__ int64_t wave_incl_scan(int64_t v, int lane) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int64_t t = __shfl_up(v, o, 64);
+        if (lane >= o) v += t;
+    }
+    return v;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Exclusive scan over a 1024-thread block; returns the block total in *total.
+__device__ int64_t block_excl_scan_1024(int64_t v, int64_t *total) {
+    __shared__ int64_t wsum[16];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int64_t inc = wave_incl_scan(v, lane);
+    if (lane == 63) wsum[w] = inc;
+    __syncthreads();
+    if (w == 0) {
+        int64_t x = lane < 16 ? wsum[lane] : 0;
+        x = wave_incl_scan(x, lane);
+        if (lane < 16) wsum[lane] = x;
+    }
+    __syncthreads();
+    const int64_t base = w > 0 ? wsum[w - 1] : 0;
+    *total = wsum[15];
+    __syncthreads();
+    return base + inc - v;
+}
+
+// acc += popcount(x) as one v_bcnt_u32_b32 with the accumulator as second source.
+// Written out so that unrolled chains keep this one-instruction form instead of
+// being reassociated into separate popcounts and three-input adds.
+__device__ __forceinline__ void popc_acc(int32_t &acc, uint32_t x) {
+    asm("v_bcnt_u32_b32 %0, %1, %0" : "+v"(acc) : "v"(x));
+}
+
+template <typename T>
+__device__ __forceinline__ T *ws_ptr(uint8_t *ws, size_t off) {
+    return reinterpret_cast<T *>(ws + off);
+}
+
+// ----------------------------------------------------------------------------
+// per-row length scheduler (one 1024-thread block per batch entry)
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L, int64_t strideL,
+                                                   int M, int L_max, Layout lay, uint8_t *ws) {
+    __shared__ int hist[SC_L_MAX_LIMIT + 1];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    uint8_t *wsb = ws + (size_t)b * lay.stride_batchA;
+    int32_t *perm = ws_ptr<int32_t>(wsb, lay.off_perm);
+    int32_t *Ls = ws_ptr<int32_t>(wsb, lay.off_Ls);
+    int32_t *tileL = ws_ptr<int32_t>(wsb, lay.off_tileL);
+    int64_t *tileOff = ws_ptr<int64_t>(wsb, lay.off_tileOff);
+    uint32_t *status = ws_ptr<uint32_t>(ws, lay.off_status);
+    const int32_t *Lb = L + (size_t)b * strideL;
+
+    for (int v = tid; v <= L_max; v += 1024) hist[v] = 0;
+    __syncthreads();
+    for (int i = tid; i < M; i += 1024) {
+        int l = Lb[i];
+        if (l < 0 || l > L_max) {
+            atomicOr(status, STATUS_BAD_LENGTH);
+            l = 0;
+        }
+        atomicAdd(&hist[l], 1);
+    }
+    __syncthreads();
+    // start position of each length bucket, longest lengths first
+    int64_t carry = 0;
+    for (int c = 0; c <= L_max; c += 1024) {
+        const int idx = L_max - (c + tid);
+        const int64_t v = idx >= 0 ? hist[idx] : 0;
+        int64_t tot;
+        const int64_t ex = block_excl_scan_1024(v, &tot);
+        if (idx >= 0) hist[idx] = (int)(carry + ex);
+        carry += tot;
+        __syncthreads();
+    }
+    for (int i = tid; i < M; i += 1024) {
+        int l = Lb[i];
+        if (l < 0 || l > L_max) l = 0;
+        const int pos = atomicAdd(&hist[l], 1);
+        perm[pos] = i;
+        Ls[pos] = l;
+    }
+    for (int p = M + tid; p < lay.MT * BM; p += 1024) {
+        perm[p] = -1;
+        Ls[p] = 0;
+    }
+    __threadfence_block();
+    __syncthreads();
+    // tile lengths (first sorted row of a tile holds its longest length) and offsets
+    carry = 0;
+    for (int c = 0; c < lay.MT; c += 1024) {
+        const int t = c + tid;
+        int tl = 0;
+        if (t < lay.MT) {
+            tl = (int)round_up(Ls[(size_t)t * BM], LSTEP);
+            tileL[t] = tl;
+        }
+        int64_t tot;
+        const int64_t ex = block_excl_scan_1024((int64_t)tl * lay.KB * BM, &tot);
+        if (t < lay.MT) tileOff[t] = carry + ex;
+        carry += tot;
+    }
+}
+
+hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L, uint8_t *ws,
+                           hipStream_t st) {
+    hipLaunchKernelGGL(k_schedule, dim3((unsigned)d.batch), dim3(1024), 0, st, L, d.strideL, d.M,
+                       d.L_max, lay, ws);
+    return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+// marginals for the bipolar identity (one wave per row; 4 waves per block)
+//   G[v] = #{d : beta_d > v}; the row's ones at cycle l are G[r_l].
+// ----------------------------------------------------------------------------
+__device__ void row_level_tail_counts(const int8_t *__restrict__ x, int K, int *hist, int lane) {
+    // hist has 260 entries; on return hist[v] = #{d : beta(x_d) > v} for v in [0, 255]
+    for (int v = lane; v < 260; v += 64) hist[v] = 0;
+    __syncthreads();
+    for (int dd = lane; dd < K; dd += 64) atomicAdd(&hist[beta_bipolar(x[dd])], 1);
+    __syncthreads();
+    // inclusive prefix over levels 0..255 (lane owns 4 consecutive levels)
+    const int h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2];
+    const int h3 = hist[4 * lane + 3];
+    const int own = h0 + h1 + h2 + h3;
+    const int before = (int)wave_incl_scan(own, lane) - own;
+    __syncthreads();
+    // G[v] = K - #{beta <= v}
+    hist[4 * lane] = K - (before + h0);
+    hist[4 * lane + 1] = K - (before + h0 + h1);
+    hist[4 * lane + 2] = K - (before + h0 + h1 + h2);
+    hist[4 * lane + 3] = K - (before + own);
+    __syncthreads();
+}
+
+// one 64-thread block per sorted row position of A
+__global__ __launch_bounds__(64) void k_marginals_A(const int8_t *__restrict__ A, int64_t lda,
+                                                    int64_t strideA, int K, Layout lay, uint8_t *ws) {
+    __shared__ int hist[260];
+    const int lane = threadIdx.x;
+    const int p = blockIdx.x, b = blockIdx.y;
+    uint8_t *wsb = ws + (size_t)b * lay.stride_batchA;
+    const int32_t *perm = ws_ptr<int32_t>(wsb, lay.off_perm);
+    const int32_t *Ls = ws_ptr<int32_t>(wsb, lay.off_Ls);
+    int32_t *RA = ws_ptr<int32_t>(wsb, lay.off_RA);
+    const uint32_t *rA = ws_ptr<uint32_t>(ws, lay.off_rA);
+    const int i = perm[p];
+    const int Li = Ls[p];
+    if (i < 0 || Li == 0) {
+        if (lane == 0) RA[p] = 0;
+        return;
+    }
+    row_level_tail_counts(A + (size_t)b * strideA + (size_t)i * lda, K, hist, lane);
+    int s = 0;
+    for (int l = lane; l < Li; l += 64) s += hist[rA[l]];
+    s = wave_sum(s);
+    if (lane == 0) RA[p] = s;
+}
+
+// one 64-thread block per row of B: RB[j][L] for L = 0..L_max
+__global__ __launch_bounds__(64) void k_marginals_B(const int8_t *__restrict__ B, int64_t ldb,
+                                                    int64_t strideB, int K, int L_max, Layout lay,
+                                                    uint8_t *ws) {
+    __shared__ int hist[260];
+    const int lane = threadIdx.x;
+    const int j = blockIdx.x, b = blockIdx.y;
+    uint8_t *wsb = ws + (size_t)b * lay.stride_batchB;
+    int32_t *RB = ws_ptr<int32_t>(wsb, lay.off_RB) + (size_t)j * (L_max + 1);
+    const uint32_t *rB = ws_ptr<uint32_t>(ws, lay.off_rB);
+    row_level_tail_counts(B + (size_t)b * strideB + (size_t)j * ldb, K, hist, lane);
+    int64_t carry = 0;
+    if (lane == 0) RB[0] = 0;
+    for (int l0 = 0; l0 < L_max; l0 += 64) {
+        const int l = l0 + lane;
+        const int64_t v = l < L_max ? hist[rB[l]] : 0;
+        const int64_t inc = wave_incl_scan(v, lane);
+        if (l < L_max) RB[l + 1] = (int32_t)(carry + inc);
+        carry += __shfl(inc, 63, 64);
+    }
+}
+
+hipError_t launch_marginals(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
+                            uint8_t *ws, hipStream_t st) {
+    const int rowsA = lay.MT * BM;
+    hipLaunchKernelGGL(k_marginals_A, dim3((unsigned)rowsA, (unsigned)d.batch), dim3(64), 0, st, A,
+                       d.lda, d.strideA, d.K, lay, ws);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_marginals_B, dim3((unsigned)d.N, (unsigned)lay.nbB), dim3(64), 0, st, B,
+                       d.ldb, d.strideB, d.K, d.L_max, lay, ws);
+    return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+// stream generation into bit planes
+// ----------------------------------------------------------------------------
+struct PlaneArgs {
+    const int8_t *X;
+    int64_t ld, strideX;        // row stride, batch stride (elements)
+    int rows, K, KB;
+    int nchunk;                 // cycle blocks of LCH per tile in the grid
+    int uniformL;               // cycles of every row when lengths are not per row
+    int tile_rows;              // BM or BN (128)
+    size_t stride_batch;        // bytes between batch entries of the workspace block
+    size_t off_perm, off_Ls, off_tileL, off_tileOff;   // 0 = not used (B side)
+    size_t off_planes, off_signs, off_r;
+    int per_row;                // 1: A side (sorted rows, per-row lengths)
+    int LBS;                    // B side: cycle stride of the planes
+};
+
+template <int POL>
+__global__ __launch_bounds__(256) void k_planes(PlaneArgs a, uint8_t *ws) {
+    __shared__ uint32_t T[2][LCH][BM + 1];
+    const int t = blockIdx.x / a.nchunk, ch = blockIdx.x % a.nchunk;
+    const int dp = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_uniform(tid >> 6);
+    uint8_t *wsb = ws + (size_t)b * a.stride_batch;
+    const uint32_t *r = ws_ptr<uint32_t>(ws, a.off_r);
+
+    int Lloop;
+    int64_t off;
+    const int32_t *perm = nullptr, *Ls = nullptr;
+    if (a.per_row) {
+        Lloop = ws_ptr<int32_t>(wsb, a.off_tileL)[t];
+        off = ws_ptr<int64_t>(wsb, a.off_tileOff)[t];
+        perm = ws_ptr<int32_t>(wsb, a.off_perm);
+        Ls = ws_ptr<int32_t>(wsb, a.off_Ls);
+    } else {
+        Lloop = a.LBS;
+        off = (int64_t)t * a.KB * a.LBS * BN;
+    }
+    const int l0 = ch * LCH;
+    if (l0 >= Lloop) return;
+    const int nl = min(LCH, Lloop - l0);
+    uint32_t *planes = ws_ptr<uint32_t>(wsb, a.off_planes) + off;
+    uint32_t *signs = POL == SC_UNIPOLAR_AND_SM ? ws_ptr<uint32_t>(wsb, a.off_signs) : nullptr;
+    const int8_t *Xb = a.X + (size_t)b * a.strideX;
+    const int d = dp * 64 + lane;
+    // the chunk's 32 comparator draws, loaded once (l0 + 31 < LBS, the draw count)
+    int rr[LCH];
+#pragma unroll
+    for (int l = 0; l < LCH; ++l) rr[l] = wave_uniform((int)r[l0 + l]);
+
+    for (int k = 0; k < 32; ++k) {
+        const int m = w * 32 + k;
+        const int p = t * 128 + m;
+        int row, Lr;
+        if (a.per_row) {
+            row = wave_uniform(perm[p]);
+            Lr = row >= 0 ? wave_uniform(Ls[p]) : 0;
+        } else {
+            row = p < a.rows ? p : -1;
+            Lr = row >= 0 ? a.uniformL : 0;
+        }
+        const bool valid = row >= 0 && d < a.K;
+        const int q = valid ? (int)Xb[(size_t)row * a.ld + d] : 0;
+        const int beta = valid ? (POL == SC_BIPOLAR_XNOR ? beta_bipolar(q) : beta_unipolar(q)) : 0;
+        const int lrem = Lr - l0;          // cycles of this row left in the chunk
+        uint32_t word = 0;
+#pragma unroll
+        for (int l = 0; l < LCH; ++l) {
+            // a cycle past the row's length compares against 256: never a one
+            const int thr = wave_uniform(l < lrem ? rr[l] : 256);
+            const uint64_t m64 = __ballot(thr < beta);
+            // lane l receives cycle l of the first 32 elements, lane 32+l of the next 32
+            word = (uint32_t)writelane_i32((int)(uint32_t)m64, l, (int)word);
+            word = (uint32_t)writelane_i32((int)(uint32_t)(m64 >> 32), l + 32, (int)word);
+        }
+        T[lane >> 5][lane & 31][m] = word;
+        if (POL == SC_UNIPOLAR_AND_SM && ch == 0) {
+            const uint64_t s64 = __ballot(valid && q < 0);
+            if (lane == 0) {
+                const size_t so = ((size_t)t * a.KB + 2 * dp) * 128 + m;
+                signs[so] = (uint32_t)s64;
+                if (2 * dp + 1 < a.KB) signs[so + 128] = (uint32_t)(s64 >> 32);
+            }
+        }
+    }
+    __syncthreads();
+    // coalesced copy-out: 2 words-per-cycle blocks x nl cycles x 128 words
+    for (int e = tid; e < 2 * LCH * 32; e += 256) {
+        const int g = e & 31, row = e >> 5;          // row = kbl * LCH + l
+        const int kbl = row / LCH, l = row % LCH;
+        const int kb = 2 * dp + kbl;
+        if (kb < a.KB && l < nl) {
+            uint4 v;
+            v.x = T[kbl][l][4 * g];
+            v.y = T[kbl][l][4 * g + 1];
+            v.z = T[kbl][l][4 * g + 2];
+            v.w = T[kbl][l][4 * g + 3];
+            uint4 *dst = reinterpret_cast<uint4 *>(planes + ((size_t)kb * Lloop + l0 + l) * 128) + g;
+            *dst = v;
+        }
+    }
+}
+
+hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
+                         uint8_t *ws, hipStream_t st) {
+    const int dpairs = (lay.KB + 1) / 2;
+    if (dpairs == 0) return hipSuccess;
+    PlaneArgs pa{};
+    pa.X = A;
+    pa.ld = d.lda;
+    pa.strideX = d.strideA;
+    pa.rows = d.M;
+    pa.K = d.K;
+    pa.KB = lay.KB;
+    pa.nchunk = (lay.LP + LCH - 1) / LCH;
+    pa.uniformL = 0;
+    pa.tile_rows = BM;
+    pa.stride_batch = lay.stride_batchA;
+    pa.off_perm = lay.off_perm;
+    pa.off_Ls = lay.off_Ls;
+    pa.off_tileL = lay.off_tileL;
+    pa.off_tileOff = lay.off_tileOff;
+    pa.off_planes = lay.off_Ap;
+    pa.off_signs = lay.off_SA;
+    pa.off_r = lay.off_rA;
+    pa.per_row = 1;
+    pa.LBS = lay.LBS;
+    dim3 gA((unsigned)(lay.MT * pa.nchunk), (unsigned)dpairs, (unsigned)d.batch);
+    if (d.polarity == SC_BIPOLAR_XNOR)
+        hipLaunchKernelGGL(k_planes<SC_BIPOLAR_XNOR>, gA, dim3(256), 0, st, pa, ws);
+    else
+        hipLaunchKernelGGL(k_planes<SC_UNIPOLAR_AND_SM>, gA, dim3(256), 0, st, pa, ws);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+
+    PlaneArgs pb = pa;
+    pb.X = B;
+    pb.ld = d.ldb;
+    pb.strideX = d.strideB;
+    pb.rows = d.N;
+    pb.nchunk = lay.LBS / LCH;
+    pb.uniformL = d.L_max;
+    pb.tile_rows = BN;
+    pb.stride_batch = lay.stride_batchB;
+    pb.off_perm = pb.off_Ls = pb.off_tileL = pb.off_tileOff = 0;
+    pb.off_planes = lay.off_Bp;
+    pb.off_signs = lay.off_SB;
+    pb.off_r = lay.off_rB;
+    pb.per_row = 0;
+    dim3 gB((unsigned)(lay.NT * pb.nchunk), (unsigned)dpairs, (unsigned)lay.nbB);
+    if (d.polarity == SC_BIPOLAR_XNOR)
+        hipLaunchKernelGGL(k_planes<SC_BIPOLAR_XNOR>, gB, dim3(256), 0, st, pb, ws);
+    else
+        hipLaunchKernelGGL(k_planes<SC_UNIPOLAR_AND_SM>, gB, dim3(256), 0, st, pb, ws);
+    return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+// packed AND/bitop3 + popcount GEMM with the Eq. (1) decode epilogue
+// ----------------------------------------------------------------------------
+struct GemmArgs {
+    int M, N, K, KB, LBS, L_max, nbB;
+    const float *sA, *sB;
+    int64_t strideSA, strideSB, strideO, ldo;
+    float *out;
+    int32_t *counts;
+};
+
+template <int POL>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs g, Layout lay, uint8_t *ws) {
+    __shared__ uint4 As[LCH * BM / 4];
+    __shared__ uint4 Bs[LCH * BN / 4];
+    const int tn = blockIdx.x, tm = blockIdx.y, b = blockIdx.z;
+    const int bB = g.nbB == 1 ? 0 : b;
+    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
+    uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
+    const int Lloop = ws_ptr<int32_t>(wsa, lay.off_tileL)[tm];
+    const int64_t offA = ws_ptr<int64_t>(wsa, lay.off_tileOff)[tm];
+    const uint32_t *Ap = ws_ptr<uint32_t>(wsa, lay.off_Ap) + offA;
+    const uint32_t *Bp = ws_ptr<uint32_t>(wsbB, lay.off_Bp);
+
+    int32_t acc[8][8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[r][c] = 0;
+
+    for (int kb = 0; kb < g.KB && Lloop > 0; ++kb) {
+        uint32_t sig[8][8];
+        if (POL == SC_UNIPOLAR_AND_SM) {
+            const uint4 *sa4 = reinterpret_cast<const uint4 *>(ws_ptr<uint32_t>(wsa, lay.off_SA) +
+                                                               ((size_t)tm * g.KB + kb) * BM);
+            const uint4 *sb4 = reinterpret_cast<const uint4 *>(ws_ptr<uint32_t>(wsbB, lay.off_SB) +
+                                                               ((size_t)tn * g.KB + kb) * BN);
+            const uint4 a0 = sa4[ty], a1 = sa4[16 + ty], b0 = sb4[tx], b1 = sb4[16 + tx];
+            const uint32_t sa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+            const uint32_t sb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+            for (int r = 0; r < 8; ++r)
+#pragma unroll
+                for (int c = 0; c < 8; ++c) {
+                    sig[r][c] = sa[r] ^ sb[c];
+                    acc[r][c] -= Lloop * __builtin_popcount(sig[r][c]);
+                }
+        }
+        const uint4 *gA = reinterpret_cast<const uint4 *>(Ap + (size_t)kb * Lloop * BM);
+        const uint4 *gB = reinterpret_cast<const uint4 *>(Bp + ((size_t)tn * g.KB + kb) * g.LBS * BN);
+        for (int l0 = 0; l0 < Lloop; l0 += LCH) {
+            const int nl = min(LCH, Lloop - l0);
+            __syncthreads();
+            for (int e = tid; e < nl * 32; e += 256) {
+                As[e] = gA[l0 * 32 + e];
+                Bs[e] = gB[l0 * 32 + e];
+            }
+            __syncthreads();
+            for (int l = 0; l < nl; l += LSTEP) {
+#pragma unroll
+                for (int u = 0; u < LSTEP; ++u) {
+                    const uint4 a0 = As[(l + u) * 32 + ty], a1 = As[(l + u) * 32 + 16 + ty];
+                    const uint4 b0 = Bs[(l + u) * 32 + tx], b1 = Bs[(l + u) * 32 + 16 + tx];
+                    const uint32_t av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+                    const uint32_t bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+                    for (int r = 0; r < 8; ++r)
+#pragma unroll
+                        for (int c = 0; c < 8; ++c) {
+                            if (POL == SC_UNIPOLAR_AND_SM)
+                                popc_acc(acc[r][c], (av[r] & bv[c]) ^ sig[r][c]);
+                            else
+                                popc_acc(acc[r][c], av[r] & bv[c]);
+                        }
+                }
+            }
+        }
+    }
+
+    // epilogue: counts and Eq. (1) decode, written in the original row order
+    const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm);
+    const int32_t *Ls = ws_ptr<int32_t>(wsa, lay.off_Ls);
+    const int32_t *RA = ws_ptr<int32_t>(wsa, lay.off_RA);
+    const int32_t *RB = ws_ptr<int32_t>(wsbB, lay.off_RB);
+    const float *sAb = g.sA + (size_t)b * g.strideSA;
+    const float *sBb = g.sB + (size_t)b * g.strideSB;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+        const int rl = r < 4 ? 4 * ty + r : 64 + 4 * ty + (r - 4);
+        const int p = tm * BM + rl;
+        const int i = perm[p];
+        if (i < 0) continue;
+        const int Li = Ls[p];
+        const int ra = POL == SC_BIPOLAR_XNOR ? RA[p] : 0;
+        const float sa = sAb[i];
+        float *orow = g.out + (size_t)b * g.strideO + (size_t)i * g.ldo;
+        int32_t *crow = g.counts ? g.counts + (size_t)b * g.strideO + (size_t)i * g.ldo : nullptr;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const int cl = c < 4 ? 4 * tx + c : 64 + 4 * tx + (c - 4);
+            const int j = tn * BN + cl;
+            if (j >= g.N) continue;
+            int32_t cnt, num;
+            if (POL == SC_BIPOLAR_XNOR) {
+                const int rb = RB[(size_t)j * (g.L_max + 1) + Li];
+                const int KL = g.K * Li;
+                cnt = KL - ra - rb + 2 * acc[r][c];
+                num = 2 * cnt - KL;
+            } else {
+                cnt = acc[r][c];
+                num = cnt;
+            }
+            float o = 0.0f;
+            if (Li > 0) o = (float)num / (float)Li * (sa * sBb[j] * 16129.0f);
+            else cnt = 0;
+            orow[j] = o;
+            if (crow) crow[j] = cnt;
+        }
+    }
+}
+
+hipError_t launch_gemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
+                       float *out, int32_t *counts, uint8_t *ws, hipStream_t st) {
+    GemmArgs g{};
+    g.M = d.M;
+    g.N = d.N;
+    g.K = d.K;
+    g.KB = lay.KB;
+    g.LBS = lay.LBS;
+    g.L_max = d.L_max;
+    g.nbB = lay.nbB;
+    g.sA = sA;
+    g.sB = sB;
+    g.strideSA = d.strideSA;
+    g.strideSB = d.strideSB;
+    g.strideO = d.strideO;
+    g.ldo = d.ldo;
+    g.out = out;
+    g.counts = counts;
+    dim3 grid((unsigned)lay.NT, (unsigned)lay.MT, (unsigned)d.batch);
+    if (d.polarity == SC_BIPOLAR_XNOR)
+        hipLaunchKernelGGL(k_gemm<SC_BIPOLAR_XNOR>, grid, dim3(256), 0, st, g, lay, ws);
+    else
+        hipLaunchKernelGGL(k_gemm<SC_UNIPOLAR_AND_SM>, grid, dim3(256), 0, st, g, lay, ws);
+    return hipGetLastError();
+}
+
+}  // namespace scg

@@ -1,0 +1,198 @@
+"""GPU parity: the HIP library against the CPU oracle, through the C ABI.
+
+Counts must agree bit for bit; decoded floats within 1e-6 relative (exact zeros on
+both sides).  The 1e-6 bound follows from the decode arithmetic: the integer
+numerator (2X - K L or S) is exact, then one fp32 division by L and two fp32
+products with the scales, i.e. at most four roundings of 2^-24 each (< 2.4e-7).
+
+Small cases span several 128x128 tiles with ragged tails and run the oracle on every
+output; the five full-size workloads (the launch configuration the benchmark times)
+are checked on sampled rows x columns, plus whole-matrix properties.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+REL_TOL = 1e-6
+
+
+def _note(msg):
+    print("[gpu-case] " + msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_32922_amd as scg
+    scg.load()
+    return torch.device("cuda:0")
+
+
+def _to_dev(g, dev):
+    import torch
+    return (torch.from_numpy(np.ascontiguousarray(g.A)).to(dev),
+            torch.from_numpy(np.ascontiguousarray(g.sA)).to(dev),
+            torch.from_numpy(np.ascontiguousarray(g.B)).to(dev),
+            torch.from_numpy(np.ascontiguousarray(g.sB)).to(dev),
+            torch.from_numpy(np.ascontiguousarray(g.L)).to(dev))
+
+
+def _run(g, dev, check_status=True):
+    import torch
+    import paper_2609_32922_amd as scg
+    A, sA, B, sB, L = _to_dev(g, dev)
+    out, cnt = scg.gemm(A, sA, B, sB, L, L_max=g.L_max, polarity=g.polarity, seed=g.seed,
+                        want_counts=True, check_status=check_status)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), cnt.cpu().numpy()
+
+
+def _compare(g, b, rows, cols, out, cnt, oracle_mod, tag):
+    bB = 0 if g.B.shape[0] == 1 else b
+    c_ref, o_ref = oracle_mod.sc_gemm(g.A[b][rows], g.B[bB][cols], g.sA[b][rows], g.sB[bB][cols],
+                                      g.L[b][rows], g.L_max, g.polarity, g.seed)
+    c_gpu = cnt[b][np.ix_(rows, cols)]
+    o_gpu = out[b][np.ix_(rows, cols)].astype(np.float64)
+    bad = np.argwhere(c_gpu != c_ref)
+    assert bad.size == 0, "%s: %d count mismatches, first at %s: gpu %d oracle %d" % (
+        tag, len(bad), bad[0], c_gpu[tuple(bad[0])], c_ref[tuple(bad[0])])
+    zero = o_ref == 0.0
+    assert np.all(o_gpu[zero] == 0.0), tag + ": expected exact zeros"
+    rel = np.abs(o_gpu[~zero] - o_ref[~zero]) / np.abs(o_ref[~zero])
+    assert rel.size == 0 or rel.max() <= REL_TOL, "%s: max rel err %.3g" % (tag, rel.max())
+
+
+def test_comparator_sequence_matches_oracle(dev, oracle_mod):
+    import paper_2609_32922_amd as scg
+    for seed in (0, 1, 2, 3, 4, 2**63 + 12345):
+        for op in (0, 1):
+            _note("comparator seed=%d op=%d" % (seed, op))
+            r = scg.comparator_sequence(seed, op, 4096).cpu().numpy()
+            assert np.array_equal(r, oracle_mod.comparator_sequence(seed, op, 4096))
+
+
+def test_bipolar_64x256x64_full(dev, oracle_mod):
+    g = W.bipolar_64x256x64().gemms[0]
+    _note("bipolar_64x256x64 full")
+    out, cnt = _run(g, dev)
+    _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "64x256x64")
+
+
+FUZZ = [
+    # batch, M, N, K, L_max, L_lo, polarity, broadcast_B, seed
+    (1, 1, 1, 1, 1, 0, 0, False, 3),
+    (1, 129, 130, 33, 70, 0, 0, False, 5),
+    (1, 300, 257, 100, 257, 0, 0, False, 7),
+    (1, 257, 129, 64, 64, 64, 0, False, 9),
+    (2, 140, 131, 96, 40, 0, 0, False, 11),
+    (3, 70, 200, 31, 100, 1, 0, True, 13),
+    (1, 129, 130, 33, 70, 0, 1, False, 15),
+    (1, 300, 257, 100, 193, 0, 1, False, 17),
+    (2, 140, 131, 65, 48, 0, 1, True, 19),
+    (1, 64, 64, 1000, 24, 0, 1, False, 21),
+    (1, 200, 150, 7, 512, 400, 0, False, 23),
+]
+
+
+@pytest.mark.parametrize("case", FUZZ, ids=[str(c) for c in FUZZ])
+def test_fuzz_full_compare(dev, oracle_mod, case):
+    batch, M, N, K, L_max, L_lo, pol, bcast, seed = case
+    rng = np.random.default_rng(seed)
+    g = W.random_gemm(rng, batch, M, N, K, L_max, pol, seed, L_lo=L_lo, broadcast_B=bcast)
+    _note("fuzz %s" % (case,))
+    out, cnt = _run(g, dev)
+    for b in range(batch):
+        _compare(g, b, np.arange(M), np.arange(N), out, cnt, oracle_mod, "fuzz%s b%d" % (case, b))
+
+
+def test_zero_lengths_and_K0(dev, oracle_mod):
+    rng = np.random.default_rng(31)
+    g = W.random_gemm(rng, 1, 150, 140, 40, 64, 0, 31)
+    g.L[0, ::3] = 0
+    _note("zero lengths")
+    out, cnt = _run(g, dev)
+    assert np.all(cnt[0, ::3] == 0) and np.all(out[0, ::3] == 0)
+    _compare(g, 0, np.arange(150), np.arange(140), out, cnt, oracle_mod, "zeroL")
+    for pol in (0, 1):
+        g0 = W.random_gemm(rng, 1, 10, 12, 0, 16, pol, 5)
+        _note("K=0 polarity %d" % pol)
+        out, cnt = _run(g0, dev)
+        assert np.all(cnt == 0) and np.all(out == 0)
+
+
+def test_out_of_range_lengths_set_status(dev):
+    import paper_2609_32922_amd as scg
+    rng = np.random.default_rng(41)
+    g = W.random_gemm(rng, 1, 50, 20, 16, 32, 0, 41)
+    g.L[0, 3] = 33
+    g.L[0, 7] = -1
+    _note("bad lengths")
+    with pytest.raises(scg.ScError) as ei:
+        _run(g, dev, check_status=True)
+    assert ei.value.code == scg.SC_ERR_DEVICE_STATUS
+    out, cnt = _run(g, dev, check_status=False)
+    assert np.all(cnt[0, 3] == 0) and np.all(cnt[0, 7] == 0)
+    g.L[0, 3] = 32
+    g.L[0, 7] = 0
+    _run(g, dev, check_status=True)          # a good call clears the status
+
+
+def test_deterministic_repeat(dev):
+    rng = np.random.default_rng(51)
+    g = W.random_gemm(rng, 1, 260, 300, 160, 96, 0, 51)
+    _note("determinism")
+    o1, c1 = _run(g, dev)
+    o2, c2 = _run(g, dev)
+    assert np.array_equal(c1, c2) and np.array_equal(o1.view(np.uint32), o2.view(np.uint32))
+
+
+# --------------------------------------------------------------------------
+# full-size workloads: sampled rows x columns against the oracle
+# --------------------------------------------------------------------------
+def _sample(n, rng, k):
+    base = [0, 1, n - 1, n - 2]
+    base += list(range(max(0, (n // 128) * 128 - 2), min(n, (n // 128) * 128 + 2)))
+    extra = rng.choice(n, size=min(k, n), replace=False).tolist()
+    return np.array(sorted(set(i for i in base + extra if 0 <= i < n)), dtype=np.int64)
+
+
+def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None):
+    rng = np.random.default_rng(7)
+    for g in w.gemms:
+        _note("%s/%s full size %s" % (w.name, g.name, g.A.shape))
+        out, cnt = _run(g, dev)
+        KL = g.K * g.L.astype(np.int64)
+        if g.polarity == 0:
+            assert np.all(cnt >= 0) and np.all(cnt <= KL[:, :, None])
+        else:
+            assert np.all(np.abs(cnt) <= KL[:, :, None])
+        bs = range(g.batch) if batches is None else batches
+        for b in bs:
+            rows = _sample(g.M, rng, nrows)
+            cols = _sample(g.N, rng, ncols)
+            _compare(g, b, rows, cols, out, cnt, oracle_mod, "%s/%s b%d" % (w.name, g.name, b))
+
+
+def test_workload_vitb16_fc1_L128(dev, oracle_mod):
+    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod)
+
+
+def test_workload_vitb16_fc1_mp64(dev, oracle_mod):
+    _check_workload(W.vitb16_fc1_mp64(), dev, oracle_mod)
+
+
+def test_workload_ditxl2_proj_mlp_group96(dev, oracle_mod):
+    _check_workload(W.ditxl2_proj_mlp_group96(), dev, oracle_mod)
+
+
+def test_workload_vitl14_336_qk_mlp(dev, oracle_mod):
+    _check_workload(W.vitl14_336_qk_mlp(), dev, oracle_mod, nrows=24, ncols=64,
+                    batches=None)
