@@ -34,13 +34,50 @@ def parse():
     p.add_argument("--cpu-rows", type=int, default=0,
                    help="rows of A for the oracle sample (0 = size it to ~15 s)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--traffic", default=None,
-                   help="JSON file with the measured HBM bytes per GEMM launch")
+    p.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                   help="only run a plain device copy of BYTES bytes (3 times), to calibrate "
+                        "the HBM byte counters against a kernel of known traffic")
     return p.parse_args()
+
+
+def kernel_source_digest():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2609_32922_amd", "csrc", "sc_kernels.hip")
+    with open(src, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per GEMM launch from the committed rocprofv3 counter summary, or None
+    when the summary is missing or the kernel source changed since it was taken."""
+    import glob
+    import re
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*counters*.md")):
+        with open(path) as f:
+            text = f.read()
+        m = re.search(r"^traffic_bytes_per_launch:\s*(\d+)\s+workload:\s*(\S+)\s+"
+                      r"kernel_source_sha256:\s*([0-9a-f]+)", text, re.M)
+        if m and m.group(2) == workload and m.group(3) == kernel_source_digest():
+            return int(m.group(1))
+    return None
+
+
+def copy_probe(nbytes):
+    import torch
+    x = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes, "reads": nbytes, "writes": nbytes}))
 
 
 def main():
     args = parse()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build runs the SC GEMM on a single "
               "MI355X (rows shard across GPUs with no collective; see DESIGN.md)",
@@ -100,10 +137,7 @@ def main():
                              for s in range(nsteps)]))
     g_dom = w.gemms[kidx]
     achieved = g_dom.bitops() / (gemm_ms * 1e-3)
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            traffic = json.load(f).get(args.workload)
+    traffic = measured_traffic(args.workload)
     roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_BITOPS / 1e12,
                 "unit": "Tbitop/s", "frac": achieved / PEAK_BITOPS, "traffic": traffic,
                 "kernel": "k_gemm<bipolar>" if g_dom.polarity == 0 else "k_gemm<unipolar>",
@@ -132,20 +166,23 @@ def cpu_baseline(w, rows):
     threads = min(len(os.sched_getaffinity(0)), 16)
     g = max(w.gemms, key=lambda x: x.bitops())
     b = 0
-    if rows <= 0:
-        # size the sample so the timed oracle run takes roughly 15 s
-        probe = 8
-        t = time.perf_counter()
-        oracle.sc_gemm(g.A[b][:probe], g.B[0 if g.B.shape[0] == 1 else b], g.sA[b][:probe],
-                       g.sB[0 if g.B.shape[0] == 1 else b], g.L[b][:probe], g.L_max, g.polarity,
-                       g.seed, nthreads=threads, want_out=True)
-        dt = time.perf_counter() - t
-        rows = int(max(probe, min(g.M, probe * 15.0 / max(dt, 1e-3))))
     bB = 0 if g.B.shape[0] == 1 else b
-    t = time.perf_counter()
-    oracle.sc_gemm(g.A[b][:rows], g.B[bB], g.sA[b][:rows], g.sB[bB], g.L[b][:rows], g.L_max,
-                   g.polarity, g.seed, nthreads=threads, want_out=True)
-    dt = time.perf_counter() - t
+
+    def run(n):
+        t = time.perf_counter()
+        oracle.sc_gemm(g.A[b][:n], g.B[bB], g.sA[b][:n], g.sB[bB], g.L[b][:n], g.L_max,
+                       g.polarity, g.seed, nthreads=threads, want_out=True)
+        return time.perf_counter() - t
+
+    target = 15.0
+    if rows <= 0:
+        # size the sample so that the timed oracle run takes about 15 s: two probes give
+        # the fixed cost (B streams) and the per-row cost
+        r1, r2 = 16, 64
+        t1, t2 = run(r1), run(r2)
+        per_row = max((t2 - t1) / (r2 - r1), 1e-6)
+        rows = int(max(r2, min(g.M, (target - max(t1 - r1 * per_row, 0.0)) / per_row)))
+    dt = run(rows)
     ops = int(g.N) * int(g.K) * int(g.L[b][:rows].astype(np.int64).sum())
     return {"value": ops / dt, "unit": "stream-bit-ops/s", "cores": threads, "kind": "oracle",
             "seconds": dt,
