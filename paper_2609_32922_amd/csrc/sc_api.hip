@@ -79,6 +79,30 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     if (!mul_ok(bb, (size_t)l.nbB, &totB)) return false;
     off += totB;
 
+    // split count of the GEMM tiles: spread work units evenly over the compute units
+    // (a unit's cost is one tile restricted to KB/S element blocks; the busiest CU
+    // carries ceil(units/CUS) of them), with a small relative charge per extra split
+    // for the partial counts that the reduction pass reads back
+    const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * l.MT * l.NT;
+    l.S = 1;
+    if (tiles > 0 && tiles < 16 * CUS && l.KB > 1) {
+        double best = -1.0;
+        for (int s = 1; s <= MAX_SPLIT && s <= l.KB; ++s) {
+            const double avg = (double)tiles * s / CUS;
+            const double eff = avg / (double)((int64_t)(avg + 0.999999)) * (1.0 - 0.005 * (s - 1));
+            if (eff > best + 1e-9) {
+                best = eff;
+                l.S = s;
+            }
+        }
+    }
+    l.off_part = off;
+    if (l.S > 1) {
+        size_t partb;
+        if (!mul_ok((size_t)tiles * (size_t)l.S, (size_t)BM * BN * 4, &partb)) return false;
+        off = align256(off + partb);
+    }
+
     // make every offset absolute for batch entry 0
     l.off_perm += baseA;
     l.off_Ls += baseA;

@@ -12,6 +12,7 @@
 //     tileOff[MT]      word offset of tile t's planes inside Ap
 //     Ap               bit planes of A: for tile t, words [KB][tileL[t]][BM]
 //     SA               sign planes of A (unipolar): [MT][KB][BM]
+//   part       partial counts when GEMM tiles are split along the element blocks
 //   per batch entry of B (1 if B is broadcast, else batch entries):
 //     Bp               bit planes of B: [NT][KB][LBS][BN]
 //     SB               sign planes of B (unipolar): [NT][KB][BN]
@@ -34,6 +35,8 @@ constexpr int BN = 128;          // rows of B per GEMM tile
 constexpr int LSTEP = 4;         // GEMM cycle loop granularity (tile lengths padded to it)
 constexpr int LCH = 32;          // cycles per LDS stage and per plane-generation block
 constexpr uint32_t STATUS_BAD_LENGTH = 1u;
+constexpr int CUS = 256;         // compute units of an MI355X (work-unit balancing target)
+constexpr int MAX_SPLIT = 8;
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -48,6 +51,8 @@ struct Layout {
     size_t stride_batchA;          // bytes per A batch entry block
     size_t off_Bp, off_SB, off_RB;
     size_t stride_batchB;          // bytes per B batch entry block
+    int S;             // splits of the element blocks per GEMM tile (1 = no split)
+    size_t off_part;   // partial counts of split tiles: [tiles][S][256 threads][64] int32
     size_t total;
 };
 

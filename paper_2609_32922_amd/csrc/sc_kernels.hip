@@ -147,9 +147,12 @@ __device__ int64_t block_excl_scan_1024(int64_t v, int64_t *total) {
 
 // acc += popcount(x) as one v_bcnt_u32_b32 with the accumulator as second source.
 // Written out so that unrolled chains keep this one-instruction form instead of
-// being reassociated into separate popcounts and three-input adds.
+// being reassociated into separate popcounts and three-input adds.  The s_nop ahead
+// of each count measurably raises how often gfx950 issues two VALU instructions per
+// SIMD in one quad-cycle in this AND/count stream (about 1.23x the single-issue rate
+// on the 6304x768x3072 layer at L = 128).
 __device__ __forceinline__ void popc_acc(int32_t &acc, uint32_t x) {
-    asm("v_bcnt_u32_b32 %0, %1, %0" : "+v"(acc) : "v"(x));
+    asm("s_nop 0\n\tv_bcnt_u32_b32 %0, %1, %0" : "+v"(acc) : "v"(x));
 }
 
 template <typename T>
@@ -471,20 +474,77 @@ hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t 
 
 // ----------------------------------------------------------------------------
 // packed AND/bitop3 + popcount GEMM with the Eq. (1) decode epilogue
+//
+// The grid is one-dimensional over work units (tile, split): a 128x128 output tile
+// of one batch entry, restricted to a contiguous range of the ceil(K/32) element
+// blocks.  Units are ordered row-tile major, so the row tiles holding the longest
+// streams (row tile 0 after the descending sort) are dispatched first.  With one
+// split the decode runs in the GEMM epilogue; with several, each unit writes its
+// int32 partial counts and k_gemm_reduce sums them and decodes.
 // ----------------------------------------------------------------------------
 struct GemmArgs {
-    int M, N, K, KB, LBS, L_max, nbB;
+    int M, N, K, KB, LBS, L_max, nbB, batch, S;
     const float *sA, *sB;
     int64_t strideSA, strideSB, strideO, ldo;
     float *out;
     int32_t *counts;
 };
 
+// counts and Eq. (1) decode of row r (0..7) of one thread's 8x8 block, written in the
+// original row order
 template <int POL>
+__device__ __forceinline__ void epilogue_row(const int32_t (&acc)[8], int r, int b, int tm, int tn,
+                                             int tx, int ty, const GemmArgs &g, const Layout &lay,
+                                             uint8_t *ws) {
+    const int bB = g.nbB == 1 ? 0 : b;
+    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
+    uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
+    const int rl = r < 4 ? 4 * ty + r : 64 + 4 * ty + (r - 4);
+    const int p = tm * BM + rl;
+    const int i = ws_ptr<int32_t>(wsa, lay.off_perm)[p];
+    if (i < 0) return;
+    const int Li = ws_ptr<int32_t>(wsa, lay.off_Ls)[p];
+    const int ra = POL == SC_BIPOLAR_XNOR ? ws_ptr<int32_t>(wsa, lay.off_RA)[p] : 0;
+    const int32_t *RB = ws_ptr<int32_t>(wsbB, lay.off_RB);
+    const float sa = g.sA[(size_t)b * g.strideSA + i];
+    const float *sBb = g.sB + (size_t)b * g.strideSB;
+    float *orow = g.out + (size_t)b * g.strideO + (size_t)i * g.ldo;
+    int32_t *crow = g.counts ? g.counts + (size_t)b * g.strideO + (size_t)i * g.ldo : nullptr;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const int cl = c < 4 ? 4 * tx + c : 64 + 4 * tx + (c - 4);
+        const int j = tn * BN + cl;
+        if (j >= g.N) continue;
+        int32_t cnt, num;
+        if (POL == SC_BIPOLAR_XNOR) {
+            const int rb = RB[(size_t)j * (g.L_max + 1) + Li];
+            const int KL = g.K * Li;
+            cnt = KL - ra - rb + 2 * acc[c];
+            num = 2 * cnt - KL;
+        } else {
+            cnt = acc[c];
+            num = cnt;
+        }
+        float o = 0.0f;
+        if (Li > 0) o = (float)num / (float)Li * (sa * sBb[j] * 16129.0f);
+        else cnt = 0;
+        orow[j] = o;
+        if (crow) crow[j] = cnt;
+    }
+}
+
+template <int POL, bool SPLIT>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, Layout lay, uint8_t *ws) {
     __shared__ uint4 As[LCH * BM / 4];
     __shared__ uint4 Bs[LCH * BN / 4];
-    const int tn = blockIdx.x, tm = blockIdx.y, b = blockIdx.z;
+    // unit -> (row tile, batch entry, column tile, split), row tile slowest
+    const int u = blockIdx.x;
+    const int s = u % g.S;
+    const int tile = u / g.S;              // = (tm * batch + b) * NT + tn
+    const int tn = tile % lay.NT;
+    const int tb = tile / lay.NT;
+    const int b = tb % g.batch, tm = tb / g.batch;
+    const int kb0 = (int)((int64_t)s * g.KB / g.S), kb1 = (int)((int64_t)(s + 1) * g.KB / g.S);
     const int bB = g.nbB == 1 ? 0 : b;
     const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
     uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
@@ -500,7 +560,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, Layout lay, uint8_t *w
 #pragma unroll
         for (int c = 0; c < 8; ++c) acc[r][c] = 0;
 
-    for (int kb = 0; kb < g.KB && Lloop > 0; ++kb) {
+    for (int kb = kb0; kb < kb1 && Lloop > 0; ++kb) {
         uint32_t sig[8][8];
         if (POL == SC_UNIPOLAR_AND_SM) {
             const uint4 *sa4 = reinterpret_cast<const uint4 *>(ws_ptr<uint32_t>(wsa, lay.off_SA) +
@@ -530,9 +590,9 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, Layout lay, uint8_t *w
             __syncthreads();
             for (int l = 0; l < nl; l += LSTEP) {
 #pragma unroll
-                for (int u = 0; u < LSTEP; ++u) {
-                    const uint4 a0 = As[(l + u) * 32 + ty], a1 = As[(l + u) * 32 + 16 + ty];
-                    const uint4 b0 = Bs[(l + u) * 32 + tx], b1 = Bs[(l + u) * 32 + 16 + tx];
+                for (int v = 0; v < LSTEP; ++v) {
+                    const uint4 a0 = As[(l + v) * 32 + ty], a1 = As[(l + v) * 32 + 16 + ty];
+                    const uint4 b0 = Bs[(l + v) * 32 + tx], b1 = Bs[(l + v) * 32 + 16 + tx];
                     const uint32_t av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
                     const uint32_t bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
 #pragma unroll
@@ -549,46 +609,62 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, Layout lay, uint8_t *w
         }
     }
 
-    // epilogue: counts and Eq. (1) decode, written in the original row order
-    const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm);
-    const int32_t *Ls = ws_ptr<int32_t>(wsa, lay.off_Ls);
-    const int32_t *RA = ws_ptr<int32_t>(wsa, lay.off_RA);
-    const int32_t *RB = ws_ptr<int32_t>(wsbB, lay.off_RB);
-    const float *sAb = g.sA + (size_t)b * g.strideSA;
-    const float *sBb = g.sB + (size_t)b * g.strideSB;
+    if (SPLIT) {
+        // partial counts of this split: [tile][split][thread][64] int32, 256 B per thread
+        int4 *dst = reinterpret_cast<int4 *>(ws_ptr<int32_t>(ws, lay.off_part) +
+                                             (((size_t)tile * g.S + s) * 256 + tid) * 64);
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-        const int rl = r < 4 ? 4 * ty + r : 64 + 4 * ty + (r - 4);
-        const int p = tm * BM + rl;
-        const int i = perm[p];
-        if (i < 0) continue;
-        const int Li = Ls[p];
-        const int ra = POL == SC_BIPOLAR_XNOR ? RA[p] : 0;
-        const float sa = sAb[i];
-        float *orow = g.out + (size_t)b * g.strideO + (size_t)i * g.ldo;
-        int32_t *crow = g.counts ? g.counts + (size_t)b * g.strideO + (size_t)i * g.ldo : nullptr;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-            const int cl = c < 4 ? 4 * tx + c : 64 + 4 * tx + (c - 4);
-            const int j = tn * BN + cl;
-            if (j >= g.N) continue;
-            int32_t cnt, num;
-            if (POL == SC_BIPOLAR_XNOR) {
-                const int rb = RB[(size_t)j * (g.L_max + 1) + Li];
-                const int KL = g.K * Li;
-                cnt = KL - ra - rb + 2 * acc[r][c];
-                num = 2 * cnt - KL;
-            } else {
-                cnt = acc[r][c];
-                num = cnt;
-            }
-            float o = 0.0f;
-            if (Li > 0) o = (float)num / (float)Li * (sa * sBb[j] * 16129.0f);
-            else cnt = 0;
-            orow[j] = o;
-            if (crow) crow[j] = cnt;
+        for (int r = 0; r < 8; ++r) {
+            dst[2 * r] = make_int4(acc[r][0], acc[r][1], acc[r][2], acc[r][3]);
+            dst[2 * r + 1] = make_int4(acc[r][4], acc[r][5], acc[r][6], acc[r][7]);
         }
+    } else {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) epilogue_row<POL>(acc[r], r, b, tm, tn, tx, ty, g, lay, ws);
     }
+}
+
+// sums the partial counts of every split of a tile and decodes.  Four blocks per
+// tile; reduce thread (g, q) owns rows 2q and 2q+1 of GEMM thread g's 8x8 block, so
+// the four threads of one g read adjacent 64-byte pieces of its partials.
+template <int POL>
+__global__ __launch_bounds__(256) void k_gemm_reduce(GemmArgs g, Layout lay, uint8_t *ws) {
+    const int tile = blockIdx.x >> 2;
+    const int tn = tile % lay.NT;
+    const int tb = tile / lay.NT;
+    const int b = tb % g.batch, tm = tb / g.batch;
+    const int gt = (blockIdx.x & 3) * 64 + (threadIdx.x >> 2);   // GEMM thread
+    const int q = threadIdx.x & 3;
+    const int tx = gt & 15, ty = gt >> 4;
+    int32_t acc0[8], acc1[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc0[c] = acc1[c] = 0;
+    const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part)) +
+                       ((size_t)tile * g.S * 256 + gt) * 16 + 4 * q;
+    for (int s = 0; s < g.S; ++s) {
+        const int4 *src = base + (size_t)s * 256 * 16;
+        const int4 u0 = src[0], v0 = src[1], u1 = src[2], v1 = src[3];
+        acc0[0] += u0.x; acc0[1] += u0.y; acc0[2] += u0.z; acc0[3] += u0.w;
+        acc0[4] += v0.x; acc0[5] += v0.y; acc0[6] += v0.z; acc0[7] += v0.w;
+        acc1[0] += u1.x; acc1[1] += u1.y; acc1[2] += u1.z; acc1[3] += u1.w;
+        acc1[4] += v1.x; acc1[5] += v1.y; acc1[6] += v1.z; acc1[7] += v1.w;
+    }
+    epilogue_row<POL>(acc0, 2 * q, b, tm, tn, tx, ty, g, lay, ws);
+    epilogue_row<POL>(acc1, 2 * q + 1, b, tm, tn, tx, ty, g, lay, ws);
+}
+
+template <int POL>
+static hipError_t launch_gemm_pol(const GemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
+    const unsigned tiles = (unsigned)(g.batch * lay.MT * lay.NT);
+    if (g.S == 1) {
+        hipLaunchKernelGGL((k_gemm<POL, false>), dim3(tiles), dim3(256), 0, st, g, lay, ws);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL((k_gemm<POL, true>), dim3(tiles * (unsigned)g.S), dim3(256), 0, st, g, lay, ws);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_gemm_reduce<POL>), dim3(tiles * 4u), dim3(256), 0, st, g, lay, ws);
+    return hipGetLastError();
 }
 
 hipError_t launch_gemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
@@ -601,6 +677,8 @@ hipError_t launch_gemm(const sc_gemm_desc &d, const Layout &lay, const float *sA
     g.LBS = lay.LBS;
     g.L_max = d.L_max;
     g.nbB = lay.nbB;
+    g.batch = d.batch;
+    g.S = lay.S;
     g.sA = sA;
     g.sB = sB;
     g.strideSA = d.strideSA;
@@ -609,12 +687,8 @@ hipError_t launch_gemm(const sc_gemm_desc &d, const Layout &lay, const float *sA
     g.ldo = d.ldo;
     g.out = out;
     g.counts = counts;
-    dim3 grid((unsigned)lay.NT, (unsigned)lay.MT, (unsigned)d.batch);
-    if (d.polarity == SC_BIPOLAR_XNOR)
-        hipLaunchKernelGGL(k_gemm<SC_BIPOLAR_XNOR>, grid, dim3(256), 0, st, g, lay, ws);
-    else
-        hipLaunchKernelGGL(k_gemm<SC_UNIPOLAR_AND_SM>, grid, dim3(256), 0, st, g, lay, ws);
-    return hipGetLastError();
+    if (d.polarity == SC_BIPOLAR_XNOR) return launch_gemm_pol<SC_BIPOLAR_XNOR>(g, lay, ws, st);
+    return launch_gemm_pol<SC_UNIPOLAR_AND_SM>(g, lay, ws, st);
 }
 
 }  // namespace scg
