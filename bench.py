@@ -99,7 +99,7 @@ def main():
     for g in w.gemms:
         t = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (g.A, g.sA, g.B, g.sB, g.L)]
         out = torch.empty((g.batch, g.M, g.N), dtype=torch.float32, device=dev)
-        d = scg.make_desc(t[0], t[2], g.L_max, g.polarity, g.seed)
+        d = scg.make_desc(t[0], t[2], g.L_max, g.polarity, g.seed, int(round(float(g.L.mean()))))
         ws = scg.Workspace(scg.sc_gemm_workspace_size(d), dev)
         staged.append((g, t, out, ws))
     bitops = w.bitops()
@@ -116,7 +116,8 @@ def main():
         for k, (g, t, out, ws) in enumerate(staged):
             pe = None if pairs is None else (pairs[k][0].cuda_event, pairs[k][1].cuda_event)
             scg.gemm(t[0], t[1], t[2], t[3], t[4], L_max=g.L_max, polarity=g.polarity,
-                     seed=g.seed, out=out, workspace=ws, stream=stream, prof_events=pe)
+                     seed=g.seed, out=out, workspace=ws, stream=stream, prof_events=pe,
+                     L_hint=int(round(float(g.L.mean()))))
 
     for _ in range(args.warmup):
         step()

@@ -59,9 +59,9 @@ enum {
     SC_OK = 0,
     SC_ERR_NULL = -1,          /* a required pointer is NULL */
     SC_ERR_SHAPE = -2,         /* batch, M, N or K negative, or K > SC_K_LIMIT */
-    SC_ERR_LEN = -3,           /* L_max outside [1, SC_L_MAX_LIMIT] */
+    SC_ERR_LEN = -3,           /* L_max outside [1, SC_L_MAX_LIMIT], or L_hint outside [0, L_max] */
     SC_ERR_POLARITY = -4,      /* polarity not one of SC_BIPOLAR_XNOR / SC_UNIPOLAR_AND_SM */
-    SC_ERR_RNG = -5,           /* rng not SC_RNG_LFSR32 */
+    SC_ERR_RNG = -5,           /* rng not SC_RNG_LFSR32 (or op not 0/1) */
     SC_ERR_WORKSPACE = -6,     /* workspace NULL or smaller than sc_gemm_workspace_size() */
     SC_ERR_HIP = -7,           /* a HIP runtime call or kernel launch failed */
     SC_ERR_DEVICE_STATUS = -8, /* (sc_gemm_status) some L_i was outside [0, L_max] */
@@ -84,7 +84,9 @@ typedef struct sc_gemm_desc {
     int32_t L_max;              /* 1..SC_L_MAX_LIMIT; every L_i must lie in [0, L_max] */
     int32_t polarity;           /* SC_BIPOLAR_XNOR or SC_UNIPOLAR_AND_SM */
     int32_t rng;                /* SC_RNG_LFSR32 */
-    int32_t reserved;           /* must be 0 */
+    int32_t L_hint;             /* optional expected mean of the L_i (0 = unknown, taken as
+                                   L_max); only tunes how GEMM tiles are split over the
+                                   compute units, never changes a result; 0..L_max */
     uint64_t seed;              /* comparator seed; same seed => bit-identical results */
     void *prof_event_begin;     /* optional hipEvent_t recorded just before the main */
     void *prof_event_end;       /*   GEMM kernel and just after it (profiling); NULL = off */

@@ -24,7 +24,7 @@ def _stream_handle(stream):
     return int(s.cuda_stream)
 
 
-def make_desc(A, B, L_max: int, polarity: int, seed: int) -> ScGemmDesc:
+def make_desc(A, B, L_max: int, polarity: int, seed: int, L_hint: int = 0) -> ScGemmDesc:
     """Descriptor for contiguous A [batch, M, K] and B [batch or 1, N, K] tensors."""
     if A.dim() == 2:
         A = A.unsqueeze(0)
@@ -39,7 +39,7 @@ def make_desc(A, B, L_max: int, polarity: int, seed: int) -> ScGemmDesc:
     d.lda, d.ldb, d.ldo = K, K, N
     d.strideA, d.strideB, d.strideO = M * K, (N * K if nb == batch and batch > 1 else 0), M * N
     d.strideSA, d.strideSB, d.strideL = M, (N if nb == batch and batch > 1 else 0), M
-    d.L_max, d.polarity, d.rng, d.reserved, d.seed = int(L_max), int(polarity), SC_RNG_LFSR32, 0, int(seed)
+    d.L_max, d.polarity, d.rng, d.L_hint, d.seed = int(L_max), int(polarity), SC_RNG_LFSR32, int(L_hint), int(seed)
     return d
 
 
@@ -61,7 +61,7 @@ class Workspace:
 
 def gemm(A, sA, B, sB, L, *, L_max: int, polarity: int = SC_BIPOLAR_XNOR, seed: int = 0,
          out=None, counts=None, want_counts: bool = False, workspace: Workspace = None,
-         stream=None, check_status: bool = False, prof_events=None):
+         stream=None, check_status: bool = False, prof_events=None, L_hint: int = 0):
     """SC GEMM on torch device tensors.
 
     A int8 [batch, M, K] (or [M, K]), sA float32 [batch, M], B int8 [batch or 1, N, K],
@@ -71,7 +71,7 @@ def gemm(A, sA, B, sB, L, *, L_max: int, polarity: int = SC_BIPOLAR_XNOR, seed: 
     squeeze = A.dim() == 2
     A3 = A.unsqueeze(0) if A.dim() == 2 else A
     B3 = B.unsqueeze(0) if B.dim() == 2 else B
-    d = make_desc(A3, B3, L_max, polarity, seed)
+    d = make_desc(A3, B3, L_max, polarity, seed, L_hint)
     for t, name in ((A3, "A"), (B3, "B"), (sA, "sA"), (sB, "sB"), (L, "L")):
         if not t.is_cuda or not t.is_contiguous():
             raise ValueError("%s must be a contiguous device tensor" % name)

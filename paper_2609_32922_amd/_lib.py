@@ -49,7 +49,7 @@ class ScGemmDesc(ctypes.Structure):
         ("L_max", ctypes.c_int32),
         ("polarity", ctypes.c_int32),
         ("rng", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("L_hint", ctypes.c_int32),
         ("seed", ctypes.c_uint64),
         ("prof_event_begin", ctypes.c_void_p),
         ("prof_event_end", ctypes.c_void_p),

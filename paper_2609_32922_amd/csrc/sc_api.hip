@@ -79,19 +79,26 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     if (!mul_ok(bb, (size_t)l.nbB, &totB)) return false;
     off += totB;
 
-    // split count of the GEMM tiles: spread work units evenly over the compute units
-    // (a unit's cost is one tile restricted to KB/S element blocks; the busiest CU
-    // carries ceil(units/CUS) of them), with a small relative charge per extra split
-    // for the partial counts that the reduction pass reads back
+    // split count of the GEMM tiles.  Estimated time of split s: the busiest CU holds
+    // ceil(units/CUS) units of average work, plus the excess of the heaviest unit over
+    // the average (row tiles run as long as their longest row: up to L_max when the
+    // lengths vary, while the average follows the mean length L_hint), plus, for s > 1,
+    // the reduction pass that reads s partial blocks and writes every tile's outputs.
+    // Rates are the measured order of magnitude (about 2.8e12 bit pairs/s per CU,
+    // 3.7e12 B/s for the reduction).
     const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * l.MT * l.NT;
     l.S = 1;
-    if (tiles > 0 && tiles < 16 * CUS && l.KB > 1) {
-        double best = -1.0;
+    if (tiles > 0 && l.KB > 1) {
+        const double Lmean = d.L_hint > 0 ? d.L_hint : d.L_max;
+        const double per_L = (double)BM * BN * 32.0 * l.KB;   // tile work per cycle
+        double best = 0.0;
         for (int s = 1; s <= MAX_SPLIT && s <= l.KB; ++s) {
-            const double avg = (double)tiles * s / CUS;
-            const double eff = avg / (double)((int64_t)(avg + 0.999999)) * (1.0 - 0.005 * (s - 1));
-            if (eff > best + 1e-9) {
-                best = eff;
+            const int64_t units = tiles * s;
+            const double avg_u = per_L * Lmean / s, max_u = per_L * d.L_max / s;
+            const double gemm = ((double)((units + CUS - 1) / CUS) * avg_u + (max_u - avg_u)) / 2.8e12;
+            const double red = s > 1 ? (double)tiles * (s + 1) * BM * BN * 4.0 / 3.7e12 + 5e-6 : 0.0;
+            if (s == 1 || gemm + red < best * 0.99) {
+                best = gemm + red;
                 l.S = s;
             }
         }
@@ -126,7 +133,8 @@ static int check_desc(const sc_gemm_desc *d) {
     // counts 2*X and K*L must stay exact in int32
     if ((int64_t)d->K * d->L_max > (1ll << 29)) return SC_ERR_SHAPE;
     if (d->polarity != SC_BIPOLAR_XNOR && d->polarity != SC_UNIPOLAR_AND_SM) return SC_ERR_POLARITY;
-    if (d->rng != SC_RNG_LFSR32 || d->reserved != 0) return SC_ERR_RNG;
+    if (d->rng != SC_RNG_LFSR32) return SC_ERR_RNG;
+    if (d->L_hint < 0 || d->L_hint > d->L_max) return SC_ERR_LEN;
     if (d->lda < d->K || d->ldb < d->K || d->ldo < d->N) return SC_ERR_STRIDE;
     if (d->strideA < 0 || d->strideB < 0 || d->strideO < 0 || d->strideSA < 0 || d->strideSB < 0 ||
         d->strideL < 0)
@@ -150,9 +158,9 @@ const char *sc_strerror(int code) {
         case SC_OK: return "SC_OK";
         case SC_ERR_NULL: return "SC_ERR_NULL: a required pointer is NULL";
         case SC_ERR_SHAPE: return "SC_ERR_SHAPE: bad batch/M/N/K (or K*L_max too large)";
-        case SC_ERR_LEN: return "SC_ERR_LEN: L_max outside [1, SC_L_MAX_LIMIT]";
+        case SC_ERR_LEN: return "SC_ERR_LEN: L_max outside [1, SC_L_MAX_LIMIT] or L_hint outside [0, L_max]";
         case SC_ERR_POLARITY: return "SC_ERR_POLARITY: unknown polarity";
-        case SC_ERR_RNG: return "SC_ERR_RNG: unknown rng (or reserved field not 0)";
+        case SC_ERR_RNG: return "SC_ERR_RNG: unknown rng or operand index";
         case SC_ERR_WORKSPACE: return "SC_ERR_WORKSPACE: workspace missing or too small";
         case SC_ERR_HIP: return "SC_ERR_HIP: a HIP call or kernel launch failed";
         case SC_ERR_DEVICE_STATUS: return "SC_ERR_DEVICE_STATUS: some L_i outside [0, L_max]";

@@ -510,26 +510,53 @@ __device__ __forceinline__ void epilogue_row(const int32_t (&acc)[8], int r, int
     const float *sBb = g.sB + (size_t)b * g.strideSB;
     float *orow = g.out + (size_t)b * g.strideO + (size_t)i * g.ldo;
     int32_t *crow = g.counts ? g.counts + (size_t)b * g.strideO + (size_t)i * g.ldo : nullptr;
+    const float scale = sa * 16129.0f;
+    const int KL = g.K * Li;
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-        const int cl = c < 4 ? 4 * tx + c : 64 + 4 * tx + (c - 4);
-        const int j = tn * BN + cl;
-        if (j >= g.N) continue;
-        int32_t cnt, num;
+    for (int h = 0; h < 2; ++h) {
+        const int j0 = tn * BN + h * 64 + 4 * tx;       // four adjacent columns
+        if (j0 >= g.N) continue;
+        int rb[4] = {0, 0, 0, 0};
         if (POL == SC_BIPOLAR_XNOR) {
-            const int rb = RB[(size_t)j * (g.L_max + 1) + Li];
-            const int KL = g.K * Li;
-            cnt = KL - ra - rb + 2 * acc[c];
-            num = 2 * cnt - KL;
-        } else {
-            cnt = acc[c];
-            num = cnt;
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (j0 + c < g.N) rb[c] = RB[(size_t)(j0 + c) * (g.L_max + 1) + Li];
         }
-        float o = 0.0f;
-        if (Li > 0) o = (float)num / (float)Li * (sa * sBb[j] * 16129.0f);
-        else cnt = 0;
-        orow[j] = o;
-        if (crow) crow[j] = cnt;
+        float o[4];
+        int32_t cnt[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int j = j0 + c < g.N ? j0 + c : j0;
+            int32_t num;
+            if (POL == SC_BIPOLAR_XNOR) {
+                cnt[c] = KL - ra - rb[c] + 2 * acc[4 * h + c];
+                num = 2 * cnt[c] - KL;
+            } else {
+                cnt[c] = acc[4 * h + c];
+                num = cnt[c];
+            }
+            o[c] = 0.0f;
+            if (Li > 0) o[c] = (float)num / (float)Li * (scale * sBb[j]);
+            else cnt[c] = 0;
+        }
+        float *op = orow + j0;
+        if (j0 + 3 < g.N && (reinterpret_cast<uintptr_t>(op) & 15) == 0) {
+            *reinterpret_cast<float4 *>(op) = make_float4(o[0], o[1], o[2], o[3]);
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (j0 + c < g.N) op[c] = o[c];
+        }
+        if (crow) {
+            int32_t *cp = crow + j0;
+            if (j0 + 3 < g.N && (reinterpret_cast<uintptr_t>(cp) & 15) == 0) {
+                *reinterpret_cast<int4 *>(cp) = make_int4(cnt[0], cnt[1], cnt[2], cnt[3]);
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    if (j0 + c < g.N) cp[c] = cnt[c];
+            }
+        }
     }
 }
 

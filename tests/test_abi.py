@@ -44,7 +44,7 @@ def test_desc_layout_matches_header(lib, tmp_path):
 int main(void) {
   printf("size %zu\\n", sizeof(sc_gemm_desc));
   F(batch) F(M) F(N) F(K) F(lda) F(ldb) F(ldo) F(strideA) F(strideB) F(strideO)
-  F(strideSA) F(strideSB) F(strideL) F(L_max) F(polarity) F(rng) F(reserved) F(seed)
+  F(strideSA) F(strideSB) F(strideL) F(L_max) F(polarity) F(rng) F(L_hint) F(seed)
   F(prof_event_begin) F(prof_event_end)
   printf("L_MAX %d K_LIMIT %d\\n", SC_L_MAX_LIMIT, SC_K_LIMIT);
   return 0;
@@ -66,7 +66,7 @@ def _desc(lib, **kw):
     d = lib.ScGemmDesc()
     d.batch, d.M, d.N, d.K = 1, 64, 64, 256
     d.lda, d.ldb, d.ldo = 256, 256, 64
-    d.L_max, d.polarity, d.rng, d.reserved, d.seed = 64, 0, 0, 0, 0
+    d.L_max, d.polarity, d.rng, d.L_hint, d.seed = 64, 0, 0, 0, 0
     for k, v in kw.items():
         setattr(d, k, v)
     return d
@@ -75,7 +75,7 @@ def _desc(lib, **kw):
 @pytest.mark.parametrize("field,value,code", [
     ("M", -1, -2), ("K", -5, -2), ("batch", -1, -2), ("K", (1 << 20) + 1, -2),
     ("L_max", 0, -3), ("L_max", 4097, -3), ("polarity", 2, -4), ("rng", 1, -5),
-    ("reserved", 7, -5), ("lda", 255, -9), ("ldo", 63, -9), ("strideA", -1, -9),
+    ("L_hint", 65, -3), ("L_hint", -1, -3), ("lda", 255, -9), ("ldo", 63, -9), ("strideA", -1, -9),
 ])
 def test_workspace_size_rejects_bad_desc(lib, field, value, code):
     n = ctypes.c_size_t(0)
