@@ -133,6 +133,47 @@ int sc_gemm_status(const void *workspace, void *stream);
  */
 int sc_comparator_sequence(uint64_t seed, int32_t op, int32_t n, uint8_t *out, void *stream);
 
+/*
+ * Symmetric int8 quantisation of fp32 rows, the input preparation the SC GEMM takes
+ * as given (Sec. 3.1: s_i = max_d |X_id| / q_max, integers in [-q_max, q_max]) and
+ * that the paper's kernel fuses with emitting the row scale (Sec. 4.2 "fused
+ * quantization").  For each batch entry b and row i of X (rows x K fp32):
+ *   per_tensor = 0:  s_i = m_i / 127 with m_i = max_d |X_id|
+ *   per_tensor = 1:  s_i = m / 127 for every row, m = max over the batch entry
+ *   Q_id = clamp(rint(X_id / s_i), -127, 127), round half to even; s = 0 gives Q = 0.
+ * All arithmetic is IEEE fp32 (the division correctly rounded), so the result is
+ * bit-identical to the same formula evaluated in fp32 on the host.
+ *   X       fp32 X[b*strideX + i*ldx + d]                (device, read)
+ *   Q       int8 Q[b*strideQ + i*ldq + d]                (device, written)
+ *   scale   fp32 scale[b*strideS + i]                    (device, written)
+ *   rowmax  fp32 rowmax[b*strideS + i] = m_i, NULLABLE   (device, written): the row
+ *           metric ||X_i||_inf of the mixed-precision policy (Sec. 4.4)
+ * Needs ldx >= K, ldq >= K.  No workspace.  Asynchronous on `stream`.
+ */
+int sc_quantize(int32_t batch, int32_t rows, int32_t K, const float *X, int64_t ldx,
+                int64_t strideX, int32_t per_tensor, int8_t *Q, int64_t ldq, int64_t strideQ,
+                float *scale, float *rowmax, int64_t strideS, void *stream);
+
+#define SC_MP_MAX_LEVELS 32
+
+/*
+ * Per-row stream lengths from a row metric (Sec. 4.4 "Row metrics" and "Threshold
+ * fitting"): within each batch entry (one operator call) the metric is min-max
+ * normalised, t_i = (g_i - min_j g_j) / (max_j g_j - min_j g_j) in fp32 (t_i = 0 when
+ * all g_j are equal), and row i gets L_i = ladder[k*] with k* the first level whose
+ * threshold it reaches, t_i >= tau[k] (k = 0 .. n_levels-2), else the shortest,
+ * ladder[n_levels-1].
+ *   metric  fp32 metric[b*strideM + i]   (device), e.g. the rowmax of sc_quantize
+ *   tau     n_levels-1 fp32 thresholds in [0,1], non-increasing   (HOST array)
+ *   ladder  n_levels int32 lengths, strictly decreasing, >= 0     (HOST array)
+ *   L_out   int32 L_out[b*strideL + i]   (device, written): feeds sc_gemm directly
+ * 1 <= n_levels <= SC_MP_MAX_LEVELS.  The thresholds come from an offline calibration
+ * that is not part of this library.  Asynchronous on `stream`.
+ */
+int sc_mp_lengths(int32_t batch, int32_t M, const float *metric, int64_t strideM,
+                  const float *tau, const int32_t *ladder, int32_t n_levels, int32_t *L_out,
+                  int64_t strideL, void *stream);
+
 /* Human-readable name of a status code (static string). */
 const char *sc_strerror(int code);
 

@@ -8,7 +8,10 @@ The arithmetic lives in ``sc_oracle.c`` (plain C, OpenMP over rows, one byte per
 stream bit, float64 decode); this module only builds it with gcc and marshals
 numpy arrays through ctypes.  Each C function's header comment cites the passage
 of the paper it follows (Sec. 3.1 encoding / comparator / Eq. (1), Sec. 4.2
-boundaries and row lengths, Sec. A.1 LFSR).
+boundaries and row lengths, Sec. A.1 LFSR).  The front-end functions at the end
+(int8 quantisation, Sec. 3.1; per-row length policy, Sec. 4.4) are plain numpy
+written element by element in fp32, the precision both sides take those integer
+decisions in.
 """
 from __future__ import annotations
 
@@ -136,3 +139,75 @@ def sc_gemm(A: np.ndarray, B: np.ndarray, sA: np.ndarray, sB: np.ndarray,
 
 def max_threads() -> int:
     return int(_load().oracle_max_threads())
+
+
+# ----------------------------------------------------------------------------
+# front end: symmetric int8 quantisation and the per-row length policy
+# (plain numpy, row by row, IEEE fp32 as the device computes it)
+# ----------------------------------------------------------------------------
+
+def quantize_rows_fp32(X: np.ndarray):
+    """Per-row symmetric int8 quantisation (Sec. 3.1: s_i = max_d |X_id| / q_max).
+
+    Returns (Q int8, s float32, m float32) with m_i = max_d |X_id|.  Every step is an
+    fp32 operation: s = m / 127, Q = clamp(rint(x / s), -127, 127) (half to even);
+    s = 0 gives Q = 0.
+    """
+    X = np.asarray(X, dtype=np.float32)
+    rows, K = X.shape
+    Q = np.zeros((rows, K), np.int8)
+    s = np.zeros(rows, np.float32)
+    m = np.zeros(rows, np.float32)
+    for i in range(rows):
+        mi = np.float32(0.0)
+        for d in range(K):
+            a = np.float32(abs(X[i, d]))
+            if a > mi:
+                mi = a
+        m[i] = mi
+        si = np.float32(mi / np.float32(127.0))
+        s[i] = si
+        if si > 0:
+            q = np.rint(X[i] / si)                    # fp32 division, half-to-even
+            Q[i] = np.clip(q, -127, 127).astype(np.int8)
+    return Q, s, m
+
+
+def quantize_tensor_fp32(X: np.ndarray):
+    """Per-tensor symmetric int8 quantisation: one scale m/127 with m = max |X|."""
+    X = np.asarray(X, dtype=np.float32)
+    rows, K = X.shape
+    m = np.float32(0.0)
+    for i in range(rows):
+        for d in range(K):
+            a = np.float32(abs(X[i, d]))
+            if a > m:
+                m = a
+    sc = np.float32(m / np.float32(127.0))
+    Q = np.zeros((rows, K), np.int8)
+    if sc > 0:
+        for i in range(rows):
+            Q[i] = np.clip(np.rint(X[i] / sc), -127, 127).astype(np.int8)
+    return Q, np.full(rows, sc, np.float32)
+
+
+def mp_lengths_fp32(metric: np.ndarray, tau, ladder) -> np.ndarray:
+    """Per-row stream lengths of one operator call (Sec. 4.4).
+
+    t_i = (g_i - min g) / (max g - min g) in fp32 (0 when max = min); row i gets
+    ladder[k] for the first k with t_i >= tau[k], else the shortest, ladder[-1].
+    """
+    g = np.asarray(metric, dtype=np.float32)
+    lo = np.float32(g.min()) if g.size else np.float32(0)
+    hi = np.float32(g.max()) if g.size else np.float32(0)
+    rng = np.float32(hi - lo)
+    out = np.zeros(g.shape[0], np.int32)
+    for i in range(g.shape[0]):
+        t = np.float32(np.float32(g[i] - lo) / rng) if rng > 0 else np.float32(0.0)
+        k = len(ladder) - 1
+        for j in range(len(ladder) - 1):
+            if t >= np.float32(tau[j]):
+                k = j
+                break
+        out[i] = int(ladder[k])
+    return out

@@ -11,11 +11,13 @@ from __future__ import annotations
 
 from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_L_MAX_LIMIT, SC_OK,  # noqa: F401
                    SC_RNG_LFSR32, SC_UNIPOLAR_AND_SM, ScError, ScGemmDesc, load, sc_comparator_sequence,
-                   sc_gemm, sc_gemm_status, sc_gemm_workspace_size, sc_version, strerror)
+                   sc_gemm, sc_gemm_status, sc_gemm_workspace_size, sc_mp_lengths, sc_quantize,
+                   sc_version, strerror)
 
-__all__ = ["gemm", "make_desc", "comparator_sequence", "Workspace", "ScGemmDesc", "ScError",
-           "sc_gemm", "sc_gemm_workspace_size", "sc_gemm_status", "sc_comparator_sequence",
-           "SC_BIPOLAR_XNOR", "SC_UNIPOLAR_AND_SM"]
+__all__ = ["gemm", "make_desc", "comparator_sequence", "quantize", "mp_lengths", "Workspace",
+           "ScGemmDesc", "ScError", "sc_gemm", "sc_gemm_workspace_size", "sc_gemm_status",
+           "sc_comparator_sequence", "sc_quantize", "sc_mp_lengths", "SC_BIPOLAR_XNOR",
+           "SC_UNIPOLAR_AND_SM"]
 
 
 def _stream_handle(stream):
@@ -113,3 +115,44 @@ def comparator_sequence(seed: int, op: int, n: int, stream=None):
     if rc != SC_OK:
         raise ScError(rc, "sc_comparator_sequence")
     return out
+
+
+def quantize(X, per_tensor: bool = False, want_rowmax: bool = False, stream=None):
+    """Device int8 quantisation of fp32 X [batch, rows, K] (or [rows, K]).
+
+    Returns (Q int8, scale float32 [batch, rows], rowmax float32 or None).
+    """
+    import torch
+    squeeze = X.dim() == 2
+    X3 = X.unsqueeze(0) if squeeze else X
+    if not X3.is_cuda or not X3.is_contiguous() or X3.dtype != torch.float32:
+        raise ValueError("X must be a contiguous float32 device tensor")
+    batch, rows, K = X3.shape
+    Q = torch.empty((batch, rows, K), dtype=torch.int8, device=X.device)
+    scale = torch.empty((batch, rows), dtype=torch.float32, device=X.device)
+    rowmax = torch.empty((batch, rows), dtype=torch.float32, device=X.device) if want_rowmax else None
+    rc = sc_quantize(batch, rows, K, X3.data_ptr(), K, rows * K, int(per_tensor), Q.data_ptr(), K,
+                     rows * K, scale.data_ptr(), rowmax.data_ptr() if rowmax is not None else 0,
+                     rows, _stream_handle(stream))
+    if rc != SC_OK:
+        raise ScError(rc, "sc_quantize")
+    if squeeze:
+        return Q[0], scale[0], (rowmax[0] if rowmax is not None else None)
+    return Q, scale, rowmax
+
+
+def mp_lengths(metric, tau, ladder, stream=None):
+    """Per-row stream lengths (int32 device tensor shaped like ``metric``) from a row
+    metric [batch, M] (or [M]) with thresholds ``tau`` and length ladder ``ladder``."""
+    import torch
+    squeeze = metric.dim() == 1
+    m2 = metric.unsqueeze(0) if squeeze else metric
+    if not m2.is_cuda or not m2.is_contiguous() or m2.dtype != torch.float32:
+        raise ValueError("metric must be a contiguous float32 device tensor")
+    batch, M = m2.shape
+    L = torch.empty((batch, M), dtype=torch.int32, device=metric.device)
+    rc = sc_mp_lengths(batch, M, m2.data_ptr(), M, list(tau), list(ladder), L.data_ptr(), M,
+                       _stream_handle(stream))
+    if rc != SC_OK:
+        raise ScError(rc, "sc_mp_lengths")
+    return L[0] if squeeze else L

@@ -85,6 +85,13 @@ def load():
     lib.sc_gemm_status.restype = ctypes.c_int
     lib.sc_comparator_sequence.argtypes = [u64, i32, i32, vp, vp]
     lib.sc_comparator_sequence.restype = ctypes.c_int
+    f32p = ctypes.POINTER(ctypes.c_float)
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    i64 = ctypes.c_int64
+    lib.sc_quantize.argtypes = [i32, i32, i32, vp, i64, i64, i32, vp, i64, i64, vp, vp, i64, vp]
+    lib.sc_quantize.restype = ctypes.c_int
+    lib.sc_mp_lengths.argtypes = [i32, i32, vp, i64, f32p, i32p, i32, vp, i64, vp]
+    lib.sc_mp_lengths.restype = ctypes.c_int
     lib.sc_strerror.argtypes = [ctypes.c_int]
     lib.sc_strerror.restype = ctypes.c_char_p
     lib.sc_version.argtypes = []
@@ -118,6 +125,22 @@ def sc_gemm_status(workspace: int, stream: int) -> int:
 
 def sc_comparator_sequence(seed: int, op: int, n: int, out: int, stream: int) -> int:
     return int(load().sc_comparator_sequence(ctypes.c_uint64(seed), op, n, out, stream or None))
+
+
+def sc_quantize(batch: int, rows: int, K: int, X: int, ldx: int, strideX: int, per_tensor: int,
+                Q: int, ldq: int, strideQ: int, scale: int, rowmax: int, strideS: int,
+                stream: int) -> int:
+    return int(load().sc_quantize(batch, rows, K, X, ldx, strideX, per_tensor, Q, ldq, strideQ,
+                                  scale, rowmax or None, strideS, stream or None))
+
+
+def sc_mp_lengths(batch: int, M: int, metric: int, strideM: int, tau, ladder, L_out: int,
+                  strideL: int, stream: int) -> int:
+    n = len(ladder)
+    tau_a = (ctypes.c_float * max(len(tau), 1))(*[float(x) for x in tau])
+    lad_a = (ctypes.c_int32 * max(n, 1))(*[int(x) for x in ladder])
+    return int(load().sc_mp_lengths(batch, M, metric, strideM, tau_a, lad_a, n, L_out, strideL,
+                                    stream or None))
 
 
 def sc_version() -> int:

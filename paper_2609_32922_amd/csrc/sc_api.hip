@@ -139,9 +139,14 @@ static int check_desc(const sc_gemm_desc *d) {
     if (d->strideA < 0 || d->strideB < 0 || d->strideO < 0 || d->strideSA < 0 || d->strideSB < 0 ||
         d->strideL < 0)
         return SC_ERR_STRIDE;
-    // distinct batch entries must not overlap in the output
-    if (d->batch > 1 && d->M > 0 && d->N > 0 && d->strideO < (int64_t)(d->M - 1) * d->ldo + d->N)
-        return SC_ERR_STRIDE;
+    // distinct batch entries must not overlap in the output: either each entry's block
+    // lies before the next one (blocked), or the entries sit side by side in the columns
+    // of one row stride (interleaved, e.g. per-head outputs of one token matrix)
+    if (d->batch > 1 && d->M > 0 && d->N > 0) {
+        const bool blocked = d->strideO >= (int64_t)(d->M - 1) * d->ldo + d->N;
+        const bool interleaved = d->strideO >= d->N && (int64_t)(d->batch - 1) * d->strideO + d->N <= d->ldo;
+        if (!blocked && !interleaved) return SC_ERR_STRIDE;
+    }
     return SC_OK;
 }
 
@@ -228,6 +233,49 @@ int sc_gemm_status(const void *workspace, void *stream) {
     if (hipMemcpy(&word, workspace, sizeof(word), hipMemcpyDeviceToHost) != hipSuccess)
         return SC_ERR_HIP;
     return (word & STATUS_BAD_LENGTH) ? SC_ERR_DEVICE_STATUS : SC_OK;
+}
+
+int sc_quantize(int32_t batch, int32_t rows, int32_t K, const float *X, int64_t ldx,
+                int64_t strideX, int32_t per_tensor, int8_t *Q, int64_t ldq, int64_t strideQ,
+                float *scale, float *rowmax, int64_t strideS, void *stream) {
+    if (batch < 0 || rows < 0 || K < 0 || K > SC_K_LIMIT) return SC_ERR_SHAPE;
+    if (per_tensor != 0 && per_tensor != 1) return SC_ERR_SHAPE;
+    if (ldx < K || ldq < K || strideX < 0 || strideQ < 0 || strideS < 0) return SC_ERR_STRIDE;
+    if (batch > 1 && rows > 0 && strideS < rows) return SC_ERR_STRIDE;
+    if (batch == 0 || rows == 0) return SC_OK;
+    if ((K > 0 && (X == nullptr || Q == nullptr)) || scale == nullptr) return SC_ERR_NULL;
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    if (launch_quantize(batch, rows, K, X, ldx, strideX, per_tensor, Q, ldq, strideQ, scale, rowmax,
+                        strideS, st) != hipSuccess)
+        return SC_ERR_HIP;
+    return SC_OK;
+}
+
+int sc_mp_lengths(int32_t batch, int32_t M, const float *metric, int64_t strideM,
+                  const float *tau, const int32_t *ladder, int32_t n_levels, int32_t *L_out,
+                  int64_t strideL, void *stream) {
+    if (batch < 0 || M < 0) return SC_ERR_SHAPE;
+    if (n_levels < 1 || n_levels > SC_MP_MAX_LEVELS) return SC_ERR_LEN;
+    if (ladder == nullptr || (n_levels > 1 && tau == nullptr)) return SC_ERR_NULL;
+    MpParams p{};
+    p.n = n_levels;
+    for (int k = 0; k < n_levels; ++k) {
+        if (ladder[k] < 0 || ladder[k] > SC_L_MAX_LIMIT || (k > 0 && ladder[k] >= ladder[k - 1]))
+            return SC_ERR_LEN;
+        p.ladder[k] = ladder[k];
+    }
+    for (int k = 0; k + 1 < n_levels; ++k) {
+        if (!(tau[k] >= 0.0f && tau[k] <= 1.0f) || (k > 0 && tau[k] > tau[k - 1])) return SC_ERR_LEN;
+        p.tau[k] = tau[k];
+    }
+    if (strideM < 0 || strideL < 0 || (batch > 1 && M > 0 && (strideM < M || strideL < M)))
+        return SC_ERR_STRIDE;
+    if (batch == 0 || M == 0) return SC_OK;
+    if (metric == nullptr || L_out == nullptr) return SC_ERR_NULL;
+    if (launch_mp_lengths(batch, M, metric, strideM, p, L_out, strideL,
+                          reinterpret_cast<hipStream_t>(stream)) != hipSuccess)
+        return SC_ERR_HIP;
+    return SC_OK;
 }
 
 int sc_comparator_sequence(uint64_t seed, int32_t op, int32_t n, uint8_t *out, void *stream) {

@@ -71,4 +71,18 @@ hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t 
 hipError_t launch_gemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
                        float *out, int32_t *counts, uint8_t *ws, hipStream_t st);
 
+// thresholds and ladder of the per-row length policy, passed by value to the kernel
+struct MpParams {
+    float tau[SC_MP_MAX_LEVELS];
+    int32_t ladder[SC_MP_MAX_LEVELS];
+    int32_t n;
+};
+
+// front end (sc_frontend.hip)
+hipError_t launch_quantize(int batch, int rows, int K, const float *X, int64_t ldx, int64_t strideX,
+                           int per_tensor, int8_t *Q, int64_t ldq, int64_t strideQ, float *scale,
+                           float *rowmax, int64_t strideS, hipStream_t st);
+hipError_t launch_mp_lengths(int batch, int M, const float *metric, int64_t strideM,
+                             const MpParams &p, int32_t *L_out, int64_t strideL, hipStream_t st);
+
 }  // namespace scg

@@ -196,3 +196,50 @@ def test_workload_ditxl2_proj_mlp_group96(dev, oracle_mod):
 def test_workload_vitl14_336_qk_mlp(dev, oracle_mod):
     _check_workload(W.vitl14_336_qk_mlp(), dev, oracle_mod, nrows=24, ncols=64,
                     batches=None)
+
+
+def test_workload_vitl14_compensator_L256(dev, oracle_mod):
+    _check_workload(W.vitl14_compensator_L256(), dev, oracle_mod, nrows=24, ncols=64)
+
+
+def test_workload_vitl14_336_attn_av(dev, oracle_mod):
+    _check_workload(W.vitl14_336_attn_av(), dev, oracle_mod, nrows=16, ncols=64, batches=range(0, 128, 9))
+
+
+def test_strided_interleaved_heads(dev, oracle_mod):
+    """Per-head GEMMs read straight out of one token matrix (lda = 1024, strideA = 64)
+    and write their outputs side by side into one output matrix (ldo = 1024,
+    strideO = 64): the layout of a per-head compensator on the block input."""
+    import torch
+    import paper_2609_32922_amd as scg
+    rng = np.random.default_rng(61)
+    T, H, dh = 300, 16, 64
+    x = rng.integers(-127, 128, (T, H * dh)).astype(np.int8)
+    sx = rng.uniform(0.01, 0.1, (H, T)).astype(np.float32)
+    Wq = rng.integers(-127, 128, (H, dh, dh)).astype(np.int8)
+    sw = rng.uniform(0.001, 0.01, (H, dh)).astype(np.float32)
+    L = rng.integers(0, 97, (H, T)).astype(np.int32)
+    d = scg.ScGemmDesc()
+    d.batch, d.M, d.N, d.K = H, T, dh, dh
+    d.lda, d.ldb, d.ldo = H * dh, dh, H * dh
+    d.strideA, d.strideB, d.strideO = dh, dh * dh, dh
+    d.strideSA, d.strideSB, d.strideL = T, dh, T
+    d.L_max, d.polarity, d.rng, d.L_hint, d.seed = 96, 0, 0, 0, 77
+    tx, tsx, tw, tsw, tL = (torch.from_numpy(a).to(dev) for a in (x, sx, Wq, sw, L))
+    out = torch.zeros((T, H * dh), dtype=torch.float32, device=dev)
+    cnt = torch.zeros((T, H * dh), dtype=torch.int32, device=dev)
+    ws = scg.Workspace(scg.sc_gemm_workspace_size(d), dev)
+    _note("strided interleaved heads")
+    rc = scg.sc_gemm(d, tx.data_ptr(), tsx.data_ptr(), tw.data_ptr(), tsw.data_ptr(), tL.data_ptr(),
+                     out.data_ptr(), cnt.data_ptr(), ws.ptr, ws.nbytes,
+                     int(torch.cuda.current_stream().cuda_stream))
+    assert rc == 0
+    assert scg.sc_gemm_status(ws.ptr, int(torch.cuda.current_stream().cuda_stream)) == 0
+    c, o = cnt.cpu().numpy(), out.cpu().numpy()
+    for h in range(H):
+        c_ref, o_ref = oracle_mod.sc_gemm(x[:, h * dh:(h + 1) * dh], Wq[h], sx[h], sw[h], L[h], 96, 0, 77)
+        assert np.array_equal(c[:, h * dh:(h + 1) * dh], c_ref), h
+        oo = o[:, h * dh:(h + 1) * dh].astype(np.float64)
+        nz = o_ref != 0
+        assert np.all(oo[~nz] == 0)
+        assert np.max(np.abs(oo[nz] - o_ref[nz]) / np.abs(o_ref[nz])) <= 1e-6

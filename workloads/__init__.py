@@ -277,12 +277,63 @@ def vitl14_336_qk_mlp(seed: int = 4, qk: bool = True, mlp: bool = True) -> Workl
                     gemms)
 
 
+def vitl14_compensator_L256(seed: int = 5) -> Workload:
+    """Per-head residual compensator of one ViT-L/14 block (224 px, batch 32 x 257 tokens):
+    16 heads, each a 64x64 SC matmul of the head's slice of the block input, at the
+    uniform compensator length L = 256, bipolar (Sec. A.2: W_b stored per head, the
+    compensator itself an SC matmul at L_comp = 256).
+
+    Block input x ~ N(0,1) with 1% Student-t(3) entries, per-row scales of each head's
+    slice; W_h ~ N(0, 0.02), per-head per-tensor scale.
+    """
+    rng = np.random.default_rng(seed)
+    T, H, dh = 32 * 257, 16, 64
+    x = _heavy_tail_normal(rng, (T, H * dh))
+    Wc = (rng.standard_normal((H, dh, dh), dtype=np.float32) * np.float32(0.02)).astype(np.float32)
+    xs = np.ascontiguousarray(x.reshape(T, H, dh).transpose(1, 0, 2))     # [H, T, 64]
+    qA, sA = quantize_rows(xs)
+    qB = np.empty((H, dh, dh), np.int8)
+    sB = np.empty((H, dh), np.float32)
+    for h in range(H):
+        qB[h], sB[h] = quantize_tensor(Wc[h])
+    g = Gemm("compensator", qA, sA, qB, sB, np.full((H, T), 256, np.int32), 256, BIPOLAR, seed)
+    return Workload("vitl14_compensator_L256",
+                    "ViT-L/14 per-head compensator 16 x (8224x64x64), bipolar, L = 256", [g])
+
+
+def vitl14_336_attn_av(seed: int = 6) -> Workload:
+    """Attention probabilities times values, ViT-L/14 at 336 px: 8 x 16 heads of
+    P (577 x 577, softmax rows, values in [0,1]) times V (577 x 64).  In the A.B^T form
+    A = P (M = K = 577) and B = V^T (N = 64).  Unipolar sign-magnitude (P >= 0, V signed).
+    Row lengths follow the peak attention probability max_j P_ij (Sec. 4.4 metric of the
+    av operator), in [8, 512] with mean 96 per head.
+    """
+    rng = np.random.default_rng(seed)
+    H, S, dh = 8 * 16, 577, 64
+    Qm = _heavy_tail_normal(rng, (H, S, dh))
+    Km = _heavy_tail_normal(rng, (H, S, dh))
+    V = _heavy_tail_normal(rng, (H, S, dh))
+    logits = np.einsum("hid,hjd->hij", Qm, Km, optimize=True).astype(np.float32) / np.float32(8.0)
+    logits -= logits.max(axis=2, keepdims=True)
+    P = np.exp(logits).astype(np.float32)
+    P /= P.sum(axis=2, keepdims=True)
+    qP, sP = quantize_rows(P)
+    Vt = np.ascontiguousarray(V.transpose(0, 2, 1))                      # [H, 64, 577]
+    qV, sV = quantize_rows(Vt)
+    L = np.stack([lengths_matched_mean(P[h].max(axis=1), 8, 512, 96) for h in range(H)])
+    g = Gemm("attn_av", qP, sP, qV, sV, L.astype(np.int32), 512, UNIPOLAR_SM, seed)
+    return Workload("vitl14_336_attn_av",
+                    "ViT-L/14-336 attention P.V 128 x (577x577x64), unipolar SM, per-row L mean 96", [g])
+
+
 WORKLOADS: Dict[str, callable] = {
     "bipolar_64x256x64_L64": bipolar_64x256x64,
     "vitb16_fc1_L128": vitb16_fc1_L128,
     "vitb16_fc1_mp64": vitb16_fc1_mp64,
     "ditxl2_proj_mlp_group96": ditxl2_proj_mlp_group96,
     "vitl14_336_qk_mlp": vitl14_336_qk_mlp,
+    "vitl14_compensator_L256": vitl14_compensator_L256,
+    "vitl14_336_attn_av": vitl14_336_attn_av,
 }
 
 
