@@ -60,6 +60,13 @@ def _load():
         lib.oracle_sc_gemm.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, u64,
                                        vp, vp, i32]
         lib.oracle_sc_gemm.restype = ctypes.c_int
+        lib.oracle_sobol_shift.argtypes = [u64, u32]
+        lib.oracle_sobol_shift.restype = u32
+        lib.oracle_sobol8.argtypes = [ctypes.c_int, u32, i32, vp]
+        lib.oracle_sobol8.restype = ctypes.c_int
+        lib.oracle_sc_gemm_cbsg.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, u64,
+                                            vp, vp, i32]
+        lib.oracle_sc_gemm_cbsg.restype = ctypes.c_int
         lib.oracle_max_threads.argtypes = []
         lib.oracle_max_threads.restype = i32
         _lib = lib
@@ -134,6 +141,41 @@ def sc_gemm(A: np.ndarray, B: np.ndarray, sA: np.ndarray, sB: np.ndarray,
                                 _ptr(counts), _ptr(out), int(nthreads))
     if rc != 0:
         raise ValueError("oracle_sc_gemm failed with code %d" % rc)
+    return counts, out
+
+
+def sobol_shift(seed: int, op: int) -> int:
+    return int(_load().oracle_sobol_shift(ctypes.c_uint64(seed), op))
+
+
+def sobol8(dim: int, shift: int, n: int = 256) -> np.ndarray:
+    """First n (<= 256) points of scrambled Sobol-8 dimension ``dim`` (1 or 2), uint8."""
+    out = np.zeros(max(n, 1), np.uint8)
+    if _load().oracle_sobol8(dim, shift, n, _ptr(out)) != 0:
+        raise ValueError("bad Sobol arguments")
+    return out[:n]
+
+
+def sc_gemm_cbsg(A: np.ndarray, B: np.ndarray, sA: np.ndarray, sB: np.ndarray,
+                 L: np.ndarray, L_max: int, polarity: int, seed: int,
+                 nthreads: int = 0, want_out: bool = True):
+    """Oracle SC GEMM with Sobol-8 C-BSG streams.  Returns (counts, out)."""
+    A = np.ascontiguousarray(A, dtype=np.int8)
+    B = np.ascontiguousarray(B, dtype=np.int8)
+    sA = np.ascontiguousarray(sA, dtype=np.float32)
+    sB = np.ascontiguousarray(sB, dtype=np.float32)
+    L = np.ascontiguousarray(L, dtype=np.int32)
+    M, K = A.shape
+    N, K2 = B.shape
+    if K2 != K or sA.shape != (M,) or sB.shape != (N,) or L.shape != (M,):
+        raise ValueError("shape mismatch")
+    counts = np.zeros((M, N), np.int32)
+    out = np.zeros((M, N), np.float64) if want_out else None
+    rc = _load().oracle_sc_gemm_cbsg(M, N, K, _ptr(A), _ptr(B), _ptr(sA), _ptr(sB), _ptr(L),
+                                     int(L_max), int(polarity), ctypes.c_uint64(seed),
+                                     _ptr(counts), _ptr(out), int(nthreads))
+    if rc != 0:
+        raise ValueError("oracle_sc_gemm_cbsg failed with code %d" % rc)
     return counts, out
 
 

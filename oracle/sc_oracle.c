@@ -40,6 +40,23 @@
  *   R-UNI    unipolar variant: magnitude streams split by sign into X+ and X-, the
  *            four partial products counted literally, S = c_pp + c_nn - c_pn - c_np.
  *
+ * Second comparator source, the paper's own (Sec. 4.2 "Datapath: cumulative-indicator
+ * C-BSG"; Sec. A.1 scrambled Sobol sequences and conditional bitstream generation,
+ * Eq. (4)-(6)).  Readings taken:
+ *   R-SOBOL  Sobol-8: r_k = shift XOR (XOR over the set bits j of k of V_j), k < 256,
+ *            8-bit direction numbers V_j = m_j << (8 - j) from the published
+ *            primitive-polynomial recurrence (Bratley and Fox; Joe and Kuo):
+ *            dimension 1 m_j = 1 (van der Corput), dimension 2 polynomial x + 1 with
+ *            m_1 = 1, m_j = 2 m_{j-1} xor m_{j-1}.  The digital shift of operand op is
+ *            the top 8 bits of SplitMix64(2*seed + op).  A uses dimension 1, B dimension 2.
+ *   R-CBSG   A's stream is its comparator stream on its own Sobol sequence.  B's
+ *            generator is gated by A's stream (Fig. 1(c)): B keeps two counters that walk
+ *            the same sequence r^B, one advanced on the cycles where A emits 1 and one on
+ *            the cycles where A emits 0; at each cycle B compares the draw its active
+ *            counter points at against its boundary.  This matches both conditional
+ *            distributions of Eq. (6) to the marginal of r^B.
+ *   R-CBSG-L L_max <= 256 (one Sobol-8 period); a shorter row takes the prefix.
+ *
  * Build: gcc -O2 -fopenmp -shared -fPIC sc_oracle.c -o libsc_oracle.so
  */
 #include <stdint.h>
@@ -265,3 +282,109 @@ int oracle_sc_gemm(int32_t M, int32_t N, int32_t K,
 
 /* Number of OpenMP threads a parallel region would use now. */
 int32_t oracle_max_threads(void) { return (int32_t)omp_get_max_threads(); }
+
+/* ------------------------------------------------------------------------- */
+/* Sobol-8 and conditional bitstream generation (C-BSG)                       */
+/* ------------------------------------------------------------------------- */
+
+/* 8-bit direction numbers of Sobol dimension `dim` (1 or 2), V[j-1] for j = 1..8. */
+static int sobol8_directions(int dim, uint32_t V[8])
+{
+    uint32_t m[9];
+    if (dim == 1) {
+        for (int j = 1; j <= 8; ++j) m[j] = 1;
+    } else if (dim == 2) {
+        /* primitive polynomial x + 1 (degree 1): m_j = 2 m_{j-1} xor m_{j-1} */
+        m[1] = 1;
+        for (int j = 2; j <= 8; ++j) m[j] = (2 * m[j - 1]) ^ m[j - 1];
+    } else {
+        return -1;
+    }
+    for (int j = 1; j <= 8; ++j) V[j - 1] = m[j] << (8 - j);
+    return 0;
+}
+
+/* The digital shift of operand `op` for `seed`. */
+uint32_t oracle_sobol_shift(uint64_t seed, uint32_t op)
+{
+    return (uint32_t)(oracle_splitmix64(2ull * seed + (uint64_t)op) >> 56);
+}
+
+/* r_k = shift xor (xor of V_j over the set bits of k), k = 0..n-1, n <= 256. */
+int oracle_sobol8(int dim, uint32_t shift, int32_t n, uint8_t *out)
+{
+    uint32_t V[8];
+    if (sobol8_directions(dim, V) != 0 || n < 0 || n > 256) return -1;
+    for (int32_t k = 0; k < n; ++k) {
+        uint32_t x = 0;
+        for (int j = 0; j < 8; ++j)
+            if ((k >> j) & 1) x ^= V[j];
+        out[k] = (uint8_t)((x ^ shift) & 255u);
+    }
+    return 0;
+}
+
+/*
+ * SC GEMM with C-BSG streams (same shapes, scales and decode as oracle_sc_gemm).
+ * For every pair (i, j) and element d the three streams are materialised cycle by
+ * cycle: zA_l = [rA_l < betaA] for l < L_i; B's draw at cycle l is r^B at counter k1
+ * if zA_l = 1 (then k1 advances) or at counter k0 if zA_l = 0 (then k0 advances);
+ * zB_l = [that draw < betaB].  Bipolar counts XNOR(zA, zB); unipolar counts the
+ * AND of the magnitude streams with the pair's sign.  L_max <= 256.
+ */
+int oracle_sc_gemm_cbsg(int32_t M, int32_t N, int32_t K,
+                        const int8_t *A, const int8_t *B,
+                        const float *sA, const float *sB,
+                        const int32_t *L, int32_t L_max,
+                        int32_t polarity, uint64_t seed,
+                        int32_t *counts, double *out, int32_t nthreads)
+{
+    if (M < 0 || N < 0 || K < 0 || L_max < 0 || L_max > 256 || (polarity != 0 && polarity != 1))
+        return -1;
+    for (int32_t i = 0; i < M; ++i)
+        if (L[i] < 0 || L[i] > L_max) return -1;
+    if (M == 0 || N == 0) return 0;
+    uint8_t rA[256], rB[256];
+    oracle_sobol8(1, oracle_sobol_shift(seed, 0), 256, rA);
+    oracle_sobol8(2, oracle_sobol_shift(seed, 1), 256, rB);
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t i = 0; i < M; ++i) {
+        const int32_t Li = L[i];
+        uint8_t za[256], zb[256];
+        for (int32_t j = 0; j < N; ++j) {
+            int64_t c = 0;
+            for (int32_t d = 0; d < K; ++d) {
+                const int32_t qa = A[(size_t)i * K + d], qb = B[(size_t)j * K + d];
+                const int32_t ba = polarity == 0 ? oracle_beta_bipolar(qa) : oracle_beta_unipolar(qa);
+                const int32_t bb = polarity == 0 ? oracle_beta_bipolar(qb) : oracle_beta_unipolar(qb);
+                sng(rA, ba, Li, za);
+                int32_t k1 = 0, k0 = 0;
+                for (int32_t l = 0; l < Li; ++l) {
+                    const int32_t draw = za[l] ? rB[k1++] : rB[k0++];
+                    zb[l] = (uint8_t)(draw < bb ? 1 : 0);
+                }
+                int32_t s = 0;
+                if (polarity == 0) {
+                    for (int32_t l = 0; l < Li; ++l) s += 1 - (za[l] ^ zb[l]);
+                } else {
+                    for (int32_t l = 0; l < Li; ++l) s += za[l] & zb[l];
+                    if ((qa < 0) != (qb < 0)) s = -s;
+                }
+                c += s;
+            }
+            const size_t o = (size_t)i * N + j;
+            if (counts) counts[o] = (int32_t)c;
+            if (out) {
+                if (Li == 0) {
+                    out[o] = 0.0;
+                } else {
+                    const double scale = (double)sA[i] * (double)sB[j] * (double)(QMAX * QMAX);
+                    out[o] = polarity == 0 ? scale * (2.0 * (double)c / (double)Li - (double)K)
+                                           : scale * (double)c / (double)Li;
+                }
+            }
+        }
+    }
+    return 0;
+}

@@ -101,3 +101,69 @@ def sc_gemm(A, B, sA, sB, L, polarity, seed):
                 else:
                     out[i][j] = scale * Fraction(c, Li)
     return counts, out
+
+
+# ---------------------------------------------------------------------------
+# Sobol-8 and conditional bitstream generation, written independently
+# ---------------------------------------------------------------------------
+
+def sobol8_points(dim, shift, n=256):
+    """Natural-order Sobol points of dimension 1 or 2 as 8-bit integers.
+
+    Dimension 1 is the base-2 radical inverse; dimension 2 uses direction numbers of
+    the polynomial x + 1, computed here as bit-reversed binomial coefficients mod 2.
+    """
+    pts = []
+    for k in range(n):
+        if dim == 1:
+            x = int("{:08b}".format(k)[::-1], 2)
+        else:
+            x = 0
+            for j in range(8):
+                if (k >> j) & 1:
+                    # m_{j+1} of x + 1 is the odd number whose bits are row j of Pascal's
+                    # triangle mod 2
+                    m = sum(((1 if (j & i) == i else 0) << i) for i in range(j + 1))
+                    x ^= m << (8 - (j + 1))
+        pts.append(x ^ shift)
+    return pts
+
+
+def cbsg_gemm(A, B, sA, sB, L, polarity, seed):
+    M, N = len(A), len(B)
+    K = len(A[0]) if M else 0
+    sh_a = splitmix64((2 * seed) & MASK64) >> 56
+    sh_b = splitmix64((2 * seed + 1) & MASK64) >> 56
+    rA = sobol8_points(1, sh_a)
+    rB = sobol8_points(2, sh_b)
+    counts = [[0] * N for _ in range(M)]
+    out = [[Fraction(0)] * N for _ in range(M)]
+    bfun = beta_bipolar if polarity == 0 else beta_unipolar
+    for i in range(M):
+        Li = L[i]
+        for j in range(N):
+            c = 0
+            for d in range(K):
+                ba, bb = bfun(A[i][d]), bfun(B[j][d])
+                ones = zeros = 0
+                s = 0
+                for l in range(Li):
+                    a = 1 if rA[l] < ba else 0
+                    if a:
+                        bbit = 1 if rB[ones] < bb else 0
+                        ones += 1
+                    else:
+                        bbit = 1 if rB[zeros] < bb else 0
+                        zeros += 1
+                    if polarity == 0:
+                        s += 1 if a == bbit else 0
+                    else:
+                        s += a & bbit
+                if polarity == 1 and (A[i][d] < 0) != (B[j][d] < 0):
+                    s = -s
+                c += s
+            counts[i][j] = c
+            if Li > 0:
+                scale = Fraction(sA[i]) * Fraction(sB[j]) * QMAX * QMAX
+                out[i][j] = scale * (Fraction(2 * c, Li) - K) if polarity == 0 else scale * Fraction(c, Li)
+    return counts, out
