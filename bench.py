@@ -35,6 +35,9 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="vitb16_fc1_L128")
+    p.add_argument("--rng", choices=("lfsr", "cbsg"), default="lfsr",
+                   help="comparator source: 32-bit LFSR, or scrambled Sobol-8 with "
+                        "conditional generation of B's stream (C-BSG, L_max <= 256)")
     p.add_argument("--cpu-rows", type=int, default=0,
                    help="rows of A for the oracle sample (0 = size it to ~15 s)")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -92,6 +95,9 @@ def main():
     import workloads as W
 
     w = W.WORKLOADS[args.workload]()
+    rng = scg.SC_RNG_SOBOL8_CBSG if args.rng == "cbsg" else scg.SC_RNG_LFSR32
+    # counter summaries are keyed by workload and comparator source
+    traffic_key = args.workload if args.rng == "lfsr" else args.workload + ":cbsg"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -99,7 +105,8 @@ def main():
     for g in w.gemms:
         t = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (g.A, g.sA, g.B, g.sB, g.L)]
         out = torch.empty((g.batch, g.M, g.N), dtype=torch.float32, device=dev)
-        d = scg.make_desc(t[0], t[2], g.L_max, g.polarity, g.seed, int(round(float(g.L.mean()))))
+        d = scg.make_desc(t[0], t[2], g.L_max, g.polarity, g.seed, int(round(float(g.L.mean()))),
+                          rng)
         ws = scg.Workspace(scg.sc_gemm_workspace_size(d), dev)
         staged.append((g, t, out, ws))
     bitops = w.bitops()
@@ -117,7 +124,7 @@ def main():
             pe = None if pairs is None else (pairs[k][0].cuda_event, pairs[k][1].cuda_event)
             scg.gemm(t[0], t[1], t[2], t[3], t[4], L_max=g.L_max, polarity=g.polarity,
                      seed=g.seed, out=out, workspace=ws, stream=stream, prof_events=pe,
-                     L_hint=int(round(float(g.L.mean()))))
+                     L_hint=int(round(float(g.L.mean()))), rng=rng)
 
     for _ in range(args.warmup):
         step()
@@ -142,22 +149,25 @@ def main():
                              for s in range(nsteps)]))
     g_dom = w.gemms[kidx]
     achieved = g_dom.bitops() / (gemm_ms * 1e-3)
-    traffic = measured_traffic(args.workload)
+    traffic = measured_traffic(traffic_key)
     roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_BITOPS / 1e12,
                 "unit": "Tbitop/s", "frac": achieved / PEAK_BITOPS, "traffic": traffic,
-                "kernel": "k_gemm<bipolar>" if g_dom.polarity == 0 else "k_gemm<unipolar>",
+                "kernel": ("k_gemm<unipolar>" if g_dom.polarity == 1 else
+                           "k_gemm<bipolar-cbsg>" if rng == scg.SC_RNG_SOBOL8_CBSG else
+                           "k_gemm<bipolar>"),
                 "kernel_ms": gemm_ms, "frac_of_single_issue_peak": achieved / PEAK_SINGLE_ISSUE}
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, args.cpu_rows)
+        cpu = cpu_baseline(w, args.cpu_rows, args.rng == "cbsg")
 
     g0 = w.gemms[0]
     cfg = {"workload": w.name, "gemms": [{"name": g.name, "batch": g.batch, "M": g.M, "N": g.N,
                                           "K": g.K, "L_mean": float(g.L.mean()),
                                           "L_max": g.L_max} for g in w.gemms],
            "polarity": "bipolar_xnor" if g0.polarity == 0 else "unipolar_and_sign_magnitude",
-           "rng": "lfsr32", "seed": g0.seed, "bitops_per_step": bitops}
+           "rng": "sobol8_cbsg" if args.rng == "cbsg" else "lfsr32", "seed": g0.seed,
+           "bitops_per_step": bitops}
     line = {"metric": METRIC, "value": value, "unit": "stream-bit-ops/s", "n_gpus": 1,
             "steps": nsteps, "warmup": args.warmup, "ms_per_step": ms_per_step,
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
@@ -165,9 +175,10 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(w, rows):
+def cpu_baseline(w, rows, cbsg=False):
     """The CPU oracle, as it stands, on the first rows of the dominant GEMM."""
     import oracle
+    ref = oracle.sc_gemm_cbsg if cbsg else oracle.sc_gemm
     threads = min(len(os.sched_getaffinity(0)), 16)
     g = max(w.gemms, key=lambda x: x.bitops())
     b = 0
@@ -175,8 +186,8 @@ def cpu_baseline(w, rows):
 
     def run(n):
         t = time.perf_counter()
-        oracle.sc_gemm(g.A[b][:n], g.B[bB], g.sA[b][:n], g.sB[bB], g.L[b][:n], g.L_max,
-                       g.polarity, g.seed, nthreads=threads, want_out=True)
+        ref(g.A[b][:n], g.B[bB], g.sA[b][:n], g.sB[bB], g.L[b][:n], g.L_max,
+            g.polarity, g.seed, nthreads=threads, want_out=True)
         return time.perf_counter() - t
 
     target = 15.0
@@ -192,7 +203,7 @@ def cpu_baseline(w, rows):
     return {"value": ops / dt, "unit": "stream-bit-ops/s", "cores": threads, "kind": "oracle",
             "seconds": dt,
             "sample": "%s/%s rows 0..%d of %d, all %d columns, K=%d, %d stream-bit-ops "
-                      "(B streams materialised inside the timed run)"
+                      "(every stream materialised inside the timed run)"
                       % (w.name, g.name, rows - 1, g.M, g.N, g.K, ops)}
 
 

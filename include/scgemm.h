@@ -31,6 +31,17 @@
  *   unipolar  z = [r_l < beta_u(q)], beta_u(q) = floor((256 |q| + 63) / 127),
  *             sign = (q < 0)
  *
+ * Second comparator source, rng = SC_RNG_SOBOL8_CBSG (Sec. 4.2 "cumulative-indicator
+ * C-BSG" and Sec. A.1 Eq. (4)-(6), readings fixed here): A draws from Sobol dimension 1
+ * (the base-2 radical inverse), B from Sobol dimension 2 (polynomial x + 1, direction
+ * numbers m = 1, 3, 5, 15, 17, 51, 85, 255), both 8-bit, natural order, each XORed with
+ * the digital shift (SplitMix64(2*seed + op) >> 56).  A's stream is its comparator
+ * stream; B's generator is gated by it: B walks r^B with one counter on the cycles
+ * where A emits 1 and another on the cycles where A emits 0, so with
+ * c = #{l < L_i : rA_l < beta_A}, the XNOR count of one element pair is
+ *   #{k < c : rB_k < beta_B} + #{k < L_i - c : rB_k >= beta_B}
+ * and the unipolar AND count is #{k < c : rB_k < beta_uB}.  Needs L_max <= 256.
+ *
  * Memory: every array pointer is a HIP DEVICE pointer; the caller owns all memory.
  * A pointer may be NULL only when its array has no elements (e.g. A when K = 0).
  * The library allocates nothing in sc_gemm and keeps no state between calls; all
@@ -59,9 +70,10 @@ enum {
     SC_OK = 0,
     SC_ERR_NULL = -1,          /* a required pointer is NULL */
     SC_ERR_SHAPE = -2,         /* batch, M, N or K negative, or K > SC_K_LIMIT */
-    SC_ERR_LEN = -3,           /* L_max outside [1, SC_L_MAX_LIMIT], or L_hint outside [0, L_max] */
+    SC_ERR_LEN = -3,           /* L_max outside [1, SC_L_MAX_LIMIT] ([1, 256] for C-BSG),
+                                  or L_hint outside [0, L_max] */
     SC_ERR_POLARITY = -4,      /* polarity not one of SC_BIPOLAR_XNOR / SC_UNIPOLAR_AND_SM */
-    SC_ERR_RNG = -5,           /* rng not SC_RNG_LFSR32 (or op not 0/1) */
+    SC_ERR_RNG = -5,           /* rng not one of SC_RNG_* (or op not 0/1) */
     SC_ERR_WORKSPACE = -6,     /* workspace NULL or smaller than sc_gemm_workspace_size() */
     SC_ERR_HIP = -7,           /* a HIP runtime call or kernel launch failed */
     SC_ERR_DEVICE_STATUS = -8, /* (sc_gemm_status) some L_i was outside [0, L_max] */
@@ -69,7 +81,7 @@ enum {
 };
 
 enum { SC_BIPOLAR_XNOR = 0, SC_UNIPOLAR_AND_SM = 1 };
-enum { SC_RNG_LFSR32 = 0 };
+enum { SC_RNG_LFSR32 = 0, SC_RNG_SOBOL8_CBSG = 1 };
 
 #define SC_L_MAX_LIMIT 4096     /* largest supported stream length */
 #define SC_K_LIMIT (1 << 20)    /* largest inner dimension (counts stay exact in int32) */
@@ -83,7 +95,7 @@ typedef struct sc_gemm_desc {
     int64_t strideL;                     /* batch stride of L_per_row (M) */
     int32_t L_max;              /* 1..SC_L_MAX_LIMIT; every L_i must lie in [0, L_max] */
     int32_t polarity;           /* SC_BIPOLAR_XNOR or SC_UNIPOLAR_AND_SM */
-    int32_t rng;                /* SC_RNG_LFSR32 */
+    int32_t rng;                /* SC_RNG_LFSR32 or SC_RNG_SOBOL8_CBSG */
     int32_t L_hint;             /* optional expected mean of the L_i (0 = unknown, taken as
                                    L_max); only tunes how GEMM tiles are split over the
                                    compute units, never changes a result; 0..L_max */
@@ -126,12 +138,14 @@ int sc_gemm(const sc_gemm_desc *desc,
 int sc_gemm_status(const void *workspace, void *stream);
 
 /*
- * The comparator sequence r_0 .. r_{n-1} of operand `op` (0 = A, 1 = B) for `seed`,
- * computed on the device exactly as sc_gemm computes it (Sec. 3.1 "Bitstream
- * generation"; LFSR of Sec. A.1 under the reading above).  `out` is a device
- * buffer of n bytes.  1 <= n <= SC_L_MAX_LIMIT.  Asynchronous on `stream`.
+ * The comparator sequence r_0 .. r_{n-1} of operand `op` (0 = A, 1 = B) for `seed`
+ * and source `rng`, computed on the device exactly as sc_gemm computes it (Sec. 3.1
+ * "Bitstream generation"; LFSR or scrambled Sobol-8 of Sec. A.1 under the readings
+ * above).  `out` is a device buffer of n bytes.  1 <= n <= SC_L_MAX_LIMIT (<= 256 for
+ * SC_RNG_SOBOL8_CBSG).  Asynchronous on `stream`.
  */
-int sc_comparator_sequence(uint64_t seed, int32_t op, int32_t n, uint8_t *out, void *stream);
+int sc_comparator_sequence(uint64_t seed, int32_t op, int32_t rng, int32_t n, uint8_t *out,
+                           void *stream);
 
 /*
  * Symmetric int8 quantisation of fp32 rows, the input preparation the SC GEMM takes

@@ -10,14 +10,14 @@ back to the CPU: without the built library every call raises.
 from __future__ import annotations
 
 from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_L_MAX_LIMIT, SC_OK,  # noqa: F401
-                   SC_RNG_LFSR32, SC_UNIPOLAR_AND_SM, ScError, ScGemmDesc, load, sc_comparator_sequence,
+                   SC_RNG_LFSR32, SC_RNG_SOBOL8_CBSG, SC_UNIPOLAR_AND_SM, ScError, ScGemmDesc, load, sc_comparator_sequence,
                    sc_gemm, sc_gemm_status, sc_gemm_workspace_size, sc_mp_lengths, sc_quantize,
                    sc_version, strerror)
 
 __all__ = ["gemm", "make_desc", "comparator_sequence", "quantize", "mp_lengths", "Workspace",
            "ScGemmDesc", "ScError", "sc_gemm", "sc_gemm_workspace_size", "sc_gemm_status",
            "sc_comparator_sequence", "sc_quantize", "sc_mp_lengths", "SC_BIPOLAR_XNOR",
-           "SC_UNIPOLAR_AND_SM"]
+           "SC_UNIPOLAR_AND_SM", "SC_RNG_LFSR32", "SC_RNG_SOBOL8_CBSG"]
 
 
 def _stream_handle(stream):
@@ -26,7 +26,8 @@ def _stream_handle(stream):
     return int(s.cuda_stream)
 
 
-def make_desc(A, B, L_max: int, polarity: int, seed: int, L_hint: int = 0) -> ScGemmDesc:
+def make_desc(A, B, L_max: int, polarity: int, seed: int, L_hint: int = 0,
+              rng: int = SC_RNG_LFSR32) -> ScGemmDesc:
     """Descriptor for contiguous A [batch, M, K] and B [batch or 1, N, K] tensors."""
     if A.dim() == 2:
         A = A.unsqueeze(0)
@@ -41,7 +42,7 @@ def make_desc(A, B, L_max: int, polarity: int, seed: int, L_hint: int = 0) -> Sc
     d.lda, d.ldb, d.ldo = K, K, N
     d.strideA, d.strideB, d.strideO = M * K, (N * K if nb == batch and batch > 1 else 0), M * N
     d.strideSA, d.strideSB, d.strideL = M, (N if nb == batch and batch > 1 else 0), M
-    d.L_max, d.polarity, d.rng, d.L_hint, d.seed = int(L_max), int(polarity), SC_RNG_LFSR32, int(L_hint), int(seed)
+    d.L_max, d.polarity, d.rng, d.L_hint, d.seed = int(L_max), int(polarity), int(rng), int(L_hint), int(seed)
     return d
 
 
@@ -63,17 +64,20 @@ class Workspace:
 
 def gemm(A, sA, B, sB, L, *, L_max: int, polarity: int = SC_BIPOLAR_XNOR, seed: int = 0,
          out=None, counts=None, want_counts: bool = False, workspace: Workspace = None,
-         stream=None, check_status: bool = False, prof_events=None, L_hint: int = 0):
+         stream=None, check_status: bool = False, prof_events=None, L_hint: int = 0,
+         rng: int = SC_RNG_LFSR32):
     """SC GEMM on torch device tensors.
 
     A int8 [batch, M, K] (or [M, K]), sA float32 [batch, M], B int8 [batch or 1, N, K],
-    sB float32 [batch or 1, N], L int32 [batch, M].  Returns (out, counts or None).
+    sB float32 [batch or 1, N], L int32 [batch, M].  ``rng`` selects the comparator
+    source (LFSR, or Sobol-8 with conditional generation of B, L_max <= 256).
+    Returns (out, counts or None).
     """
     import torch
     squeeze = A.dim() == 2
     A3 = A.unsqueeze(0) if A.dim() == 2 else A
     B3 = B.unsqueeze(0) if B.dim() == 2 else B
-    d = make_desc(A3, B3, L_max, polarity, seed, L_hint)
+    d = make_desc(A3, B3, L_max, polarity, seed, L_hint, rng)
     for t, name in ((A3, "A"), (B3, "B"), (sA, "sA"), (sB, "sB"), (L, "L")):
         if not t.is_cuda or not t.is_contiguous():
             raise ValueError("%s must be a contiguous device tensor" % name)
@@ -107,11 +111,11 @@ def gemm(A, sA, B, sB, L, *, L_max: int, polarity: int = SC_BIPOLAR_XNOR, seed: 
     return out, counts
 
 
-def comparator_sequence(seed: int, op: int, n: int, stream=None):
+def comparator_sequence(seed: int, op: int, n: int, stream=None, rng: int = SC_RNG_LFSR32):
     """Device comparator sequence r_0..r_{n-1} (uint8 tensor) of operand ``op``."""
     import torch
     out = torch.empty(n, dtype=torch.uint8, device="cuda")
-    rc = sc_comparator_sequence(seed, op, n, out.data_ptr(), _stream_handle(stream))
+    rc = sc_comparator_sequence(seed, op, rng, n, out.data_ptr(), _stream_handle(stream))
     if rc != SC_OK:
         raise ScError(rc, "sc_comparator_sequence")
     return out

@@ -26,6 +26,7 @@ SC_ERR_STRIDE = -9
 SC_BIPOLAR_XNOR = 0
 SC_UNIPOLAR_AND_SM = 1
 SC_RNG_LFSR32 = 0
+SC_RNG_SOBOL8_CBSG = 1
 SC_L_MAX_LIMIT = 4096
 SC_K_LIMIT = 1 << 20
 
@@ -83,7 +84,7 @@ def load():
     lib.sc_gemm.restype = ctypes.c_int
     lib.sc_gemm_status.argtypes = [vp, vp]
     lib.sc_gemm_status.restype = ctypes.c_int
-    lib.sc_comparator_sequence.argtypes = [u64, i32, i32, vp, vp]
+    lib.sc_comparator_sequence.argtypes = [u64, i32, i32, i32, vp, vp]
     lib.sc_comparator_sequence.restype = ctypes.c_int
     f32p = ctypes.POINTER(ctypes.c_float)
     i32p = ctypes.POINTER(ctypes.c_int32)
@@ -123,8 +124,8 @@ def sc_gemm_status(workspace: int, stream: int) -> int:
     return int(load().sc_gemm_status(workspace, stream or None))
 
 
-def sc_comparator_sequence(seed: int, op: int, n: int, out: int, stream: int) -> int:
-    return int(load().sc_comparator_sequence(ctypes.c_uint64(seed), op, n, out, stream or None))
+def sc_comparator_sequence(seed: int, op: int, rng: int, n: int, out: int, stream: int) -> int:
+    return int(load().sc_comparator_sequence(ctypes.c_uint64(seed), op, rng, n, out, stream or None))
 
 
 def sc_quantize(batch: int, rows: int, K: int, X: int, ldx: int, strideX: int, per_tensor: int,

@@ -28,7 +28,10 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.LP = (int)round_up(d.L_max, LSTEP);
     l.nbB = (d.strideB == 0) ? 1 : d.batch;
     if (l.nbB < 1) l.nbB = 1;
+    const bool cbsg = d.rng == SC_RNG_SOBOL8_CBSG;
     const bool uni = d.polarity == SC_UNIPOLAR_AND_SM;
+    l.mode = uni ? MODE_SIGNED : (cbsg ? MODE_CBSG : MODE_AND);
+    const bool signsA = l.mode != MODE_AND, signsB = uni, needRB = l.mode == MODE_AND;
 
     // the status word is always the first word of the workspace
     size_t off = 0;
@@ -38,6 +41,8 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     off = align256(off + (size_t)l.LBS * 4);
     l.off_rB = off;
     off = align256(off + (size_t)l.LBS * 4);
+    l.off_CA = off;
+    if (cbsg) off = align256(off + (size_t)(d.L_max + 1) * CA_COLS * 2);
 
     // one A block per batch entry
     const size_t rowsA = (size_t)l.MT * BM;
@@ -56,7 +61,7 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     if (!mul_ok(rowsA * (size_t)l.KB, (size_t)l.LP * 4, &sz)) return false;
     a = align256(a + sz);
     l.off_SA = a;
-    if (uni) a = align256(a + rowsA * (size_t)l.KB * 4);
+    if (signsA) a = align256(a + rowsA * (size_t)l.KB * 4);
     l.stride_batchA = a;
     const size_t baseA = off;
     size_t totA;
@@ -70,9 +75,9 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     if (!mul_ok(rowsB * (size_t)l.KB, (size_t)l.LBS * 4, &sz)) return false;
     bb = align256(bb + sz);
     l.off_SB = bb;
-    if (uni) bb = align256(bb + rowsB * (size_t)l.KB * 4);
+    if (signsB) bb = align256(bb + rowsB * (size_t)l.KB * 4);
     l.off_RB = bb;
-    if (!uni) bb = align256(bb + (size_t)d.N * (size_t)(d.L_max + 1) * 4);
+    if (needRB) bb = align256(bb + (size_t)d.N * (size_t)(d.L_max + 1) * 4);
     l.stride_batchB = bb;
     const size_t baseB = off;
     size_t totB;
@@ -133,7 +138,8 @@ static int check_desc(const sc_gemm_desc *d) {
     // counts 2*X and K*L must stay exact in int32
     if ((int64_t)d->K * d->L_max > (1ll << 29)) return SC_ERR_SHAPE;
     if (d->polarity != SC_BIPOLAR_XNOR && d->polarity != SC_UNIPOLAR_AND_SM) return SC_ERR_POLARITY;
-    if (d->rng != SC_RNG_LFSR32) return SC_ERR_RNG;
+    if (d->rng != SC_RNG_LFSR32 && d->rng != SC_RNG_SOBOL8_CBSG) return SC_ERR_RNG;
+    if (d->rng == SC_RNG_SOBOL8_CBSG && d->L_max > CBSG_L_MAX) return SC_ERR_LEN;
     if (d->L_hint < 0 || d->L_hint > d->L_max) return SC_ERR_LEN;
     if (d->lda < d->K || d->ldb < d->K || d->ldo < d->N) return SC_ERR_STRIDE;
     if (d->strideA < 0 || d->strideB < 0 || d->strideO < 0 || d->strideSA < 0 || d->strideSB < 0 ||
@@ -156,14 +162,16 @@ using namespace scg;
 
 extern "C" {
 
-int sc_version(void) { return 10000; }
+int sc_version(void) { return 10100; }
 
 const char *sc_strerror(int code) {
     switch (code) {
         case SC_OK: return "SC_OK";
         case SC_ERR_NULL: return "SC_ERR_NULL: a required pointer is NULL";
         case SC_ERR_SHAPE: return "SC_ERR_SHAPE: bad batch/M/N/K (or K*L_max too large)";
-        case SC_ERR_LEN: return "SC_ERR_LEN: L_max outside [1, SC_L_MAX_LIMIT] or L_hint outside [0, L_max]";
+        case SC_ERR_LEN:
+            return "SC_ERR_LEN: L_max outside [1, SC_L_MAX_LIMIT] ([1, 256] for C-BSG) or L_hint "
+                   "outside [0, L_max]";
         case SC_ERR_POLARITY: return "SC_ERR_POLARITY: unknown polarity";
         case SC_ERR_RNG: return "SC_ERR_RNG: unknown rng or operand index";
         case SC_ERR_WORKSPACE: return "SC_ERR_WORKSPACE: workspace missing or too small";
@@ -204,15 +212,18 @@ int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const in
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
     uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
 
-    hipError_t e = launch_draws(d.seed, lay.LBS, reinterpret_cast<uint32_t *>(ws + lay.off_rA),
+    uint32_t *rA = reinterpret_cast<uint32_t *>(ws + lay.off_rA);
+    hipError_t e = launch_draws(d.seed, d.rng, lay.LBS, rA,
                                 reinterpret_cast<uint32_t *>(ws + lay.off_rB), nullptr, -1,
                                 reinterpret_cast<uint32_t *>(ws + lay.off_status), st);
     if (e != hipSuccess) return SC_ERR_HIP;
     if (d.batch == 0 || d.M == 0 || d.N == 0) return SC_OK;
 
+    if (d.rng == SC_RNG_SOBOL8_CBSG &&
+        launch_cbsg_table(rA, d.L_max, reinterpret_cast<uint16_t *>(ws + lay.off_CA), st) != hipSuccess)
+        return SC_ERR_HIP;
     if ((e = launch_schedule(d, lay, L_per_row, ws, st)) != hipSuccess) return SC_ERR_HIP;
-    if (d.polarity == SC_BIPOLAR_XNOR &&
-        (e = launch_marginals(d, lay, A, B, ws, st)) != hipSuccess)
+    if (lay.mode == MODE_AND && (e = launch_marginals(d, lay, A, B, ws, st)) != hipSuccess)
         return SC_ERR_HIP;
     if ((e = launch_planes(d, lay, A, B, ws, st)) != hipSuccess) return SC_ERR_HIP;
     if (d.prof_event_begin != nullptr &&
@@ -278,12 +289,15 @@ int sc_mp_lengths(int32_t batch, int32_t M, const float *metric, int64_t strideM
     return SC_OK;
 }
 
-int sc_comparator_sequence(uint64_t seed, int32_t op, int32_t n, uint8_t *out, void *stream) {
+int sc_comparator_sequence(uint64_t seed, int32_t op, int32_t rng, int32_t n, uint8_t *out,
+                           void *stream) {
     if (out == nullptr) return SC_ERR_NULL;
-    if (op != 0 && op != 1) return SC_ERR_RNG;
-    if (n < 1 || n > SC_L_MAX_LIMIT) return SC_ERR_LEN;
+    if ((op != 0 && op != 1) || (rng != SC_RNG_LFSR32 && rng != SC_RNG_SOBOL8_CBSG))
+        return SC_ERR_RNG;
+    if (n < 1 || n > (rng == SC_RNG_SOBOL8_CBSG ? CBSG_L_MAX : SC_L_MAX_LIMIT)) return SC_ERR_LEN;
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-    if (launch_draws(seed, n, nullptr, nullptr, out, op, nullptr, st) != hipSuccess) return SC_ERR_HIP;
+    if (launch_draws(seed, rng, n, nullptr, nullptr, out, op, nullptr, st) != hipSuccess)
+        return SC_ERR_HIP;
     return SC_OK;
 }
 

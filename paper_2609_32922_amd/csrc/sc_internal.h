@@ -2,24 +2,27 @@
 //
 // Data layout in device memory (all inside the caller's workspace):
 //
-//   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
 //   status     one uint32 (bit 0: some L_i out of range)
+//   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
+//   CA         C-BSG only: CA[L][beta] = #{l < L : rA_l < beta}, uint16 [L_max+1][257]
 //   per batch entry b of A (batch entries):
 //     perm[MT*BM]      sorted position -> original row (or -1 for padding)
 //     Ls[MT*BM]        stream length at each sorted position
-//     RA[MT*BM]        row marginal  sum_d sum_{l<L} zA   (bipolar)
+//     RA[MT*BM]        row marginal  sum_d sum_{l<L} zA   (bipolar, both sequences)
 //     tileL[MT]        cycles the GEMM runs for row tile t (max L in tile, padded to 4)
 //     tileOff[MT]      word offset of tile t's planes inside Ap
 //     Ap               bit planes of A: for tile t, words [KB][tileL[t]][BM]
-//     SA               sign planes of A (unipolar): [MT][KB][BM]
+//     SA               sign planes of A (unipolar; bipolar C-BSG): [MT][KB][BM]
 //   part       partial counts when GEMM tiles are split along the element blocks
 //   per batch entry of B (1 if B is broadcast, else batch entries):
 //     Bp               bit planes of B: [NT][KB][LBS][BN]
 //     SB               sign planes of B (unipolar): [NT][KB][BN]
 //     RB               prefix marginals RB[j][L] = sum_d sum_{l<L} zB, L = 0..L_max
+//                      (bipolar with the LFSR sequence only)
 //
 // A "bit plane" word packs 32 consecutive inner-dimension elements d = 32*kb .. 32*kb+31
-// of one row at one cycle l: bit t = z[row][32*kb + t][l].
+// of one row at one cycle l: bit t = z[row][32*kb + t][l].  With C-BSG the planes of A
+// are indexed by B's draw counter k instead of the cycle (see k_planes).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -37,6 +40,13 @@ constexpr int LCH = 32;          // cycles per LDS stage and per plane-generatio
 constexpr uint32_t STATUS_BAD_LENGTH = 1u;
 constexpr int CUS = 256;         // compute units of an MI355X (work-unit balancing target)
 constexpr int MAX_SPLIT = 8;
+constexpr int CBSG_L_MAX = 256;  // one period of the 8-bit Sobol sequences
+constexpr int CA_COLS = 257;     // boundaries 0..256
+
+// counting modes of the GEMM hot loop and its decode
+constexpr int MODE_AND = 0;      // bipolar, LFSR: AND counts plus both marginals
+constexpr int MODE_SIGNED = 1;   // unipolar: popc((a & b) ^ sA ^ sB), signed AND counts
+constexpr int MODE_CBSG = 2;     // bipolar C-BSG: popc((D & Z) ^ sA) plus A's marginal
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -46,7 +56,8 @@ struct Layout {
     int LBS;           // cycle stride of B planes and length of draw arrays (L_max rounded to LCH)
     int LP;            // L_max rounded up to LSTEP
     int nbB;           // batch entries of B planes (1 when B is broadcast)
-    size_t off_rA, off_rB, off_status;
+    int mode;          // MODE_AND, MODE_SIGNED or MODE_CBSG
+    size_t off_rA, off_rB, off_status, off_CA;
     size_t off_perm, off_Ls, off_RA, off_tileL, off_tileOff, off_Ap, off_SA;
     size_t stride_batchA;          // bytes per A batch entry block
     size_t off_Bp, off_SB, off_RB;
@@ -60,8 +71,9 @@ struct Layout {
 bool make_layout(const sc_gemm_desc &d, Layout *lay);
 
 // Kernel launchers (sc_kernels.hip).  All return hipSuccess or the launch error.
-hipError_t launch_draws(uint64_t seed, int n, uint32_t *rA, uint32_t *rB, uint8_t *bytes_out,
-                        int op_only, uint32_t *status, hipStream_t st);
+hipError_t launch_draws(uint64_t seed, int rng, int n, uint32_t *rA, uint32_t *rB,
+                        uint8_t *bytes_out, int op_only, uint32_t *status, hipStream_t st);
+hipError_t launch_cbsg_table(const uint32_t *rA, int L_max, uint16_t *CA, hipStream_t st);
 hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L,
                            uint8_t *ws, hipStream_t st);
 hipError_t launch_marginals(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,

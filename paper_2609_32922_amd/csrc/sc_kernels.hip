@@ -2,7 +2,9 @@
 //
 // Pipeline of one sc_gemm call (all on the caller's stream):
 //   k_draws      comparator sequences r^A, r^B (Sec. 3.1 "Bitstream generation",
-//                LFSR of Sec. A.1) -- one lane per cycle via LFSR jump-ahead
+//                LFSR or scrambled Sobol-8 of Sec. A.1) -- one lane per cycle, the LFSR
+//                through jump-ahead
+//   k_cbsg_table C-BSG only: CA[L][beta] = ones of A's stream in its first L cycles
 //   k_schedule   per-row length scheduler: validates L_i, counting-sorts rows by L
 //                (descending) so that a 128-row tile runs for the longest length it
 //                holds (Sec. 4.2: "row i stops at l_i"; Sec. 4.1 cost ~ sum of l_i)
@@ -10,7 +12,7 @@
 //   k_planes     comparator stream generation into packed bit planes (one word =
 //                32 inner-dimension elements at one cycle); 64 lanes compare one
 //                row's 64 elements against r_l in one v_cmp, the wave ballot is the
-//                packed word
+//                packed word.  With C-BSG, A's planes are intervals of B's counter.
 //   k_gemm       tiled AND/bitop3 + popcount over (d, l), int32 accumulators, and the
 //                Eq. (1) decode epilogue in the original row order
 //
@@ -19,6 +21,14 @@
 // is one AND and one popcount per 32 bit pairs and A's planes can be zero beyond L_i.
 // Unipolar sign-magnitude counts use popc((a & b) ^ sigma) with sigma = signA ^ signB
 // per 32 elements, which equals the signed AND count plus popc(sigma) per cycle.
+//
+// C-BSG (Sec. 4.2, Eq. (6)): with c = ones of A's stream over the row's L cycles and
+// Z_k = [rB_k < beta_B], one element pair contributes
+//   sum_k [k < c] Z_k + [k < L - c] (1 - Z_k) = (L - c) + sgn * sum_k D_k Z_k,
+// D_k = [min(c, L-c) <= k < max(c, L-c)], sgn = -1 if c < L - c else +1,
+// so the bipolar C-BSG counts run the same signed hot loop as unipolar, with A's
+// planes holding D and A's signs holding sgn, plus the marginal K L - sum_d c.
+// Unipolar C-BSG is the plain signed loop with A's planes holding [k < c].
 #include "sc_internal.h"
 
 namespace scg {
@@ -66,20 +76,48 @@ __device__ __forceinline__ uint32_t gf2_mulmod(uint32_t a, uint32_t b) {
     return acc;
 }
 
-__global__ __launch_bounds__(256) void k_draws(uint64_t seed, int n, uint32_t *rA, uint32_t *rB,
-                                               uint8_t *bytes_out, int op_only, uint32_t *status) {
+// 8-bit Sobol direction numbers V_j = m_j 2^(8-j), j = 1..8: dimension 1 has m_j = 1;
+// dimension 2 comes from the primitive polynomial x + 1, whose recurrence is
+// m_j = m_{j-1} xor 2 m_{j-1} from m_1 = 1.
+struct SobolDirs {
+    uint32_t v[2][8];
+};
+constexpr SobolDirs make_sobol_dirs() {
+    SobolDirs t{};
+    uint32_t m = 1u;
+    for (int j = 1; j <= 8; ++j) {
+        t.v[0][j - 1] = 1u << (8 - j);
+        if (j > 1) m = m ^ (m << 1);
+        t.v[1][j - 1] = m << (8 - j);
+    }
+    return t;
+}
+__constant__ SobolDirs kSobol = make_sobol_dirs();
+
+__global__ __launch_bounds__(256) void k_draws(uint64_t seed, int rng, int n, uint32_t *rA,
+                                               uint32_t *rB, uint8_t *bytes_out, int op_only,
+                                               uint32_t *status) {
     const int l = blockIdx.x * blockDim.x + threadIdx.x;
     const int op = op_only >= 0 ? op_only : (int)blockIdx.y;
     if (status != nullptr && l == 0 && blockIdx.y == 0) *status = 0u;
     if (l >= n) return;
-    uint32_t s0 = (uint32_t)(splitmix64(2ull * seed + (uint64_t)op) >> 32);
-    if (s0 == 0u) s0 = 1u;
-    uint32_t s = gf2_mulmod(s0, kJump.v[l]);
+    const uint64_t h = splitmix64(2ull * seed + (uint64_t)op);
     uint32_t v = 0;
+    if (rng == SC_RNG_SOBOL8_CBSG) {
+        // point l (< 256) of dimension op + 1, digitally shifted by the top 8 bits of h
+        v = (uint32_t)(h >> 56);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-        v = (v << 1) | (s & 1u);
-        s = (s >> 1) ^ ((s & 1u) ? kFeedback : 0u);
+        for (int j = 0; j < 8; ++j)
+            if ((l >> j) & 1) v ^= kSobol.v[op][j];
+    } else {
+        uint32_t s0 = (uint32_t)(h >> 32);
+        if (s0 == 0u) s0 = 1u;
+        uint32_t s = gf2_mulmod(s0, kJump.v[l]);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            v = (v << 1) | (s & 1u);
+            s = (s >> 1) ^ ((s & 1u) ? kFeedback : 0u);
+        }
     }
     if (bytes_out != nullptr)
         bytes_out[l] = (uint8_t)v;
@@ -87,10 +125,33 @@ __global__ __launch_bounds__(256) void k_draws(uint64_t seed, int n, uint32_t *r
         (op == 0 ? rA : rB)[l] = v;
 }
 
-hipError_t launch_draws(uint64_t seed, int n, uint32_t *rA, uint32_t *rB, uint8_t *bytes_out,
-                        int op_only, uint32_t *status, hipStream_t st) {
+hipError_t launch_draws(uint64_t seed, int rng, int n, uint32_t *rA, uint32_t *rB,
+                        uint8_t *bytes_out, int op_only, uint32_t *status, hipStream_t st) {
     dim3 grid((unsigned)((n + 255) / 256), op_only >= 0 ? 1u : 2u);
-    hipLaunchKernelGGL(k_draws, grid, dim3(256), 0, st, seed, n, rA, rB, bytes_out, op_only, status);
+    hipLaunchKernelGGL(k_draws, grid, dim3(256), 0, st, seed, rng, n, rA, rB, bytes_out, op_only,
+                       status);
+    return hipGetLastError();
+}
+
+// CA[L][beta] = #{l < L : rA_l < beta} for L = 0..L_max, beta = 0..256 (one thread per
+// boundary; L_max <= 256 draws staged in LDS)
+__global__ __launch_bounds__(320) void k_cbsg_table(const uint32_t *__restrict__ rA, int L_max,
+                                                    uint16_t *__restrict__ CA) {
+    __shared__ uint32_t r[CBSG_L_MAX];
+    const int beta = threadIdx.x;
+    for (int l = threadIdx.x; l < L_max; l += blockDim.x) r[l] = rA[l];
+    __syncthreads();
+    if (beta >= CA_COLS) return;
+    uint32_t c = 0;
+    for (int l = 0; l < L_max; ++l) {
+        CA[(size_t)l * CA_COLS + beta] = (uint16_t)c;
+        c += r[l] < (uint32_t)beta ? 1u : 0u;
+    }
+    CA[(size_t)L_max * CA_COLS + beta] = (uint16_t)c;
+}
+
+hipError_t launch_cbsg_table(const uint32_t *rA, int L_max, uint16_t *CA, hipStream_t st) {
+    hipLaunchKernelGGL(k_cbsg_table, dim3(1), dim3(320), 0, st, rA, L_max, CA);
     return hipGetLastError();
 }
 
@@ -170,6 +231,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     uint8_t *wsb = ws + (size_t)b * lay.stride_batchA;
     int32_t *perm = ws_ptr<int32_t>(wsb, lay.off_perm);
     int32_t *Ls = ws_ptr<int32_t>(wsb, lay.off_Ls);
+    int32_t *RA = ws_ptr<int32_t>(wsb, lay.off_RA);     // zeroed here, summed by C-BSG planes
     int32_t *tileL = ws_ptr<int32_t>(wsb, lay.off_tileL);
     int64_t *tileOff = ws_ptr<int64_t>(wsb, lay.off_tileOff);
     uint32_t *status = ws_ptr<uint32_t>(ws, lay.off_status);
@@ -203,10 +265,12 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         const int pos = atomicAdd(&hist[l], 1);
         perm[pos] = i;
         Ls[pos] = l;
+        RA[pos] = 0;
     }
     for (int p = M + tid; p < lay.MT * BM; p += 1024) {
         perm[p] = -1;
         Ls[p] = 0;
+        RA[p] = 0;
     }
     __threadfence_block();
     __syncthreads();
@@ -328,12 +392,24 @@ struct PlaneArgs {
     size_t stride_batch;        // bytes between batch entries of the workspace block
     size_t off_perm, off_Ls, off_tileL, off_tileOff;   // 0 = not used (B side)
     size_t off_planes, off_signs, off_r;
+    size_t off_CA, off_RA;      // C-BSG (A side): count table, row marginal
     int per_row;                // 1: A side (sorted rows, per-row lengths)
     int LBS;                    // B side: cycle stride of the planes
 };
 
-template <int POL>
+// One block covers one 128-row tile, LCH cycles and 64 elements (two plane words per
+// row and cycle).  Each wave takes 32 rows; its 64 lanes are the 64 elements.
+//
+// Comparator mode (CBSG = false): bit of element d at cycle l is [r_l < beta_d] for
+// l < L_row.  Sign planes (unipolar) hold [q_d < 0].
+//
+// C-BSG mode (CBSG = true, A side only): A's planes are indexed by B's draw counter k.
+// With c_d = CA[L_row][beta_d] the bit is [lo_d <= k < hi_d]: [0, c_d) for unipolar,
+// [min(c_d, L-c_d), max(c_d, L-c_d)) for bipolar, whose sign planes hold [c_d < L - c_d]
+// and whose blocks of the first cycle chunk add sum_d c_d into RA.
+template <int POL, bool CBSG>
 __global__ __launch_bounds__(256) void k_planes(PlaneArgs a, uint8_t *ws) {
+    constexpr bool SIGNS = POL == SC_UNIPOLAR_AND_SM || CBSG;
     __shared__ uint32_t T[2][LCH][BM + 1];
     const int t = blockIdx.x / a.nchunk, ch = blockIdx.x % a.nchunk;
     const int dp = blockIdx.y, b = blockIdx.z;
@@ -357,13 +433,17 @@ __global__ __launch_bounds__(256) void k_planes(PlaneArgs a, uint8_t *ws) {
     if (l0 >= Lloop) return;
     const int nl = min(LCH, Lloop - l0);
     uint32_t *planes = ws_ptr<uint32_t>(wsb, a.off_planes) + off;
-    uint32_t *signs = POL == SC_UNIPOLAR_AND_SM ? ws_ptr<uint32_t>(wsb, a.off_signs) : nullptr;
+    uint32_t *signs = SIGNS ? ws_ptr<uint32_t>(wsb, a.off_signs) : nullptr;
+    const uint16_t *CA = CBSG ? ws_ptr<uint16_t>(ws, a.off_CA) : nullptr;
+    int32_t *RA = CBSG && POL == SC_BIPOLAR_XNOR ? ws_ptr<int32_t>(wsb, a.off_RA) : nullptr;
     const int8_t *Xb = a.X + (size_t)b * a.strideX;
     const int d = dp * 64 + lane;
     // the chunk's 32 comparator draws, loaded once (l0 + 31 < LBS, the draw count)
     int rr[LCH];
+    if (!CBSG) {
 #pragma unroll
-    for (int l = 0; l < LCH; ++l) rr[l] = wave_uniform((int)r[l0 + l]);
+        for (int l = 0; l < LCH; ++l) rr[l] = wave_uniform((int)r[l0 + l]);
+    }
 
     for (int k = 0; k < 32; ++k) {
         const int m = w * 32 + k;
@@ -379,20 +459,44 @@ __global__ __launch_bounds__(256) void k_planes(PlaneArgs a, uint8_t *ws) {
         const bool valid = row >= 0 && d < a.K;
         const int q = valid ? (int)Xb[(size_t)row * a.ld + d] : 0;
         const int beta = valid ? (POL == SC_BIPOLAR_XNOR ? beta_bipolar(q) : beta_unipolar(q)) : 0;
-        const int lrem = Lr - l0;          // cycles of this row left in the chunk
         uint32_t word = 0;
+        bool neg = valid && q < 0;
+        if (CBSG) {
+            const int c = valid ? (int)CA[(size_t)Lr * CA_COLS + beta] : 0;
+            int lo = 0, hi = c;
+            if (POL == SC_BIPOLAR_XNOR) {
+                const int e = Lr - c;
+                lo = min(c, e);
+                hi = max(c, e);
+                neg = valid && c < e;
+                if (ch == 0) {
+                    const int sc = wave_sum(c);
+                    if (lane == 0 && sc != 0) atomicAdd(&RA[p], sc);
+                }
+            }
+            const uint32_t width = (uint32_t)(valid ? hi - lo : 0);
 #pragma unroll
-        for (int l = 0; l < LCH; ++l) {
-            // a cycle past the row's length compares against 256: never a one
-            const int thr = wave_uniform(l < lrem ? rr[l] : 256);
-            const uint64_t m64 = __ballot(thr < beta);
-            // lane l receives cycle l of the first 32 elements, lane 32+l of the next 32
-            word = (uint32_t)writelane_i32((int)(uint32_t)m64, l, (int)word);
-            word = (uint32_t)writelane_i32((int)(uint32_t)(m64 >> 32), l + 32, (int)word);
+            for (int l = 0; l < LCH; ++l) {
+                // counter index l0 + l inside [lo, hi); beyond the row's length hi <= L
+                const uint64_t m64 = __ballot((uint32_t)(l0 + l - lo) < width);
+                word = (uint32_t)writelane_i32((int)(uint32_t)m64, l, (int)word);
+                word = (uint32_t)writelane_i32((int)(uint32_t)(m64 >> 32), l + 32, (int)word);
+            }
+        } else {
+            const int lrem = Lr - l0;          // cycles of this row left in the chunk
+#pragma unroll
+            for (int l = 0; l < LCH; ++l) {
+                // a cycle past the row's length compares against 256: never a one
+                const int thr = wave_uniform(l < lrem ? rr[l] : 256);
+                const uint64_t m64 = __ballot(thr < beta);
+                // lane l receives cycle l of the first 32 elements, lane 32+l of the next 32
+                word = (uint32_t)writelane_i32((int)(uint32_t)m64, l, (int)word);
+                word = (uint32_t)writelane_i32((int)(uint32_t)(m64 >> 32), l + 32, (int)word);
+            }
         }
         T[lane >> 5][lane & 31][m] = word;
-        if (POL == SC_UNIPOLAR_AND_SM && ch == 0) {
-            const uint64_t s64 = __ballot(valid && q < 0);
+        if (SIGNS && ch == 0) {
+            const uint64_t s64 = __ballot(neg);
             if (lane == 0) {
                 const size_t so = ((size_t)t * a.KB + 2 * dp) * 128 + m;
                 signs[so] = (uint32_t)s64;
@@ -418,10 +522,20 @@ __global__ __launch_bounds__(256) void k_planes(PlaneArgs a, uint8_t *ws) {
     }
 }
 
+template <bool CBSG>
+static void launch_planes_side(int polarity, dim3 grid, const PlaneArgs &pa, uint8_t *ws,
+                               hipStream_t st) {
+    if (polarity == SC_BIPOLAR_XNOR)
+        hipLaunchKernelGGL((k_planes<SC_BIPOLAR_XNOR, CBSG>), grid, dim3(256), 0, st, pa, ws);
+    else
+        hipLaunchKernelGGL((k_planes<SC_UNIPOLAR_AND_SM, CBSG>), grid, dim3(256), 0, st, pa, ws);
+}
+
 hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
                          uint8_t *ws, hipStream_t st) {
     const int dpairs = (lay.KB + 1) / 2;
     if (dpairs == 0) return hipSuccess;
+    const bool cbsg = d.rng == SC_RNG_SOBOL8_CBSG;
     PlaneArgs pa{};
     pa.X = A;
     pa.ld = d.lda;
@@ -440,13 +554,15 @@ hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t 
     pa.off_planes = lay.off_Ap;
     pa.off_signs = lay.off_SA;
     pa.off_r = lay.off_rA;
+    pa.off_CA = lay.off_CA;
+    pa.off_RA = lay.off_RA;
     pa.per_row = 1;
     pa.LBS = lay.LBS;
     dim3 gA((unsigned)(lay.MT * pa.nchunk), (unsigned)dpairs, (unsigned)d.batch);
-    if (d.polarity == SC_BIPOLAR_XNOR)
-        hipLaunchKernelGGL(k_planes<SC_BIPOLAR_XNOR>, gA, dim3(256), 0, st, pa, ws);
+    if (cbsg)
+        launch_planes_side<true>(d.polarity, gA, pa, ws, st);
     else
-        hipLaunchKernelGGL(k_planes<SC_UNIPOLAR_AND_SM>, gA, dim3(256), 0, st, pa, ws);
+        launch_planes_side<false>(d.polarity, gA, pa, ws, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 
@@ -463,12 +579,10 @@ hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t 
     pb.off_planes = lay.off_Bp;
     pb.off_signs = lay.off_SB;
     pb.off_r = lay.off_rB;
+    pb.off_CA = pb.off_RA = 0;
     pb.per_row = 0;
     dim3 gB((unsigned)(lay.NT * pb.nchunk), (unsigned)dpairs, (unsigned)lay.nbB);
-    if (d.polarity == SC_BIPOLAR_XNOR)
-        hipLaunchKernelGGL(k_planes<SC_BIPOLAR_XNOR>, gB, dim3(256), 0, st, pb, ws);
-    else
-        hipLaunchKernelGGL(k_planes<SC_UNIPOLAR_AND_SM>, gB, dim3(256), 0, st, pb, ws);
+    launch_planes_side<false>(d.polarity, gB, pb, ws, st);
     return hipGetLastError();
 }
 
@@ -491,8 +605,9 @@ struct GemmArgs {
 };
 
 // counts and Eq. (1) decode of row r (0..7) of one thread's 8x8 block, written in the
-// original row order
-template <int POL>
+// original row order.  acc holds, per mode: MODE_AND the AND count (X = K L - RA - RB +
+// 2 acc); MODE_SIGNED the signed count S; MODE_CBSG sum_d sgn D.Z (X = K L - RA + acc).
+template <int MODE>
 __device__ __forceinline__ void epilogue_row(const int32_t (&acc)[8], int r, int b, int tm, int tn,
                                              int tx, int ty, const GemmArgs &g, const Layout &lay,
                                              uint8_t *ws) {
@@ -504,7 +619,7 @@ __device__ __forceinline__ void epilogue_row(const int32_t (&acc)[8], int r, int
     const int i = ws_ptr<int32_t>(wsa, lay.off_perm)[p];
     if (i < 0) return;
     const int Li = ws_ptr<int32_t>(wsa, lay.off_Ls)[p];
-    const int ra = POL == SC_BIPOLAR_XNOR ? ws_ptr<int32_t>(wsa, lay.off_RA)[p] : 0;
+    const int ra = MODE != MODE_SIGNED ? ws_ptr<int32_t>(wsa, lay.off_RA)[p] : 0;
     const int32_t *RB = ws_ptr<int32_t>(wsbB, lay.off_RB);
     const float sa = g.sA[(size_t)b * g.strideSA + i];
     const float *sBb = g.sB + (size_t)b * g.strideSB;
@@ -517,7 +632,7 @@ __device__ __forceinline__ void epilogue_row(const int32_t (&acc)[8], int r, int
         const int j0 = tn * BN + h * 64 + 4 * tx;       // four adjacent columns
         if (j0 >= g.N) continue;
         int rb[4] = {0, 0, 0, 0};
-        if (POL == SC_BIPOLAR_XNOR) {
+        if (MODE == MODE_AND) {
 #pragma unroll
             for (int c = 0; c < 4; ++c)
                 if (j0 + c < g.N) rb[c] = RB[(size_t)(j0 + c) * (g.L_max + 1) + Li];
@@ -528,8 +643,11 @@ __device__ __forceinline__ void epilogue_row(const int32_t (&acc)[8], int r, int
         for (int c = 0; c < 4; ++c) {
             const int j = j0 + c < g.N ? j0 + c : j0;
             int32_t num;
-            if (POL == SC_BIPOLAR_XNOR) {
+            if (MODE == MODE_AND) {
                 cnt[c] = KL - ra - rb[c] + 2 * acc[4 * h + c];
+                num = 2 * cnt[c] - KL;
+            } else if (MODE == MODE_CBSG) {
+                cnt[c] = KL - ra + acc[4 * h + c];
                 num = 2 * cnt[c] - KL;
             } else {
                 cnt[c] = acc[4 * h + c];
@@ -560,7 +678,7 @@ __device__ __forceinline__ void epilogue_row(const int32_t (&acc)[8], int r, int
     }
 }
 
-template <int POL, bool SPLIT>
+template <int MODE, bool SPLIT>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, Layout lay, uint8_t *ws) {
     __shared__ uint4 As[LCH * BM / 4];
     __shared__ uint4 Bs[LCH * BN / 4];
@@ -589,12 +707,17 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, Layout lay, uint8_t *w
 
     for (int kb = kb0; kb < kb1 && Lloop > 0; ++kb) {
         uint32_t sig[8][8];
-        if (POL == SC_UNIPOLAR_AND_SM) {
+        if (MODE != MODE_AND) {
             const uint4 *sa4 = reinterpret_cast<const uint4 *>(ws_ptr<uint32_t>(wsa, lay.off_SA) +
                                                                ((size_t)tm * g.KB + kb) * BM);
-            const uint4 *sb4 = reinterpret_cast<const uint4 *>(ws_ptr<uint32_t>(wsbB, lay.off_SB) +
-                                                               ((size_t)tn * g.KB + kb) * BN);
-            const uint4 a0 = sa4[ty], a1 = sa4[16 + ty], b0 = sb4[tx], b1 = sb4[16 + tx];
+            const uint4 a0 = sa4[ty], a1 = sa4[16 + ty];
+            uint4 b0 = make_uint4(0u, 0u, 0u, 0u), b1 = b0;
+            if (MODE == MODE_SIGNED) {
+                const uint4 *sb4 = reinterpret_cast<const uint4 *>(
+                    ws_ptr<uint32_t>(wsbB, lay.off_SB) + ((size_t)tn * g.KB + kb) * BN);
+                b0 = sb4[tx];
+                b1 = sb4[16 + tx];
+            }
             const uint32_t sa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
             const uint32_t sb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
 #pragma unroll
@@ -626,7 +749,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, Layout lay, uint8_t *w
                     for (int r = 0; r < 8; ++r)
 #pragma unroll
                         for (int c = 0; c < 8; ++c) {
-                            if (POL == SC_UNIPOLAR_AND_SM)
+                            if (MODE != MODE_AND)
                                 popc_acc(acc[r][c], (av[r] & bv[c]) ^ sig[r][c]);
                             else
                                 popc_acc(acc[r][c], av[r] & bv[c]);
@@ -647,14 +770,14 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, Layout lay, uint8_t *w
         }
     } else {
 #pragma unroll
-        for (int r = 0; r < 8; ++r) epilogue_row<POL>(acc[r], r, b, tm, tn, tx, ty, g, lay, ws);
+        for (int r = 0; r < 8; ++r) epilogue_row<MODE>(acc[r], r, b, tm, tn, tx, ty, g, lay, ws);
     }
 }
 
 // sums the partial counts of every split of a tile and decodes.  Four blocks per
 // tile; reduce thread (g, q) owns rows 2q and 2q+1 of GEMM thread g's 8x8 block, so
 // the four threads of one g read adjacent 64-byte pieces of its partials.
-template <int POL>
+template <int MODE>
 __global__ __launch_bounds__(256) void k_gemm_reduce(GemmArgs g, Layout lay, uint8_t *ws) {
     const int tile = blockIdx.x >> 2;
     const int tn = tile % lay.NT;
@@ -676,21 +799,21 @@ __global__ __launch_bounds__(256) void k_gemm_reduce(GemmArgs g, Layout lay, uin
         acc1[0] += u1.x; acc1[1] += u1.y; acc1[2] += u1.z; acc1[3] += u1.w;
         acc1[4] += v1.x; acc1[5] += v1.y; acc1[6] += v1.z; acc1[7] += v1.w;
     }
-    epilogue_row<POL>(acc0, 2 * q, b, tm, tn, tx, ty, g, lay, ws);
-    epilogue_row<POL>(acc1, 2 * q + 1, b, tm, tn, tx, ty, g, lay, ws);
+    epilogue_row<MODE>(acc0, 2 * q, b, tm, tn, tx, ty, g, lay, ws);
+    epilogue_row<MODE>(acc1, 2 * q + 1, b, tm, tn, tx, ty, g, lay, ws);
 }
 
-template <int POL>
-static hipError_t launch_gemm_pol(const GemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
+template <int MODE>
+static hipError_t launch_gemm_mode(const GemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
     const unsigned tiles = (unsigned)(g.batch * lay.MT * lay.NT);
     if (g.S == 1) {
-        hipLaunchKernelGGL((k_gemm<POL, false>), dim3(tiles), dim3(256), 0, st, g, lay, ws);
+        hipLaunchKernelGGL((k_gemm<MODE, false>), dim3(tiles), dim3(256), 0, st, g, lay, ws);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((k_gemm<POL, true>), dim3(tiles * (unsigned)g.S), dim3(256), 0, st, g, lay, ws);
+    hipLaunchKernelGGL((k_gemm<MODE, true>), dim3(tiles * (unsigned)g.S), dim3(256), 0, st, g, lay, ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_gemm_reduce<POL>), dim3(tiles * 4u), dim3(256), 0, st, g, lay, ws);
+    hipLaunchKernelGGL((k_gemm_reduce<MODE>), dim3(tiles * 4u), dim3(256), 0, st, g, lay, ws);
     return hipGetLastError();
 }
 
@@ -714,8 +837,9 @@ hipError_t launch_gemm(const sc_gemm_desc &d, const Layout &lay, const float *sA
     g.ldo = d.ldo;
     g.out = out;
     g.counts = counts;
-    if (d.polarity == SC_BIPOLAR_XNOR) return launch_gemm_pol<SC_BIPOLAR_XNOR>(g, lay, ws, st);
-    return launch_gemm_pol<SC_UNIPOLAR_AND_SM>(g, lay, ws, st);
+    if (lay.mode == MODE_AND) return launch_gemm_mode<MODE_AND>(g, lay, ws, st);
+    if (lay.mode == MODE_CBSG) return launch_gemm_mode<MODE_CBSG>(g, lay, ws, st);
+    return launch_gemm_mode<MODE_SIGNED>(g, lay, ws, st);
 }
 
 }  // namespace scg

@@ -74,7 +74,7 @@ def _desc(lib, **kw):
 
 @pytest.mark.parametrize("field,value,code", [
     ("M", -1, -2), ("K", -5, -2), ("batch", -1, -2), ("K", (1 << 20) + 1, -2),
-    ("L_max", 0, -3), ("L_max", 4097, -3), ("polarity", 2, -4), ("rng", 1, -5),
+    ("L_max", 0, -3), ("L_max", 4097, -3), ("polarity", 2, -4), ("rng", 2, -5), ("rng", -1, -5),
     ("L_hint", 65, -3), ("L_hint", -1, -3), ("lda", 255, -9), ("ldo", 63, -9), ("strideA", -1, -9),
 ])
 def test_workspace_size_rejects_bad_desc(lib, field, value, code):
@@ -82,6 +82,19 @@ def test_workspace_size_rejects_bad_desc(lib, field, value, code):
     so = lib.load()
     d = _desc(lib, **{field: value})
     assert so.sc_gemm_workspace_size(ctypes.byref(d), ctypes.byref(n)) == code
+
+
+def test_cbsg_length_limit(lib):
+    # the Sobol-8 sequences have period 256: longer C-BSG streams are rejected
+    assert lib.sc_gemm_workspace_size(_desc(lib, rng=1, L_max=256)) > 0
+    so = lib.load()
+    n = ctypes.c_size_t(0)
+    d = _desc(lib, rng=1, L_max=257, L_hint=0)
+    assert so.sc_gemm_workspace_size(ctypes.byref(d), ctypes.byref(n)) == lib.SC_ERR_LEN
+    # C-BSG keeps a count table but no marginals of B
+    lfsr = lib.sc_gemm_workspace_size(_desc(lib, L_max=256, N=4096, ldo=4096))
+    cbsg = lib.sc_gemm_workspace_size(_desc(lib, rng=1, L_max=256, N=4096, ldo=4096))
+    assert cbsg < lfsr
 
 
 def test_workspace_size_values(lib):
@@ -115,10 +128,12 @@ def test_sc_gemm_argument_errors_before_any_hip_call(lib):
 
 def test_comparator_sequence_argument_errors(lib):
     fake = 1 << 40
-    assert lib.sc_comparator_sequence(0, 0, 16, 0, 0) == lib.SC_ERR_NULL
-    assert lib.sc_comparator_sequence(0, 2, 16, fake, 0) == lib.SC_ERR_RNG
-    assert lib.sc_comparator_sequence(0, 0, 0, fake, 0) == lib.SC_ERR_LEN
-    assert lib.sc_comparator_sequence(0, 0, 4097, fake, 0) == lib.SC_ERR_LEN
+    assert lib.sc_comparator_sequence(0, 0, 0, 16, 0, 0) == lib.SC_ERR_NULL
+    assert lib.sc_comparator_sequence(0, 2, 0, 16, fake, 0) == lib.SC_ERR_RNG
+    assert lib.sc_comparator_sequence(0, 0, 2, 16, fake, 0) == lib.SC_ERR_RNG
+    assert lib.sc_comparator_sequence(0, 0, 0, 0, fake, 0) == lib.SC_ERR_LEN
+    assert lib.sc_comparator_sequence(0, 0, 0, 4097, fake, 0) == lib.SC_ERR_LEN
+    assert lib.sc_comparator_sequence(0, 1, 1, 257, fake, 0) == lib.SC_ERR_LEN
     assert lib.sc_gemm_status(0, 0) == lib.SC_ERR_NULL
 
 

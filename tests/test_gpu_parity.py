@@ -45,20 +45,21 @@ def _to_dev(g, dev):
             torch.from_numpy(np.ascontiguousarray(g.L)).to(dev))
 
 
-def _run(g, dev, check_status=True):
+def _run(g, dev, check_status=True, rng=0):
     import torch
     import paper_2609_32922_amd as scg
     A, sA, B, sB, L = _to_dev(g, dev)
     out, cnt = scg.gemm(A, sA, B, sB, L, L_max=g.L_max, polarity=g.polarity, seed=g.seed,
-                        want_counts=True, check_status=check_status)
+                        want_counts=True, check_status=check_status, rng=rng)
     torch.cuda.synchronize()
     return out.cpu().numpy(), cnt.cpu().numpy()
 
 
-def _compare(g, b, rows, cols, out, cnt, oracle_mod, tag):
+def _compare(g, b, rows, cols, out, cnt, oracle_mod, tag, rng=0):
     bB = 0 if g.B.shape[0] == 1 else b
-    c_ref, o_ref = oracle_mod.sc_gemm(g.A[b][rows], g.B[bB][cols], g.sA[b][rows], g.sB[bB][cols],
-                                      g.L[b][rows], g.L_max, g.polarity, g.seed)
+    ref = oracle_mod.sc_gemm_cbsg if rng == 1 else oracle_mod.sc_gemm
+    c_ref, o_ref = ref(g.A[b][rows], g.B[bB][cols], g.sA[b][rows], g.sB[bB][cols],
+                       g.L[b][rows], g.L_max, g.polarity, g.seed)
     c_gpu = cnt[b][np.ix_(rows, cols)]
     o_gpu = out[b][np.ix_(rows, cols)].astype(np.float64)
     bad = np.argwhere(c_gpu != c_ref)
@@ -164,11 +165,11 @@ def _sample(n, rng, k):
     return np.array(sorted(set(i for i in base + extra if 0 <= i < n)), dtype=np.int64)
 
 
-def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None):
+def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None, seq=0):
     rng = np.random.default_rng(7)
     for g in w.gemms:
-        _note("%s/%s full size %s" % (w.name, g.name, g.A.shape))
-        out, cnt = _run(g, dev)
+        _note("%s/%s full size %s rng %d" % (w.name, g.name, g.A.shape, seq))
+        out, cnt = _run(g, dev, rng=seq)
         KL = g.K * g.L.astype(np.int64)
         if g.polarity == 0:
             assert np.all(cnt >= 0) and np.all(cnt <= KL[:, :, None])
@@ -178,7 +179,8 @@ def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None):
         for b in bs:
             rows = _sample(g.M, rng, nrows)
             cols = _sample(g.N, rng, ncols)
-            _compare(g, b, rows, cols, out, cnt, oracle_mod, "%s/%s b%d" % (w.name, g.name, b))
+            _compare(g, b, rows, cols, out, cnt, oracle_mod, "%s/%s b%d" % (w.name, g.name, b),
+                     rng=seq)
 
 
 def test_workload_vitb16_fc1_L128(dev, oracle_mod):
@@ -243,3 +245,99 @@ def test_strided_interleaved_heads(dev, oracle_mod):
         nz = o_ref != 0
         assert np.all(oo[~nz] == 0)
         assert np.max(np.abs(oo[nz] - o_ref[nz]) / np.abs(o_ref[nz])) <= 1e-6
+
+
+# --------------------------------------------------------------------------
+# Sobol-8 sequences with conditional generation of B's stream (C-BSG)
+# --------------------------------------------------------------------------
+def test_sobol_sequence_matches_oracle(dev, oracle_mod):
+    import paper_2609_32922_amd as scg
+    for seed in (0, 1, 5, 2**64 - 1):
+        for op in (0, 1):
+            _note("sobol seed=%d op=%d" % (seed, op))
+            r = scg.comparator_sequence(seed, op, 256, rng=scg.SC_RNG_SOBOL8_CBSG).cpu().numpy()
+            ref = oracle_mod.sobol8(op + 1, oracle_mod.sobol_shift(seed, op), 256)
+            assert np.array_equal(r, ref)
+            # one full period visits every 8-bit value once
+            assert np.array_equal(np.sort(r), np.arange(256))
+
+
+CBSG_FUZZ = [
+    # batch, M, N, K, L_max, L_lo, polarity, broadcast_B, seed
+    (1, 1, 1, 1, 1, 0, 0, False, 101),
+    (1, 129, 130, 33, 70, 0, 0, False, 103),
+    (1, 300, 257, 100, 256, 0, 0, False, 105),
+    (1, 257, 129, 64, 64, 64, 0, False, 107),
+    (2, 140, 131, 96, 40, 0, 0, False, 109),
+    (3, 70, 200, 31, 100, 1, 0, True, 111),
+    (1, 129, 130, 33, 70, 0, 1, False, 113),
+    (1, 300, 257, 100, 193, 0, 1, False, 115),
+    (2, 140, 131, 65, 48, 0, 1, True, 117),
+    (1, 64, 64, 1000, 24, 0, 1, False, 119),
+    (1, 200, 150, 7, 256, 200, 0, False, 121),
+]
+
+
+@pytest.mark.parametrize("case", CBSG_FUZZ, ids=[str(c) for c in CBSG_FUZZ])
+def test_cbsg_fuzz_full_compare(dev, oracle_mod, case):
+    batch, M, N, K, L_max, L_lo, pol, bcast, seed = case
+    rng = np.random.default_rng(seed)
+    g = W.random_gemm(rng, batch, M, N, K, L_max, pol, seed, L_lo=L_lo, broadcast_B=bcast)
+    _note("cbsg fuzz %s" % (case,))
+    out, cnt = _run(g, dev, rng=1)
+    for b in range(batch):
+        _compare(g, b, np.arange(M), np.arange(N), out, cnt, oracle_mod,
+                 "cbsg%s b%d" % (case, b), rng=1)
+
+
+def test_cbsg_extreme_values(dev, oracle_mod):
+    """Saturated and zero operands: c = 0, c = L and c = L - c hit every branch of the
+    interval planes (empty interval, full interval, sign flips)."""
+    rng = np.random.default_rng(131)
+    for pol in (0, 1):
+        g = W.random_gemm(rng, 1, 140, 136, 70, 96, pol, 131 + pol)
+        vals = np.array([-127, -126, -1, 0, 1, 126, 127], np.int8)
+        g.A[0] = rng.choice(vals, g.A[0].shape)
+        g.B[0] = rng.choice(vals, g.B[0].shape)
+        _note("cbsg extremes polarity %d" % pol)
+        out, cnt = _run(g, dev, rng=1)
+        _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod,
+                 "cbsg extremes %d" % pol, rng=1)
+
+
+def test_cbsg_zero_lengths_and_K0(dev, oracle_mod):
+    rng = np.random.default_rng(141)
+    g = W.random_gemm(rng, 1, 150, 140, 40, 64, 0, 141)
+    g.L[0, ::3] = 0
+    _note("cbsg zero lengths")
+    out, cnt = _run(g, dev, rng=1)
+    assert np.all(cnt[0, ::3] == 0) and np.all(out[0, ::3] == 0)
+    _compare(g, 0, np.arange(150), np.arange(140), out, cnt, oracle_mod, "cbsg zeroL", rng=1)
+    for pol in (0, 1):
+        g0 = W.random_gemm(rng, 1, 10, 12, 0, 16, pol, 5)
+        _note("cbsg K=0 polarity %d" % pol)
+        out, cnt = _run(g0, dev, rng=1)
+        assert np.all(cnt == 0) and np.all(out == 0)
+
+
+def test_cbsg_bad_lengths_set_status(dev):
+    import paper_2609_32922_amd as scg
+    rng = np.random.default_rng(151)
+    g = W.random_gemm(rng, 1, 50, 20, 16, 32, 0, 151)
+    g.L[0, 3] = 33
+    _note("cbsg bad lengths")
+    with pytest.raises(scg.ScError) as ei:
+        _run(g, dev, check_status=True, rng=1)
+    assert ei.value.code == scg.SC_ERR_DEVICE_STATUS
+
+
+def test_cbsg_workload_vitb16_fc1_L128(dev, oracle_mod):
+    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod, nrows=24, ncols=64, seq=1)
+
+
+def test_cbsg_workload_vitb16_fc1_mp64(dev, oracle_mod):
+    _check_workload(W.vitb16_fc1_mp64(), dev, oracle_mod, nrows=24, ncols=64, seq=1)
+
+
+def test_cbsg_workload_ditxl2_proj_mlp_group96(dev, oracle_mod):
+    _check_workload(W.ditxl2_proj_mlp_group96(), dev, oracle_mod, nrows=16, ncols=48, seq=1)
