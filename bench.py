@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 METRIC = "SC stream-bit-ops/sec (M·N·K·L) and % of gfx950 bitop+popcount peak"
 PEAK_BITOPS = 256 * 128 * 2.4e9 * 32 / 2         # 1.2583e15 (dual-issue VALU rate)
 PEAK_SINGLE_ISSUE = 256 * 64 * 2.4e9 * 32 / 2    # 6.2915e14 (one VALU issue per quad-cycle)
+PEAK_FP4_FLOPS = 10.1e15                         # dense fp4 (e2m1) MFMA, MI355X
 
 
 def parse():
@@ -35,6 +36,9 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="vitb16_fc1_L128")
+    p.add_argument("--engine", choices=("auto", "valu", "mfma"), default="auto",
+                   help="counting engine: packed popcount on the VALUs, or fp4 products on "
+                        "the matrix cores (auto: MFMA while K*L_max <= 2^24)")
     p.add_argument("--rng", choices=("lfsr", "cbsg"), default="lfsr",
                    help="comparator source: 32-bit LFSR, or scrambled Sobol-8 with "
                         "conditional generation of B's stream (C-BSG, L_max <= 256)")
@@ -49,9 +53,11 @@ def parse():
 
 def kernel_source_digest():
     import hashlib
-    src = os.path.join(ROOT, "paper_2609_32922_amd", "csrc", "sc_kernels.hip")
-    with open(src, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for name in ("sc_internal.h", "sc_kernels.hip", "sc_mfma.hip"):
+        with open(os.path.join(ROOT, "paper_2609_32922_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic(workload):
@@ -96,8 +102,11 @@ def main():
 
     w = W.WORKLOADS[args.workload]()
     rng = scg.SC_RNG_SOBOL8_CBSG if args.rng == "cbsg" else scg.SC_RNG_LFSR32
-    # counter summaries are keyed by workload and comparator source
-    traffic_key = args.workload if args.rng == "lfsr" else args.workload + ":cbsg"
+    engine = {"auto": scg.SC_ENGINE_AUTO, "valu": scg.SC_ENGINE_VALU,
+              "mfma": scg.SC_ENGINE_MFMA}[args.engine]
+    resolved = {g.name: (engine if engine != scg.SC_ENGINE_AUTO else
+                         (scg.SC_ENGINE_MFMA if g.K * g.L_max <= (1 << 24) else scg.SC_ENGINE_VALU))
+                for g in w.gemms}
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -106,7 +115,7 @@ def main():
         t = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (g.A, g.sA, g.B, g.sB, g.L)]
         out = torch.empty((g.batch, g.M, g.N), dtype=torch.float32, device=dev)
         d = scg.make_desc(t[0], t[2], g.L_max, g.polarity, g.seed, int(round(float(g.L.mean()))),
-                          rng)
+                          rng, engine)
         ws = scg.Workspace(scg.sc_gemm_workspace_size(d), dev)
         staged.append((g, t, out, ws))
     bitops = w.bitops()
@@ -124,7 +133,7 @@ def main():
             pe = None if pairs is None else (pairs[k][0].cuda_event, pairs[k][1].cuda_event)
             scg.gemm(t[0], t[1], t[2], t[3], t[4], L_max=g.L_max, polarity=g.polarity,
                      seed=g.seed, out=out, workspace=ws, stream=stream, prof_events=pe,
-                     L_hint=int(round(float(g.L.mean()))), rng=rng)
+                     L_hint=int(round(float(g.L.mean()))), rng=rng, engine=engine)
 
     for _ in range(args.warmup):
         step()
@@ -149,13 +158,24 @@ def main():
                              for s in range(nsteps)]))
     g_dom = w.gemms[kidx]
     achieved = g_dom.bitops() / (gemm_ms * 1e-3)
+    dom_engine = resolved[g_dom.name]
+    # counter summaries are keyed by workload, comparator source and engine
+    traffic_key = "%s:%s:%s" % (args.workload, args.rng,
+                                "mfma" if dom_engine == scg.SC_ENGINE_MFMA else "valu")
     traffic = measured_traffic(traffic_key)
-    roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_BITOPS / 1e12,
-                "unit": "Tbitop/s", "frac": achieved / PEAK_BITOPS, "traffic": traffic,
-                "kernel": ("k_gemm<unipolar>" if g_dom.polarity == 1 else
-                           "k_gemm<bipolar-cbsg>" if rng == scg.SC_RNG_SOBOL8_CBSG else
-                           "k_gemm<bipolar>"),
-                "kernel_ms": gemm_ms, "frac_of_single_issue_peak": achieved / PEAK_SINGLE_ISSUE}
+    if dom_engine == scg.SC_ENGINE_MFMA:
+        # one bit-pair product = one fp4 multiply-add = 2 flops on the matrix cores
+        roofline = {"bound": "mfma", "achieved": 2 * achieved / 1e12, "peak": PEAK_FP4_FLOPS / 1e12,
+                    "unit": "TFLOP/s", "frac": 2 * achieved / PEAK_FP4_FLOPS, "traffic": traffic,
+                    "kernel": "k_mgemm<%s>" % ("bipolar" if g_dom.polarity == 0 else "unipolar"),
+                    "kernel_ms": gemm_ms, "frac_of_valu_bitop_peak": achieved / PEAK_BITOPS}
+    else:
+        roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_BITOPS / 1e12,
+                    "unit": "Tbitop/s", "frac": achieved / PEAK_BITOPS, "traffic": traffic,
+                    "kernel": ("k_gemm<unipolar>" if g_dom.polarity == 1 else
+                               "k_gemm<bipolar-cbsg>" if rng == scg.SC_RNG_SOBOL8_CBSG else
+                               "k_gemm<bipolar>"),
+                    "kernel_ms": gemm_ms, "frac_of_single_issue_peak": achieved / PEAK_SINGLE_ISSUE}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -167,10 +187,12 @@ def main():
                                           "L_max": g.L_max} for g in w.gemms],
            "polarity": "bipolar_xnor" if g0.polarity == 0 else "unipolar_and_sign_magnitude",
            "rng": "sobol8_cbsg" if args.rng == "cbsg" else "lfsr32", "seed": g0.seed,
+           "engine": {k: ("mfma" if v == scg.SC_ENGINE_MFMA else "valu") for k, v in resolved.items()},
            "bitops_per_step": bitops}
     line = {"metric": METRIC, "value": value, "unit": "stream-bit-ops/s", "n_gpus": 1,
             "steps": nsteps, "warmup": args.warmup, "ms_per_step": ms_per_step,
-            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "fp4" if dom_engine == scg.SC_ENGINE_MFMA else "u32",
             "data": "synthetic", "config": cfg, "roofline": roofline, "cpu_baseline": cpu}
     print(json.dumps(line), flush=True)
 

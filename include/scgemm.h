@@ -77,11 +77,20 @@ enum {
     SC_ERR_WORKSPACE = -6,     /* workspace NULL or smaller than sc_gemm_workspace_size() */
     SC_ERR_HIP = -7,           /* a HIP runtime call or kernel launch failed */
     SC_ERR_DEVICE_STATUS = -8, /* (sc_gemm_status) some L_i was outside [0, L_max] */
-    SC_ERR_STRIDE = -9         /* a row stride is smaller than the row length */
+    SC_ERR_STRIDE = -9,        /* a row stride is smaller than the row length */
+    SC_ERR_ENGINE = -10        /* unknown engine, reserved != 0, or MFMA with K*L_max > 2^24 */
 };
 
 enum { SC_BIPOLAR_XNOR = 0, SC_UNIPOLAR_AND_SM = 1 };
 enum { SC_RNG_LFSR32 = 0, SC_RNG_SOBOL8_CBSG = 1 };
+
+/* Counting engine.  Both give identical counts and outputs.
+ *   SC_ENGINE_VALU  packed bit planes, AND/XOR + popcount on the vector ALUs
+ *   SC_ENGINE_MFMA  stream bits as fp4 (e2m1) values in {-1, 0, +1}, counted by the
+ *                   matrix cores in fp32 (exact: every partial sum is an integer
+ *                   below 2^24); needs K * L_max <= 2^24
+ *   SC_ENGINE_AUTO  MFMA when K * L_max <= 2^24, else VALU */
+enum { SC_ENGINE_AUTO = 0, SC_ENGINE_VALU = 1, SC_ENGINE_MFMA = 2 };
 
 #define SC_L_MAX_LIMIT 4096     /* largest supported stream length */
 #define SC_K_LIMIT (1 << 20)    /* largest inner dimension (counts stay exact in int32) */
@@ -99,6 +108,8 @@ typedef struct sc_gemm_desc {
     int32_t L_hint;             /* optional expected mean of the L_i (0 = unknown, taken as
                                    L_max); only tunes how GEMM tiles are split over the
                                    compute units, never changes a result; 0..L_max */
+    int32_t engine;             /* SC_ENGINE_AUTO, SC_ENGINE_VALU or SC_ENGINE_MFMA */
+    int32_t reserved;           /* must be 0 */
     uint64_t seed;              /* comparator seed; same seed => bit-identical results */
     void *prof_event_begin;     /* optional hipEvent_t recorded just before the main */
     void *prof_event_end;       /*   GEMM kernel and just after it (profiling); NULL = off */

@@ -10,14 +10,16 @@ back to the CPU: without the built library every call raises.
 from __future__ import annotations
 
 from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_L_MAX_LIMIT, SC_OK,  # noqa: F401
-                   SC_RNG_LFSR32, SC_RNG_SOBOL8_CBSG, SC_UNIPOLAR_AND_SM, ScError, ScGemmDesc, load, sc_comparator_sequence,
+                   SC_ENGINE_AUTO, SC_ENGINE_MFMA, SC_ENGINE_VALU, SC_RNG_LFSR32,
+                   SC_RNG_SOBOL8_CBSG, SC_UNIPOLAR_AND_SM, ScError, ScGemmDesc, load, sc_comparator_sequence,
                    sc_gemm, sc_gemm_status, sc_gemm_workspace_size, sc_mp_lengths, sc_quantize,
                    sc_version, strerror)
 
 __all__ = ["gemm", "make_desc", "comparator_sequence", "quantize", "mp_lengths", "Workspace",
            "ScGemmDesc", "ScError", "sc_gemm", "sc_gemm_workspace_size", "sc_gemm_status",
            "sc_comparator_sequence", "sc_quantize", "sc_mp_lengths", "SC_BIPOLAR_XNOR",
-           "SC_UNIPOLAR_AND_SM", "SC_RNG_LFSR32", "SC_RNG_SOBOL8_CBSG"]
+           "SC_UNIPOLAR_AND_SM", "SC_RNG_LFSR32", "SC_RNG_SOBOL8_CBSG", "SC_ENGINE_AUTO",
+           "SC_ENGINE_VALU", "SC_ENGINE_MFMA"]
 
 
 def _stream_handle(stream):
@@ -27,7 +29,7 @@ def _stream_handle(stream):
 
 
 def make_desc(A, B, L_max: int, polarity: int, seed: int, L_hint: int = 0,
-              rng: int = SC_RNG_LFSR32) -> ScGemmDesc:
+              rng: int = SC_RNG_LFSR32, engine: int = SC_ENGINE_AUTO) -> ScGemmDesc:
     """Descriptor for contiguous A [batch, M, K] and B [batch or 1, N, K] tensors."""
     if A.dim() == 2:
         A = A.unsqueeze(0)
@@ -43,6 +45,7 @@ def make_desc(A, B, L_max: int, polarity: int, seed: int, L_hint: int = 0,
     d.strideA, d.strideB, d.strideO = M * K, (N * K if nb == batch and batch > 1 else 0), M * N
     d.strideSA, d.strideSB, d.strideL = M, (N if nb == batch and batch > 1 else 0), M
     d.L_max, d.polarity, d.rng, d.L_hint, d.seed = int(L_max), int(polarity), int(rng), int(L_hint), int(seed)
+    d.engine = int(engine)
     return d
 
 
@@ -65,19 +68,20 @@ class Workspace:
 def gemm(A, sA, B, sB, L, *, L_max: int, polarity: int = SC_BIPOLAR_XNOR, seed: int = 0,
          out=None, counts=None, want_counts: bool = False, workspace: Workspace = None,
          stream=None, check_status: bool = False, prof_events=None, L_hint: int = 0,
-         rng: int = SC_RNG_LFSR32):
+         rng: int = SC_RNG_LFSR32, engine: int = SC_ENGINE_AUTO):
     """SC GEMM on torch device tensors.
 
     A int8 [batch, M, K] (or [M, K]), sA float32 [batch, M], B int8 [batch or 1, N, K],
     sB float32 [batch or 1, N], L int32 [batch, M].  ``rng`` selects the comparator
-    source (LFSR, or Sobol-8 with conditional generation of B, L_max <= 256).
+    source (LFSR, or Sobol-8 with conditional generation of B, L_max <= 256) and
+    ``engine`` the counting engine (AUTO, VALU popcount or MFMA fp4).
     Returns (out, counts or None).
     """
     import torch
     squeeze = A.dim() == 2
     A3 = A.unsqueeze(0) if A.dim() == 2 else A
     B3 = B.unsqueeze(0) if B.dim() == 2 else B
-    d = make_desc(A3, B3, L_max, polarity, seed, L_hint, rng)
+    d = make_desc(A3, B3, L_max, polarity, seed, L_hint, rng, engine)
     for t, name in ((A3, "A"), (B3, "B"), (sA, "sA"), (sB, "sB"), (L, "L")):
         if not t.is_cuda or not t.is_contiguous():
             raise ValueError("%s must be a contiguous device tensor" % name)

@@ -10,7 +10,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["sc_kernels.hip", "sc_frontend.hip", "sc_api.hip"]
+SOURCES = ["sc_kernels.hip", "sc_mfma.hip", "sc_frontend.hip", "sc_api.hip"]
 OUT = os.path.join(HERE, "libscgemm.so")
 
 HIPCC_FLAGS = [

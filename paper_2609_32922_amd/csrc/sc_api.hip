@@ -19,9 +19,20 @@ bool mul_ok(size_t a, size_t b, size_t *r) {
 
 }  // namespace
 
+// the engine an AUTO descriptor runs on
+static int resolve_engine(const sc_gemm_desc &d) {
+    if (d.engine != SC_ENGINE_AUTO) return d.engine;
+    return (int64_t)d.K * d.L_max <= MFMA_EXACT ? SC_ENGINE_MFMA : SC_ENGINE_VALU;
+}
+
 bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     Layout l{};
+    l.engine = resolve_engine(d);
+    const bool mfma = l.engine == SC_ENGINE_MFMA;
     l.KB = (d.K + 31) / 32;
+    l.KQP = (int)round_up((d.K + 3) / 4, 4);
+    l.tstep = mfma ? MSTEP : LSTEP;
+    l.words_per_L = mfma ? (int64_t)l.KQP * 64 : (int64_t)l.KB * BM;
     l.MT = (d.M + BM - 1) / BM;
     l.NT = (d.N + BN - 1) / BN;
     l.LBS = (int)round_up(d.L_max, LCH);
@@ -31,7 +42,8 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     const bool cbsg = d.rng == SC_RNG_SOBOL8_CBSG;
     const bool uni = d.polarity == SC_UNIPOLAR_AND_SM;
     l.mode = uni ? MODE_SIGNED : (cbsg ? MODE_CBSG : MODE_AND);
-    const bool signsA = l.mode != MODE_AND, signsB = uni, needRB = l.mode == MODE_AND;
+    const bool signsA = !mfma && l.mode != MODE_AND, signsB = !mfma && uni;
+    const bool needRB = !mfma && l.mode == MODE_AND;
 
     // the status word is always the first word of the workspace
     size_t off = 0;
@@ -58,7 +70,9 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.off_tileOff = a;
     a = align256(a + (size_t)l.MT * 8);
     l.off_Ap = a;
-    if (!mul_ok(rowsA * (size_t)l.KB, (size_t)l.LP * 4, &sz)) return false;
+    // largest planes of one batch entry: every tile at L_max rounded up to its step
+    if (!mul_ok((size_t)l.MT * (size_t)l.words_per_L, (size_t)round_up(d.L_max, l.tstep) * 4, &sz))
+        return false;
     a = align256(a + sz);
     l.off_SA = a;
     if (signsA) a = align256(a + rowsA * (size_t)l.KB * 4);
@@ -72,7 +86,8 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     const size_t rowsB = (size_t)l.NT * BN;
     size_t bb = 0;
     l.off_Bp = bb;
-    if (!mul_ok(rowsB * (size_t)l.KB, (size_t)l.LBS * 4, &sz)) return false;
+    if (!mul_ok((size_t)l.NT * (size_t)l.words_per_L, (size_t)l.LBS * 4, &sz)) return false;
+    (void)rowsB;
     bb = align256(bb + sz);
     l.off_SB = bb;
     if (signsB) bb = align256(bb + rowsB * (size_t)l.KB * 4);
@@ -91,16 +106,19 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     // the reduction pass that reads s partial blocks and writes every tile's outputs.
     // Rates are the measured order of magnitude (about 2.8e12 bit pairs/s per CU,
     // 3.7e12 B/s for the reduction).
+    // The MFMA engine counts about 4x faster per CU (bit pairs as fp4 products).
     const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * l.MT * l.NT;
+    const int kunits = mfma ? l.KQP / 4 : l.KB;     // indivisible steps along K per cycle
+    const double rate = mfma ? 1.0e13 : 2.8e12;
     l.S = 1;
-    if (tiles > 0 && l.KB > 1) {
+    if (tiles > 0 && kunits > 1) {
         const double Lmean = d.L_hint > 0 ? d.L_hint : d.L_max;
-        const double per_L = (double)BM * BN * 32.0 * l.KB;   // tile work per cycle
+        const double per_L = (double)BM * BN * (mfma ? 4.0 * l.KQP : 32.0 * l.KB);
         double best = 0.0;
-        for (int s = 1; s <= MAX_SPLIT && s <= l.KB; ++s) {
+        for (int s = 1; s <= MAX_SPLIT && s <= kunits; ++s) {
             const int64_t units = tiles * s;
             const double avg_u = per_L * Lmean / s, max_u = per_L * d.L_max / s;
-            const double gemm = ((double)((units + CUS - 1) / CUS) * avg_u + (max_u - avg_u)) / 2.8e12;
+            const double gemm = ((double)((units + CUS - 1) / CUS) * avg_u + (max_u - avg_u)) / rate;
             const double red = s > 1 ? (double)tiles * (s + 1) * BM * BN * 4.0 / 3.7e12 + 5e-6 : 0.0;
             if (s == 1 || gemm + red < best * 0.99) {
                 best = gemm + red;
@@ -141,6 +159,10 @@ static int check_desc(const sc_gemm_desc *d) {
     if (d->rng != SC_RNG_LFSR32 && d->rng != SC_RNG_SOBOL8_CBSG) return SC_ERR_RNG;
     if (d->rng == SC_RNG_SOBOL8_CBSG && d->L_max > CBSG_L_MAX) return SC_ERR_LEN;
     if (d->L_hint < 0 || d->L_hint > d->L_max) return SC_ERR_LEN;
+    if ((d->engine != SC_ENGINE_AUTO && d->engine != SC_ENGINE_VALU && d->engine != SC_ENGINE_MFMA) ||
+        d->reserved != 0)
+        return SC_ERR_ENGINE;
+    if (d->engine == SC_ENGINE_MFMA && (int64_t)d->K * d->L_max > MFMA_EXACT) return SC_ERR_ENGINE;
     if (d->lda < d->K || d->ldb < d->K || d->ldo < d->N) return SC_ERR_STRIDE;
     if (d->strideA < 0 || d->strideB < 0 || d->strideO < 0 || d->strideSA < 0 || d->strideSB < 0 ||
         d->strideL < 0)
@@ -162,7 +184,7 @@ using namespace scg;
 
 extern "C" {
 
-int sc_version(void) { return 10100; }
+int sc_version(void) { return 10200; }
 
 const char *sc_strerror(int code) {
     switch (code) {
@@ -178,6 +200,9 @@ const char *sc_strerror(int code) {
         case SC_ERR_HIP: return "SC_ERR_HIP: a HIP call or kernel launch failed";
         case SC_ERR_DEVICE_STATUS: return "SC_ERR_DEVICE_STATUS: some L_i outside [0, L_max]";
         case SC_ERR_STRIDE: return "SC_ERR_STRIDE: a stride is too small or negative";
+        case SC_ERR_ENGINE:
+            return "SC_ERR_ENGINE: unknown engine, reserved field not 0, or MFMA engine with "
+                   "K*L_max > 2^24";
         default: return "unknown status code";
     }
 }
@@ -223,13 +248,17 @@ int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const in
         launch_cbsg_table(rA, d.L_max, reinterpret_cast<uint16_t *>(ws + lay.off_CA), st) != hipSuccess)
         return SC_ERR_HIP;
     if ((e = launch_schedule(d, lay, L_per_row, ws, st)) != hipSuccess) return SC_ERR_HIP;
-    if (lay.mode == MODE_AND && (e = launch_marginals(d, lay, A, B, ws, st)) != hipSuccess)
+    const bool mfma = lay.engine == SC_ENGINE_MFMA;
+    if (!mfma && lay.mode == MODE_AND && (e = launch_marginals(d, lay, A, B, ws, st)) != hipSuccess)
         return SC_ERR_HIP;
-    if ((e = launch_planes(d, lay, A, B, ws, st)) != hipSuccess) return SC_ERR_HIP;
+    e = mfma ? launch_mplanes(d, lay, A, B, ws, st) : launch_planes(d, lay, A, B, ws, st);
+    if (e != hipSuccess) return SC_ERR_HIP;
     if (d.prof_event_begin != nullptr &&
         hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_begin), st) != hipSuccess)
         return SC_ERR_HIP;
-    if ((e = launch_gemm(d, lay, sA, sB, out, counts, ws, st)) != hipSuccess) return SC_ERR_HIP;
+    e = mfma ? launch_mgemm(d, lay, sA, sB, out, counts, ws, st)
+             : launch_gemm(d, lay, sA, sB, out, counts, ws, st);
+    if (e != hipSuccess) return SC_ERR_HIP;
     if (d.prof_event_end != nullptr &&
         hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_end), st) != hipSuccess)
         return SC_ERR_HIP;

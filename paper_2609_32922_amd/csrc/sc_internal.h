@@ -23,6 +23,13 @@
 // A "bit plane" word packs 32 consecutive inner-dimension elements d = 32*kb .. 32*kb+31
 // of one row at one cycle l: bit t = z[row][32*kb + t][l].  With C-BSG the planes of A
 // are indexed by B's draw counter k instead of the cycle (see k_planes).
+//
+// MFMA engine: Ap and Bp hold fp4 (e2m1) "nibble planes" instead; there are no
+// marginals and no sign planes.  A slot is (octet o of 8 cycles, element quad dq of 4
+// elements) and holds 16 bytes: dword e = element 4*dq+e, nibble c = cycle 8*o+c, with
+// value +1 (0x2), -1 (0xA) or 0.  Slots are ordered s = o * KQP + dq and each slot
+// stores its 128 rows contiguously: A tile t is uint4 [Lloop/8 * KQP][128], B tile is
+// uint4 [LBS/8 * KQP][128].  A row of length L has zero nibbles at cycles >= L.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -48,7 +55,27 @@ constexpr int MODE_AND = 0;      // bipolar, LFSR: AND counts plus both marginal
 constexpr int MODE_SIGNED = 1;   // unipolar: popc((a & b) ^ sA ^ sB), signed AND counts
 constexpr int MODE_CBSG = 2;     // bipolar C-BSG: popc((D & Z) ^ sA) plus A's marginal
 
+// MFMA engine
+constexpr int MSTEP = 8;         // cycles per octet (tile lengths padded to it)
+constexpr int MSTAGE = 16;       // slots per LDS stage of the MFMA GEMM (4 MFMA k-steps)
+constexpr int OCH = 4;           // octets per block of the nibble-plane generator
+constexpr int64_t MFMA_EXACT = 1ll << 24;   // K * L_max bound for exact fp32 counts
+
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// comparator boundaries of an int8 value (bipolar, and unipolar magnitude)
+__device__ __forceinline__ int beta_bipolar(int q) { return (256 * (q + 127) + 127) / 254; }
+__device__ __forceinline__ int beta_unipolar(int q) {
+    const int a = q < 0 ? -q : q;
+    return (256 * a + 63) / 127;
+}
+
+__device__ __forceinline__ int wave_uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+template <typename T>
+__device__ __forceinline__ T *ws_ptr(uint8_t *ws, size_t off) {
+    return reinterpret_cast<T *>(ws + off);
+}
 
 struct Layout {
     int KB;            // words per cycle per row = ceil(K/32)
@@ -56,7 +83,11 @@ struct Layout {
     int LBS;           // cycle stride of B planes and length of draw arrays (L_max rounded to LCH)
     int LP;            // L_max rounded up to LSTEP
     int nbB;           // batch entries of B planes (1 when B is broadcast)
-    int mode;          // MODE_AND, MODE_SIGNED or MODE_CBSG
+    int mode;          // MODE_AND, MODE_SIGNED or MODE_CBSG (VALU engine)
+    int engine;        // SC_ENGINE_VALU or SC_ENGINE_MFMA (resolved, never AUTO)
+    int KQP;           // MFMA: element quads per octet, ceil(K/4) rounded up to 4
+    int tstep;         // tile cycle counts are rounded up to this (LSTEP or MSTEP)
+    int64_t words_per_L;   // plane words of one 128-row tile per cycle of its length
     size_t off_rA, off_rB, off_status, off_CA;
     size_t off_perm, off_Ls, off_RA, off_tileL, off_tileOff, off_Ap, off_SA;
     size_t stride_batchA;          // bytes per A batch entry block
@@ -82,6 +113,12 @@ hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t 
                          const int8_t *B, uint8_t *ws, hipStream_t st);
 hipError_t launch_gemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
                        float *out, int32_t *counts, uint8_t *ws, hipStream_t st);
+
+// MFMA engine (sc_mfma.hip)
+hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,
+                          const int8_t *B, uint8_t *ws, hipStream_t st);
+hipError_t launch_mgemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
+                        float *out, int32_t *counts, uint8_t *ws, hipStream_t st);
 
 // thresholds and ladder of the per-row length policy, passed by value to the kernel
 struct MpParams {

@@ -158,13 +158,6 @@ hipError_t launch_cbsg_table(const uint32_t *rA, int L_max, uint16_t *CA, hipStr
 // ----------------------------------------------------------------------------
 // helpers
 // ----------------------------------------------------------------------------
-__device__ __forceinline__ int beta_bipolar(int q) { return (256 * (q + 127) + 127) / 254; }
-__device__ __forceinline__ int beta_unipolar(int q) {
-    const int a = q < 0 ? -q : q;
-    return (256 * a + 63) / 127;
-}
-
-__device__ __forceinline__ int wave_uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // v_writelane_b32 through the compiler intrinsic (not inline asm), so that the backend
 // sees the instruction and inserts the wait states it needs after the v_cmp that
@@ -216,10 +209,6 @@ __device__ __forceinline__ void popc_acc(int32_t &acc, uint32_t x) {
     asm("s_nop 0\n\tv_bcnt_u32_b32 %0, %1, %0" : "+v"(acc) : "v"(x));
 }
 
-template <typename T>
-__device__ __forceinline__ T *ws_ptr(uint8_t *ws, size_t off) {
-    return reinterpret_cast<T *>(ws + off);
-}
 
 // ----------------------------------------------------------------------------
 // per-row length scheduler (one 1024-thread block per batch entry)
@@ -280,11 +269,11 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         const int t = c + tid;
         int tl = 0;
         if (t < lay.MT) {
-            tl = (int)round_up(Ls[(size_t)t * BM], LSTEP);
+            tl = (int)round_up(Ls[(size_t)t * BM], lay.tstep);
             tileL[t] = tl;
         }
         int64_t tot;
-        const int64_t ex = block_excl_scan_1024((int64_t)tl * lay.KB * BM, &tot);
+        const int64_t ex = block_excl_scan_1024((int64_t)tl * lay.words_per_L, &tot);
         if (t < lay.MT) tileOff[t] = carry + ex;
         carry += tot;
     }

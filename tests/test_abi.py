@@ -44,7 +44,8 @@ def test_desc_layout_matches_header(lib, tmp_path):
 int main(void) {
   printf("size %zu\\n", sizeof(sc_gemm_desc));
   F(batch) F(M) F(N) F(K) F(lda) F(ldb) F(ldo) F(strideA) F(strideB) F(strideO)
-  F(strideSA) F(strideSB) F(strideL) F(L_max) F(polarity) F(rng) F(L_hint) F(seed)
+  F(strideSA) F(strideSB) F(strideL) F(L_max) F(polarity) F(rng) F(L_hint) F(engine)
+  F(reserved) F(seed)
   F(prof_event_begin) F(prof_event_end)
   printf("L_MAX %d K_LIMIT %d\\n", SC_L_MAX_LIMIT, SC_K_LIMIT);
   return 0;
@@ -76,6 +77,7 @@ def _desc(lib, **kw):
     ("M", -1, -2), ("K", -5, -2), ("batch", -1, -2), ("K", (1 << 20) + 1, -2),
     ("L_max", 0, -3), ("L_max", 4097, -3), ("polarity", 2, -4), ("rng", 2, -5), ("rng", -1, -5),
     ("L_hint", 65, -3), ("L_hint", -1, -3), ("lda", 255, -9), ("ldo", 63, -9), ("strideA", -1, -9),
+    ("engine", 3, -10), ("engine", -1, -10), ("reserved", 1, -10),
 ])
 def test_workspace_size_rejects_bad_desc(lib, field, value, code):
     n = ctypes.c_size_t(0)
@@ -91,10 +93,24 @@ def test_cbsg_length_limit(lib):
     n = ctypes.c_size_t(0)
     d = _desc(lib, rng=1, L_max=257, L_hint=0)
     assert so.sc_gemm_workspace_size(ctypes.byref(d), ctypes.byref(n)) == lib.SC_ERR_LEN
-    # C-BSG keeps a count table but no marginals of B
-    lfsr = lib.sc_gemm_workspace_size(_desc(lib, L_max=256, N=4096, ldo=4096))
-    cbsg = lib.sc_gemm_workspace_size(_desc(lib, rng=1, L_max=256, N=4096, ldo=4096))
+    # on the VALU engine C-BSG keeps a count table but no marginals of B
+    lfsr = lib.sc_gemm_workspace_size(_desc(lib, L_max=256, N=4096, ldo=4096, engine=1))
+    cbsg = lib.sc_gemm_workspace_size(_desc(lib, rng=1, L_max=256, N=4096, ldo=4096, engine=1))
     assert cbsg < lfsr
+
+
+def test_mfma_engine_exactness_bound(lib):
+    # fp32 counts are exact only while K * L_max <= 2^24: an explicit MFMA request past
+    # it is refused, AUTO takes the VALU engine there
+    so = lib.load()
+    n = ctypes.c_size_t(0)
+    big = _desc(lib, K=65536, lda=65536, ldb=65536, L_max=512, engine=lib.SC_ENGINE_MFMA)
+    assert so.sc_gemm_workspace_size(ctypes.byref(big), ctypes.byref(n)) == lib.SC_ERR_ENGINE
+    for eng in (lib.SC_ENGINE_AUTO, lib.SC_ENGINE_VALU):
+        ok = _desc(lib, K=65536, lda=65536, ldb=65536, L_max=512, engine=eng)
+        assert lib.sc_gemm_workspace_size(ok) > 0
+    at = _desc(lib, K=65536, lda=65536, ldb=65536, L_max=256, engine=lib.SC_ENGINE_MFMA)
+    assert lib.sc_gemm_workspace_size(at) > 0
 
 
 def test_workspace_size_values(lib):
@@ -138,7 +154,7 @@ def test_comparator_sequence_argument_errors(lib):
 
 
 def test_strerror_and_version(lib):
-    for code in range(-9, 1):
+    for code in range(-10, 1):
         assert lib.strerror(code).startswith("SC_")
     assert "unknown" in lib.strerror(-100)
     assert lib.sc_version() >= 10000

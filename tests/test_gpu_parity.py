@@ -45,12 +45,16 @@ def _to_dev(g, dev):
             torch.from_numpy(np.ascontiguousarray(g.L)).to(dev))
 
 
-def _run(g, dev, check_status=True, rng=0):
+ENGINES = [1, 2]            # SC_ENGINE_VALU, SC_ENGINE_MFMA
+ENGINE_IDS = ["valu", "mfma"]
+
+
+def _run(g, dev, check_status=True, rng=0, engine=0):
     import torch
     import paper_2609_32922_amd as scg
     A, sA, B, sB, L = _to_dev(g, dev)
     out, cnt = scg.gemm(A, sA, B, sB, L, L_max=g.L_max, polarity=g.polarity, seed=g.seed,
-                        want_counts=True, check_status=check_status, rng=rng)
+                        want_counts=True, check_status=check_status, rng=rng, engine=engine)
     torch.cuda.synchronize()
     return out.cpu().numpy(), cnt.cpu().numpy()
 
@@ -80,10 +84,11 @@ def test_comparator_sequence_matches_oracle(dev, oracle_mod):
             assert np.array_equal(r, oracle_mod.comparator_sequence(seed, op, 4096))
 
 
-def test_bipolar_64x256x64_full(dev, oracle_mod):
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
+def test_bipolar_64x256x64_full(dev, oracle_mod, engine):
     g = W.bipolar_64x256x64().gemms[0]
-    _note("bipolar_64x256x64 full")
-    out, cnt = _run(g, dev)
+    _note("bipolar_64x256x64 full engine %d" % engine)
+    out, cnt = _run(g, dev, engine=engine)
     _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "64x256x64")
 
 
@@ -103,29 +108,31 @@ FUZZ = [
 ]
 
 
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
 @pytest.mark.parametrize("case", FUZZ, ids=[str(c) for c in FUZZ])
-def test_fuzz_full_compare(dev, oracle_mod, case):
+def test_fuzz_full_compare(dev, oracle_mod, case, engine):
     batch, M, N, K, L_max, L_lo, pol, bcast, seed = case
     rng = np.random.default_rng(seed)
     g = W.random_gemm(rng, batch, M, N, K, L_max, pol, seed, L_lo=L_lo, broadcast_B=bcast)
-    _note("fuzz %s" % (case,))
-    out, cnt = _run(g, dev)
+    _note("fuzz %s engine %d" % (case, engine))
+    out, cnt = _run(g, dev, engine=engine)
     for b in range(batch):
         _compare(g, b, np.arange(M), np.arange(N), out, cnt, oracle_mod, "fuzz%s b%d" % (case, b))
 
 
-def test_zero_lengths_and_K0(dev, oracle_mod):
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
+def test_zero_lengths_and_K0(dev, oracle_mod, engine):
     rng = np.random.default_rng(31)
     g = W.random_gemm(rng, 1, 150, 140, 40, 64, 0, 31)
     g.L[0, ::3] = 0
-    _note("zero lengths")
-    out, cnt = _run(g, dev)
+    _note("zero lengths engine %d" % engine)
+    out, cnt = _run(g, dev, engine=engine)
     assert np.all(cnt[0, ::3] == 0) and np.all(out[0, ::3] == 0)
     _compare(g, 0, np.arange(150), np.arange(140), out, cnt, oracle_mod, "zeroL")
     for pol in (0, 1):
         g0 = W.random_gemm(rng, 1, 10, 12, 0, 16, pol, 5)
         _note("K=0 polarity %d" % pol)
-        out, cnt = _run(g0, dev)
+        out, cnt = _run(g0, dev, engine=engine)
         assert np.all(cnt == 0) and np.all(out == 0)
 
 
@@ -146,13 +153,16 @@ def test_out_of_range_lengths_set_status(dev):
     _run(g, dev, check_status=True)          # a good call clears the status
 
 
-def test_deterministic_repeat(dev):
+def test_deterministic_repeat_and_engines_agree(dev):
     rng = np.random.default_rng(51)
     g = W.random_gemm(rng, 1, 260, 300, 160, 96, 0, 51)
     _note("determinism")
-    o1, c1 = _run(g, dev)
-    o2, c2 = _run(g, dev)
+    o1, c1 = _run(g, dev, engine=2)
+    o2, c2 = _run(g, dev, engine=2)
     assert np.array_equal(c1, c2) and np.array_equal(o1.view(np.uint32), o2.view(np.uint32))
+    # the two engines give bit-identical counts and decoded floats
+    o3, c3 = _run(g, dev, engine=1)
+    assert np.array_equal(c1, c3) and np.array_equal(o1.view(np.uint32), o3.view(np.uint32))
 
 
 # --------------------------------------------------------------------------
@@ -165,11 +175,11 @@ def _sample(n, rng, k):
     return np.array(sorted(set(i for i in base + extra if 0 <= i < n)), dtype=np.int64)
 
 
-def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None, seq=0):
+def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None, seq=0, engine=0):
     rng = np.random.default_rng(7)
     for g in w.gemms:
-        _note("%s/%s full size %s rng %d" % (w.name, g.name, g.A.shape, seq))
-        out, cnt = _run(g, dev, rng=seq)
+        _note("%s/%s full size %s rng %d engine %d" % (w.name, g.name, g.A.shape, seq, engine))
+        out, cnt = _run(g, dev, rng=seq, engine=engine)
         KL = g.K * g.L.astype(np.int64)
         if g.polarity == 0:
             assert np.all(cnt >= 0) and np.all(cnt <= KL[:, :, None])
@@ -183,16 +193,18 @@ def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None, seq=0)
                      rng=seq)
 
 
-def test_workload_vitb16_fc1_L128(dev, oracle_mod):
-    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod)
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
+def test_workload_vitb16_fc1_L128(dev, oracle_mod, engine):
+    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod, engine=engine)
 
 
 def test_workload_vitb16_fc1_mp64(dev, oracle_mod):
     _check_workload(W.vitb16_fc1_mp64(), dev, oracle_mod)
 
 
-def test_workload_ditxl2_proj_mlp_group96(dev, oracle_mod):
-    _check_workload(W.ditxl2_proj_mlp_group96(), dev, oracle_mod)
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
+def test_workload_ditxl2_proj_mlp_group96(dev, oracle_mod, engine):
+    _check_workload(W.ditxl2_proj_mlp_group96(), dev, oracle_mod, engine=engine)
 
 
 def test_workload_vitl14_336_qk_mlp(dev, oracle_mod):
@@ -278,19 +290,21 @@ CBSG_FUZZ = [
 ]
 
 
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
 @pytest.mark.parametrize("case", CBSG_FUZZ, ids=[str(c) for c in CBSG_FUZZ])
-def test_cbsg_fuzz_full_compare(dev, oracle_mod, case):
+def test_cbsg_fuzz_full_compare(dev, oracle_mod, case, engine):
     batch, M, N, K, L_max, L_lo, pol, bcast, seed = case
     rng = np.random.default_rng(seed)
     g = W.random_gemm(rng, batch, M, N, K, L_max, pol, seed, L_lo=L_lo, broadcast_B=bcast)
-    _note("cbsg fuzz %s" % (case,))
-    out, cnt = _run(g, dev, rng=1)
+    _note("cbsg fuzz %s engine %d" % (case, engine))
+    out, cnt = _run(g, dev, rng=1, engine=engine)
     for b in range(batch):
         _compare(g, b, np.arange(M), np.arange(N), out, cnt, oracle_mod,
                  "cbsg%s b%d" % (case, b), rng=1)
 
 
-def test_cbsg_extreme_values(dev, oracle_mod):
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
+def test_cbsg_extreme_values(dev, oracle_mod, engine):
     """Saturated and zero operands: c = 0, c = L and c = L - c hit every branch of the
     interval planes (empty interval, full interval, sign flips)."""
     rng = np.random.default_rng(131)
@@ -299,8 +313,8 @@ def test_cbsg_extreme_values(dev, oracle_mod):
         vals = np.array([-127, -126, -1, 0, 1, 126, 127], np.int8)
         g.A[0] = rng.choice(vals, g.A[0].shape)
         g.B[0] = rng.choice(vals, g.B[0].shape)
-        _note("cbsg extremes polarity %d" % pol)
-        out, cnt = _run(g, dev, rng=1)
+        _note("cbsg extremes polarity %d engine %d" % (pol, engine))
+        out, cnt = _run(g, dev, rng=1, engine=engine)
         _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod,
                  "cbsg extremes %d" % pol, rng=1)
 
@@ -331,8 +345,9 @@ def test_cbsg_bad_lengths_set_status(dev):
     assert ei.value.code == scg.SC_ERR_DEVICE_STATUS
 
 
-def test_cbsg_workload_vitb16_fc1_L128(dev, oracle_mod):
-    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod, nrows=24, ncols=64, seq=1)
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
+def test_cbsg_workload_vitb16_fc1_L128(dev, oracle_mod, engine):
+    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod, nrows=24, ncols=64, seq=1, engine=engine)
 
 
 def test_cbsg_workload_vitb16_fc1_mp64(dev, oracle_mod):
