@@ -35,6 +35,8 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.words_per_L = mfma ? (int64_t)l.KQP * 64 : (int64_t)l.KB * BM;
     l.MT = (d.M + BM - 1) / BM;
     l.NT = (d.N + BN - 1) / BN;
+    l.mbn = l.NT > 1 ? 2 * BN : BN;
+    if (mfma) l.NT = (int)round_up(l.NT, l.mbn / BN);
     l.LBS = (int)round_up(d.L_max, LCH);
     l.LP = (int)round_up(d.L_max, LSTEP);
     l.nbB = (d.strideB == 0) ? 1 : d.batch;
@@ -99,28 +101,33 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     if (!mul_ok(bb, (size_t)l.nbB, &totB)) return false;
     off += totB;
 
-    // split count of the GEMM tiles.  Estimated time of split s: the busiest CU holds
-    // ceil(units/CUS) units of average work, plus the excess of the heaviest unit over
-    // the average (row tiles run as long as their longest row: up to L_max when the
-    // lengths vary, while the average follows the mean length L_hint), plus, for s > 1,
-    // the reduction pass that reads s partial blocks and writes every tile's outputs.
-    // Rates are the measured order of magnitude (about 2.8e12 bit pairs/s per CU,
-    // 3.7e12 B/s for the reduction).
-    // The MFMA engine counts about 4x faster per CU (bit pairs as fp4 products).
-    const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * l.MT * l.NT;
-    const int kunits = mfma ? l.KQP / 4 : l.KB;     // indivisible steps along K per cycle
-    const double rate = mfma ? 1.0e13 : 2.8e12;
+    // split count of the GEMM tiles.  Estimated time of split s: the busiest slot (a
+    // resident block) runs ceil(units/slots) units of average work, plus the excess of
+    // the heaviest unit over the average (row tiles run as long as their longest row: up
+    // to L_max when the lengths vary, while the average follows the mean length L_hint),
+    // plus, for s > 1, writing and summing s partial tiles.  Units are dealt to the
+    // eight XCDs round-robin, so s is a power of two: each XCD then keeps one k-range of
+    // its tiles, and its L2 serves that range to all of them.  Rates are the measured
+    // order of magnitude: VALU engine 2.8e12 bit pairs/s per CU; MFMA engine 4.8e12
+    // products/s per resident block (two per CU); partial sums at 3e12 B/s.
+    const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * l.MT * (mfma ? l.NT / (l.mbn / BN) : l.NT);
+    const int kunits = mfma ? l.KQP / 2 : l.KB;     // indivisible steps along K per cycle
+    const int slots = mfma ? CUS * MFMA_BLOCKS_PER_CU : CUS;
+    const double rate = mfma ? 4.8e12 : 2.8e12;
+    const double tile_bytes = (double)BM * (mfma ? l.mbn : BN) * 4.0;
     l.S = 1;
     if (tiles > 0 && kunits > 1) {
         const double Lmean = d.L_hint > 0 ? d.L_hint : d.L_max;
-        const double per_L = (double)BM * BN * (mfma ? 4.0 * l.KQP : 32.0 * l.KB);
+        const double per_L = mfma ? (double)BM * l.mbn * 4.0 * l.KQP : (double)BM * BN * 32.0 * l.KB;
         double best = 0.0;
-        for (int s = 1; s <= MAX_SPLIT && s <= kunits; ++s) {
+        for (int s = 1; s <= MAX_SPLIT && s <= kunits; s = mfma ? 2 * s : s + 1) {
             const int64_t units = tiles * s;
             const double avg_u = per_L * Lmean / s, max_u = per_L * d.L_max / s;
-            const double gemm = ((double)((units + CUS - 1) / CUS) * avg_u + (max_u - avg_u)) / rate;
-            const double red = s > 1 ? (double)tiles * (s + 1) * BM * BN * 4.0 / 3.7e12 + 5e-6 : 0.0;
-            if (s == 1 || gemm + red < best * 0.99) {
+            const double gemm = ((double)((units + slots - 1) / slots) * avg_u + (max_u - avg_u)) / rate;
+            const double red = s > 1 ? (mfma ? (double)tiles * (2 * s) * tile_bytes / 3e12
+                                             : (double)tiles * (s + 1) * tile_bytes / 3.7e12) + 5e-6
+                                     : 0.0;
+            if (s == 1 || gemm + red < best * (mfma ? 0.97 : 0.99)) {
                 best = gemm + red;
                 l.S = s;
             }
@@ -129,7 +136,7 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.off_part = off;
     if (l.S > 1) {
         size_t partb;
-        if (!mul_ok((size_t)tiles * (size_t)l.S, (size_t)BM * BN * 4, &partb)) return false;
+        if (!mul_ok((size_t)tiles * (size_t)l.S, (size_t)BM * (mfma ? l.mbn : BN) * 4, &partb)) return false;
         off = align256(off + partb);
     }
 

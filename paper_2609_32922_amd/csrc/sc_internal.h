@@ -57,8 +57,9 @@ constexpr int MODE_CBSG = 2;     // bipolar C-BSG: popc((D & Z) ^ sA) plus A's m
 
 // MFMA engine
 constexpr int MSTEP = 8;         // cycles per octet (tile lengths padded to it)
-constexpr int MSTAGE = 16;       // slots per LDS stage of the MFMA GEMM (4 MFMA k-steps)
-constexpr int OCH = 4;           // octets per block of the nibble-plane generator
+constexpr int MSTAGE = 4;        // slots per LDS stage of the MFMA GEMM (2 MFMA k-steps)
+constexpr int MFMA_BLOCKS_PER_CU = 2;   // resident MFMA GEMM blocks per CU (LDS bound)
+constexpr int OCH = 8;           // octets per block of the nibble-plane generator
 constexpr int64_t MFMA_EXACT = 1ll << 24;   // K * L_max bound for exact fp32 counts
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -79,7 +80,8 @@ __device__ __forceinline__ T *ws_ptr(uint8_t *ws, size_t off) {
 
 struct Layout {
     int KB;            // words per cycle per row = ceil(K/32)
-    int MT, NT;        // row tiles of A and B
+    int MT, NT;        // row tiles of A and B (MFMA engine: NT rounded up to a multiple
+                       // of mbn / 128, the B plane tiles one GEMM block takes)
     int LBS;           // cycle stride of B planes and length of draw arrays (L_max rounded to LCH)
     int LP;            // L_max rounded up to LSTEP
     int nbB;           // batch entries of B planes (1 when B is broadcast)
@@ -87,6 +89,7 @@ struct Layout {
     int engine;        // SC_ENGINE_VALU or SC_ENGINE_MFMA (resolved, never AUTO)
     int KQP;           // MFMA: element quads per octet, ceil(K/4) rounded up to 4
     int tstep;         // tile cycle counts are rounded up to this (LSTEP or MSTEP)
+    int mbn;           // MFMA engine: columns of B per GEMM block (256, or 128 when N <= 128)
     int64_t words_per_L;   // plane words of one 128-row tile per cycle of its length
     size_t off_rA, off_rB, off_status, off_CA;
     size_t off_perm, off_Ls, off_RA, off_tileL, off_tileOff, off_Ap, off_SA;

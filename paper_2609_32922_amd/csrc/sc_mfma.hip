@@ -10,22 +10,26 @@
 //   C-BSG     A holds sgn * D_k (bipolar) or sign(q) * [k < c] (unipolar) over B's draw
 //             counter k, B holds its comparator stream on r^B as above; bipolar then
 //             gives X = (K L + P) / 2 and unipolar S = P (Sec. 4.2, Eq. (6))
-// v_mfma_scale_f32_16x16x128_f8f6f4 with unit scales sums 128 such products into fp32;
+// v_mfma_scale_f32_32x32x64_f8f6f4 with unit scales sums 64 such products into fp32;
 // every partial sum is an integer of magnitude <= K L <= 2^24, so the count is exact
 // and independent of the summation order.
 //
 //   k_mplanes     nibble planes of A (sorted rows, per-row lengths) or B, one block per
-//                 128-row tile x 32 cycles x 64 elements; element parameters and an
-//                 8-cycle lookup table in LDS, 1 KB coalesced stores
-//   k_mgemm       128x128 output tile per 256-thread block, 64x64 per wave as 4x4
-//                 16x16 MFMA blocks, 16 slots (4 MFMA k-steps) per LDS stage
+//                 128-row tile x 64 cycles x 64 elements; element parameters and an
+//                 8-cycle lookup table in LDS, 16-byte stores, 1 KB per wave
+//   k_mgemm       128x256 output tile per 256-thread block, 64x128 per wave as 2x4
+//                 32x32 MFMA blocks (128x128 and 64x64 when N <= 128), 4 slots (2 MFMA
+//                 k-steps of 64) per LDS stage, two LDS buffers (48 KB: two blocks per
+//                 CU).  The 32x32x64 form keeps the matrix cores fed at two waves per
+//                 SIMD, where the 16x16x128 form loses several cycles per instruction to
+//                 issue; the wide wave tile reads 6 KB of LDS per 8 MFMAs.
 //   k_mgemm_reduce sums the partial counts of split tiles and decodes
 #include "sc_internal.h"
 
 namespace scg {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
-typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));   // one slot row: 32 nibbles
 
 constexpr uint32_t NIB_POS = 0x2u;   // e2m1 +1.0
@@ -62,6 +66,7 @@ __global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
     __shared__ uint32_t prm[64 * PRM_STRIDE];    // [element][row] packed parameters
     __shared__ uint32_t lut[OCH * CA_COLS];      // comparator: 8 nibbles per octet and beta
     __shared__ uint32_t spread[256];             // interval: 8-bit mask -> 8 nibbles of +1
+    __shared__ uint32_t rr[OCH * MSTEP];         // comparator: the block's draws
     const int t = blockIdx.x / a.nchunk, ch = blockIdx.x % a.nchunk;
     const int qg = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -128,48 +133,48 @@ __global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
         for (int c = 0; c < 8; ++c) x |= ((v >> c) & 1u) ? (NIB_POS << (4 * c)) : 0u;
         spread[tid] = x;
     } else {
-        const uint32_t *r = ws_ptr<uint32_t>(ws, a.off_r) + (size_t)o0 * MSTEP;
+        if (tid < no * MSTEP) rr[tid] = ws_ptr<uint32_t>(ws, a.off_r)[(size_t)o0 * MSTEP + tid];
+        __syncthreads();
         const uint32_t zero_nib = POL == SC_BIPOLAR_XNOR ? NIB_NEG : 0u;
         for (int e = tid; e < no * CA_COLS; e += 256) {
             const int o = e / CA_COLS, beta = e % CA_COLS;
             uint32_t x = 0;
 #pragma unroll
             for (int c = 0; c < 8; ++c)
-                x |= (r[o * MSTEP + c] < (uint32_t)beta ? NIB_POS : zero_nib) << (4 * c);
+                x |= (rr[o * MSTEP + c] < (uint32_t)beta ? NIB_POS : zero_nib) << (4 * c);
             lut[e] = x;
         }
     }
     __syncthreads();
 
-    // 3. planes: per slot, thread tid writes row tid/4 dword tid%4, then rows 64..127
-    uint32_t *planes = ws_ptr<uint32_t>(wsb, a.off_planes) + off;
+    // 3. planes: thread (half h = tid / 128, row m = tid % 128) writes the 16 bytes of
+    //    row m in slot (octet, quad 2 * pair + h); one wave stores 1 KB contiguously
+    u4 *planes = reinterpret_cast<u4 *>(ws_ptr<uint32_t>(wsb, a.off_planes) + off);
+    const int m = tid & (BM - 1), h = tid >> 7;
     for (int o = 0; o < no; ++o) {
         const int oa = o0 + o, c0 = oa * MSTEP;
-        for (int dq = 0; dq < 16; ++dq) {
-            const int qd = qg * 16 + dq;
+        for (int pr = 0; pr < 8; ++pr) {
+            const int dq = 2 * pr + h, qd = qg * 16 + dq;
             if (qd >= a.KQP) break;
-            uint32_t *dst = planes + ((size_t)oa * a.KQP + qd) * BM * 4;
+            u4 v;
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int idx = tid + 256 * h;
-                const int m = idx >> 2, e = idx & 3;
+            for (int e = 0; e < 4; ++e) {
                 const uint32_t pk = prm[(4 * dq + e) * PRM_STRIDE + m];
-                uint32_t v;
+                uint32_t x;
                 if (CBSG) {
                     const int lo = (int)(pk & 511u), hi = (int)((pk >> 9) & 511u);
                     const int a0 = min(max(lo - c0, 0), 8), a1 = min(max(hi - c0, 0), 8);
-                    const uint32_t bits = ((1u << a1) - 1u) & ~((1u << a0) - 1u);
-                    v = spread[bits];
+                    x = spread[((1u << a1) - 1u) & ~((1u << a0) - 1u)];
                 } else {
                     const int beta = (int)(pk & 511u), Le = (int)((pk >> 9) & 8191u);
                     const int rem = Le - c0;
-                    v = lut[o * CA_COLS + beta];
-                    if (rem <= 0) v = 0u;
-                    else if (rem < 8) v &= (1u << (4 * rem)) - 1u;
+                    x = lut[o * CA_COLS + beta];
+                    if (rem <= 0) x = 0u;
+                    else if (rem < 8) x &= (1u << (4 * rem)) - 1u;
                 }
-                if (pk >> 31) v = negate_nibbles(v);
-                dst[idx] = v;
+                v[e] = (pk >> 31) ? negate_nibbles(x) : x;
             }
+            planes[((size_t)oa * a.KQP + qd) * BM + m] = v;
         }
     }
 }
@@ -220,7 +225,7 @@ hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t
     pb.ld = d.ldb;
     pb.strideX = d.strideB;
     pb.rows = d.N;
-    pb.nchunk = lay.LBS / (OCH * MSTEP);
+    pb.nchunk = (lay.LBS / MSTEP + OCH - 1) / OCH;
     pb.uniformL = d.L_max;
     pb.per_row = 0;
     pb.stride_batch = lay.stride_batchB;
@@ -281,129 +286,220 @@ __device__ __forceinline__ void mdecode4(const int32_t (&P)[4], int p, int j0, i
     }
 }
 
+// Block tile: BM = 128 rows of A x WB columns of B, WB = 256 (two 128-column B plane
+// tiles) or 128 (one; taken when N <= 128, where a wider tile would mostly multiply
+// padding).
+constexpr int PER_TA = MSTAGE * BM / 256;   // u4 of A per thread per stage
+constexpr int KSTEPS = MSTAGE / 2;          // MFMA k-steps (2 slots = 64 k each) per stage
+
+template <int WB>
+struct MTile {
+    static constexpr int PER_TB = MSTAGE * WB / 256;   // u4 of B per thread per stage
+    static constexpr int BUF = MSTAGE * (BM + WB);     // u4 per LDS buffer (A slots, then B)
+    static constexpr int NCB = WB / 64;                // 32-column MFMA blocks per wave
+};
+
+template <int WB>
+struct Stage {
+    u4 a[PER_TA], b[MTile<WB>::PER_TB];
+};
+
+// Loads the stage of slots [ks, ks + MSTAGE) into registers.  A short last stage re-reads
+// its last slot instead of running past the unit (the compute loop never reads those
+// LDS entries), so every load is in bounds.  In pass k thread tid takes A row tid % 128
+// of slot 2k + tid / 128, and B column tid % WB (of the block's WB) of slot
+// k * 256 / WB + tid / WB; columns 128.. come from the second B plane tile.
+template <int WB>
+__device__ __forceinline__ void load_stage(const u4 *gA, const u4 *gB0, const u4 *gB1, int64_t ks,
+                                           int64_t k1, int tid, Stage<WB> &r) {
+    const int last = (int)min((int64_t)MSTAGE, k1 - ks) - 1;
+    const u4 *pa = gA + ks * BM + (tid & (BM - 1));
+    const int col = tid % WB;
+    const u4 *pb = (col < BN ? gB0 : gB1) + ks * BN + (col & (BN - 1));
+#pragma unroll
+    for (int k = 0; k < PER_TA; ++k) r.a[k] = pa[min(2 * k + (tid >> 7), last) * BM];
+#pragma unroll
+    for (int k = 0; k < MTile<WB>::PER_TB; ++k)
+        r.b[k] = pb[min(k * (256 / WB) + tid / WB, last) * BN];
+}
+
+// LDS buffer: A [MSTAGE][128], then B [MSTAGE][WB]
+template <int WB>
+__device__ __forceinline__ void store_stage(u4 *buf, int tid, const Stage<WB> &r) {
+#pragma unroll
+    for (int k = 0; k < PER_TA; ++k) buf[tid + 256 * k] = r.a[k];
+#pragma unroll
+    for (int k = 0; k < MTile<WB>::PER_TB; ++k) buf[MSTAGE * BM + 256 * k + tid] = r.b[k];
+}
+
+// operand fragments of k-step j of an LDS buffer for one wave (64 rows x WB/2 columns):
+// A rows wr + 32i + l%32, B columns wc + 32c + l%32, slot 2j + l/32 (the 32x32x64 operand
+// layout: 32 consecutive k per lane, lanes 32..63 holding the second half of k)
+template <int WB>
+struct Frags {
+    u4 a[2], b[MTile<WB>::NCB];
+};
+template <int WB>
+__device__ __forceinline__ void read_frags(const u4 *buf, int j, int grp, int wr, int wc, int i32,
+                                           Frags<WB> &f) {
+    const u4 *As = buf + (2 * j + grp) * BM, *Bs = buf + MSTAGE * BM + (2 * j + grp) * WB;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) f.a[i] = As[wr + 32 * i + i32];
+#pragma unroll
+    for (int c = 0; c < MTile<WB>::NCB; ++c) f.b[c] = Bs[wc + 32 * c + i32];
+}
+
 __device__ __forceinline__ v8i frag(u4 x) {
-    v8i r = {(int)x.x, (int)x.y, (int)x.z, (int)x.w, 0, 0, 0, 0};
+    v8i r = {(int)x[0], (int)x[1], (int)x[2], (int)x[3], 0, 0, 0, 0};
     return r;
 }
 
-constexpr int PER_T = MSTAGE * BM / 256;   // uint4 of A (and of B) per thread per stage
-
-// Loads the stage of slots [ks, ks + MSTAGE) into registers.  A short last stage re-reads
-// its last slot row instead of running past the unit (the compute loop never reads
-// those LDS entries), so every load is in bounds.
-__device__ __forceinline__ void load_stage(const u4 *gA, const u4 *gB, int64_t ks, int64_t k1,
-                                           int tid, u4 (&ra)[PER_T], u4 (&rb)[PER_T]) {
-    const int last = (int)min((int64_t)MSTAGE, k1 - ks) * BM - 1;
-    const u4 *pa = gA + ks * BM, *pb = gB + ks * BN;
+// the MFMAs of one k-step of a wave's tile
+template <int WB>
+__device__ __forceinline__ void mma(v16f (&acc)[2][MTile<WB>::NCB], const Frags<WB> &f) {
 #pragma unroll
-    for (int k = 0; k < PER_T; ++k) {
-        const int e = min(tid + 256 * k, last);
-        ra[k] = pa[e];
-        rb[k] = pb[e];
-    }
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int c = 0; c < MTile<WB>::NCB; ++c)
+            acc[i][c] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(frag(f.a[i]), frag(f.b[c]),
+                                                                        acc[i][c], 4, 4, 0, 127, 0, 127);
 }
 
-// One block: the 128x128 tile (tm, tn) of batch entry b over a contiguous range of MFMA
-// k-steps (4 slots each).  Wave w owns rows 64*(w/2).., columns 64*(w%2)..; lane l reads
-// slot 4j + l/16 of row (or column) l%16 of each 16-row block, which is the operand
-// layout of the 16x16x128 instruction (32 consecutive k per lane).  The accumulator
-// element e of lane l is row 4*(l/16)+e, column l%16 of its 16x16 block.
-template <bool BIP, bool SPLIT>
+// One stage of the block's pipeline.  On entry the fragments of the stage's first
+// k-step are in fragment set PF, LDS buffer st % 2 holds the stage, and register set
+// 1 - PR holds stage st + 1 (loaded during stage st - 1).  The loads of stage st + 2
+// go into register set PR, so global latency is covered by two stages of MFMAs; k-step
+// j+1's fragments are read while the MFMAs of k-step j issue, and the next stage's
+// first k-step right after the barrier, while the last MFMAs of this stage still run.
+template <int WB, int PF, int PR>
+__device__ __forceinline__ void mstage(int64_t st, int64_t nst, int64_t k0, int64_t k1, const u4 *gA,
+                                       const u4 *gB0, const u4 *gB1, u4 *smem, int tid, int grp,
+                                       int wr, int wc, int i32, v16f (&acc)[2][MTile<WB>::NCB],
+                                       Frags<WB> (&f)[2], Stage<WB> (&r)[2]) {
+    constexpr int BUF = MTile<WB>::BUF;
+    // Loads and LDS reads are issued unconditionally (past the last stage they re-read
+    // the last stage, in bounds, and their data is never used) so that the wait counts
+    // before each use are fixed and only cover the older group.
+    const int64_t ks = k0 + st * MSTAGE, klast = k0 + (nst - 1) * MSTAGE;
+    const int nk = (int)min((int64_t)MSTAGE, k1 - ks) / 2;        // k-steps in this stage
+    const bool more = st + 1 < nst;
+    load_stage<WB>(gA, gB0, gB1, min(ks + 2 * MSTAGE, klast), k1, tid, r[PR]);
+    // keep the loads at the top of the stage: the scheduler would otherwise sink them
+    // next to their LDS stores and expose their latency
+    __builtin_amdgcn_sched_barrier(0);
+    const u4 *buf = smem + (st & 1) * BUF;
+    __builtin_amdgcn_s_setprio(1);       // favour this wave's MFMA issue over its neighbour's
+#pragma unroll
+    for (int j = 0; j < KSTEPS; ++j) {
+        if (j + 1 < KSTEPS) read_frags<WB>(buf, j + 1, grp, wr, wc, i32, f[(PF + j + 1) & 1]);
+        if (j < nk) mma<WB>(acc, f[(PF + j) & 1]);
+    }
+    __builtin_amdgcn_s_setprio(0);
+    __builtin_amdgcn_sched_barrier(0);
+    u4 *nbuf = smem + ((st + 1) & 1) * BUF;
+    if (more) store_stage<WB>(nbuf, tid, r[1 - PR]);
+    __syncthreads();
+    // a stage that has a successor is full: its successor starts in set PF + KSTEPS
+    read_frags<WB>(nbuf, 0, grp, wr, wc, i32, f[(PF + KSTEPS) & 1]);
+}
+
+// One block: the 128 x WB tile (tm, tw) of batch entry b over a contiguous range of MFMA
+// k-steps (2 slots each).  Wave w owns rows 64*(w/2).., columns (WB/2)*(w%2)..; lane l
+// reads slot 2j + l/32 of row (or column) l%32 of each 32-row block.  The accumulator
+// element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32 of its 32x32 block.
+template <bool BIP, bool SPLIT, int WB>
 __global__ __launch_bounds__(256, 2) void k_mgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
-    __shared__ u4 smem[MSTAGE * (BM + BN)];
-    u4 *As = smem, *Bs = smem + MSTAGE * BM;
+    constexpr int BUF = MTile<WB>::BUF, NCB = MTile<WB>::NCB;
+    __shared__ u4 smem[2 * BUF];
+    const int NTW = lay.NT / (WB / BN);
     const int u = blockIdx.x;
     const int s = u % g.S;
     const int tile = u / g.S;
-    const int tn = tile % lay.NT;
-    const int tb = tile / lay.NT;
+    const int tw = tile % NTW;
+    const int tb = tile / NTW;
     const int b = tb % g.batch, tm = tb / g.batch;
     const int bB = g.nbB == 1 ? 0 : b;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int grp = lane >> 4, i16 = lane & 15;
-    const int wr = (w >> 1) * 64, wc = (w & 1) * 64;
+    const int grp = lane >> 5, i32 = lane & 31;
+    const int wr = (w >> 1) * 64, wc = (w & 1) * (WB / 2);
     uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
     uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
     const int Lloop = ws_ptr<int32_t>(wsa, lay.off_tileL)[tm];
-    const int64_t nsteps = (int64_t)(Lloop / MSTEP) * g.KQP / 4;
-    const int64_t k0 = (int64_t)s * nsteps / g.S * 4, k1 = (int64_t)(s + 1) * nsteps / g.S * 4;
+    const int64_t nsteps = (int64_t)(Lloop / MSTEP) * g.KQP / 2;       // k-steps of 2 slots
+    const int64_t k0 = (int64_t)s * nsteps / g.S * 2, k1 = (int64_t)(s + 1) * nsteps / g.S * 2;
     const u4 *gA = reinterpret_cast<const u4 *>(ws_ptr<uint32_t>(wsa, lay.off_Ap) +
                                                 ws_ptr<int64_t>(wsa, lay.off_tileOff)[tm]);
-    const u4 *gB = reinterpret_cast<const u4 *>(ws_ptr<uint32_t>(wsbB, lay.off_Bp)) +
-                   (size_t)tn * (g.LBS / MSTEP) * g.KQP * BN;
+    const size_t btile = (size_t)(g.LBS / MSTEP) * g.KQP * BN;          // u4 per B plane tile
+    const u4 *gB0 = reinterpret_cast<const u4 *>(ws_ptr<uint32_t>(wsbB, lay.off_Bp)) +
+                    (size_t)tw * (WB / BN) * btile;
+    const u4 *gB1 = WB > BN ? gB0 + btile : gB0;
 
-    v4f acc[4][4];
+    v16f acc[2][NCB];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[i][c] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int c = 0; c < NCB; ++c) acc[i][c] = v16f{};
 
-    // software pipeline: the next stage's 16 KB of A and B slots are loaded into
-    // registers while the current stage is multiplied out of LDS
-    u4 ra[PER_T], rb[PER_T];
-    if (k0 < k1) load_stage(gA, gB, k0, k1, tid, ra, rb);
-    for (int64_t ks = k0; ks < k1; ks += MSTAGE) {
-        const int nsl = (int)min((int64_t)MSTAGE, k1 - ks);
-        __syncthreads();
-#pragma unroll
-        for (int k = 0; k < PER_T; ++k) {
-            As[tid + 256 * k] = ra[k];
-            Bs[tid + 256 * k] = rb[k];
-        }
-        __syncthreads();
-        if (ks + MSTAGE < k1) load_stage(gA, gB, ks + MSTAGE, k1, tid, ra, rb);
-#pragma unroll
-        for (int j = 0; j < MSTAGE / 4; ++j) {
-            if (4 * j >= nsl) break;
-            u4 av[4], bv[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) av[i] = As[(4 * j + grp) * BM + wr + 16 * i + i16];
-#pragma unroll
-            for (int c = 0; c < 4; ++c) bv[c] = Bs[(4 * j + grp) * BN + wc + 16 * c + i16];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int c = 0; c < 4; ++c)
-                    acc[i][c] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
-                        frag(av[i]), frag(bv[c]), acc[i][c], 4, 4, 0, 127, 0, 127);
-        }
+    Stage<WB> r[2];
+    Frags<WB> f[2];
+    const int64_t nst = (k1 - k0 + MSTAGE - 1) / MSTAGE;
+    if (nst > 0) {
+        load_stage<WB>(gA, gB0, gB1, k0, k1, tid, r[0]);
+        store_stage<WB>(smem, tid, r[0]);
+        load_stage<WB>(gA, gB0, gB1, k0 + min((int64_t)1, nst - 1) * MSTAGE, k1, tid, r[1]);
+    }
+    __syncthreads();
+    if (nst > 0) read_frags<WB>(smem, 0, grp, wr, wc, i32, f[0]);
+    // stages in pairs, so that the register set of a stage (st % 2) and the fragment set
+    // of its first k-step are fixed at compile time
+    for (int64_t st = 0; st < nst; st += 2) {
+        mstage<WB, 0, 0>(st, nst, k0, k1, gA, gB0, gB1, smem, tid, grp, wr, wc, i32, acc, f, r);
+        if (st + 1 < nst)
+            mstage<WB, KSTEPS & 1, 1>(st + 1, nst, k0, k1, gA, gB0, gB1, smem, tid, grp, wr, wc, i32,
+                                      acc, f, r);
     }
 
     if (SPLIT) {
-        // partial sums of this split as int32 [tile][split][128 rows][128 columns]
-        int32_t *part = ws_ptr<int32_t>(ws, lay.off_part) + ((size_t)tile * g.S + s) * BM * BN;
+        // partial sums of this split as int32 [tile][split][128 rows][WB columns]
+        int32_t *part = ws_ptr<int32_t>(ws, lay.off_part) + ((size_t)tile * g.S + s) * BM * WB;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
+            for (int c = 0; c < NCB; ++c)
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    part[(wr + 16 * i + 4 * grp + e) * BN + wc + 16 * c + i16] = (int32_t)acc[i][c][e];
+                for (int e = 0; e < 16; ++e)
+                    part[(wr + 32 * i + 8 * (e >> 2) + 4 * grp + (e & 3)) * WB + wc + 32 * c + i32] =
+                        (int32_t)acc[i][c][e];
     } else {
-        // transpose through LDS, 64 rows at a time, so that each thread decodes four
+        // transpose through LDS, 32 rows at a time, so that each thread decodes four
         // adjacent columns of one row
-        int32_t *T = reinterpret_cast<int32_t *>(smem);    // 64 x 132 int32
-        constexpr int TS = BN + 4;
-        for (int h = 0; h < 2; ++h) {
+        constexpr int TS = WB + 4, TR = 32;
+        static_assert(TR * TS * 4 <= 2 * BUF * 16, "the epilogue transpose must fit the LDS buffers");
+        int32_t *T = reinterpret_cast<int32_t *>(smem);    // 32 x (WB + 4) int32
+        for (int h = 0; h < BM / TR; ++h) {
             __syncthreads();
-            if (wr == 64 * h) {
+            // pass h holds rows 32h .. 32h + 31: MFMA block i = h % 2 of the waves at wr = 64 (h / 2)
+            if (wr == 64 * (h >> 1)) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < 2; ++i) {
+                    if (i != (h & 1)) continue;
 #pragma unroll
-                    for (int c = 0; c < 4; ++c)
+                    for (int c = 0; c < NCB; ++c)
 #pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            T[(16 * i + 4 * grp + e) * TS + wc + 16 * c + i16] = (int32_t)acc[i][c][e];
+                        for (int e = 0; e < 16; ++e)
+                            T[(8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] =
+                                (int32_t)acc[i][c][e];
+                }
             }
             __syncthreads();
-            for (int k = 0; k < 8; ++k) {
-                const int idx = tid + 256 * k;        // 64 rows x 32 column quads
-                const int rl = idx >> 5, cq = idx & 31;
-                const int j0 = tn * BN + 4 * cq;
+            for (int k = 0; k < TR * (WB / 4) / 256; ++k) {
+                const int idx = tid + 256 * k;        // 32 rows x WB/4 column quads
+                const int rl = idx / (WB / 4), cq = idx % (WB / 4);
+                const int j0 = tw * WB + 4 * cq;
                 if (j0 >= g.N) continue;
                 const int4 v = *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]);
                 const int32_t P[4] = {v.x, v.y, v.z, v.w};
-                mdecode4<BIP>(P, tm * BM + 64 * h + rl, j0, min(4, g.N - j0), b, g, lay, ws);
+                mdecode4<BIP>(P, tm * BM + TR * h + rl, j0, min(4, g.N - j0), b, g, lay, ws);
             }
         }
     }
@@ -411,22 +507,23 @@ __global__ __launch_bounds__(256, 2) void k_mgemm(MGemmArgs g, Layout lay, uint8
 
 // sums the partial counts of every split of a tile and decodes (four blocks per tile,
 // 32 rows each; thread = row x four adjacent columns)
-template <bool BIP>
+template <bool BIP, int WB>
 __global__ __launch_bounds__(256) void k_mgemm_reduce(MGemmArgs g, Layout lay, uint8_t *ws) {
+    const int NTW = lay.NT / (WB / BN);
     const int tile = blockIdx.x >> 2, quarter = blockIdx.x & 3;
-    const int tn = tile % lay.NT;
-    const int tb = tile / lay.NT;
+    const int tw = tile % NTW;
+    const int tb = tile / NTW;
     const int b = tb % g.batch, tm = tb / g.batch;
     const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part) +
-                                                      (size_t)tile * g.S * BM * BN);
-    for (int k = 0; k < 4; ++k) {
-        const int idx = threadIdx.x + 256 * k;        // 32 rows x 32 column quads
-        const int rl = quarter * 32 + (idx >> 5), cq = idx & 31;
-        const int j0 = tn * BN + 4 * cq;
+                                                      (size_t)tile * g.S * BM * WB);
+    for (int k = 0; k < 32 * (WB / 4) / 256; ++k) {
+        const int idx = threadIdx.x + 256 * k;        // 32 rows x WB/4 column quads
+        const int rl = quarter * 32 + idx / (WB / 4), cq = idx % (WB / 4);
+        const int j0 = tw * WB + 4 * cq;
         if (j0 >= g.N) continue;
         int32_t P[4] = {0, 0, 0, 0};
         for (int s = 0; s < g.S; ++s) {
-            const int4 v = base[((size_t)s * BM + rl) * (BN / 4) + cq];
+            const int4 v = base[((size_t)s * BM + rl) * (WB / 4) + cq];
             P[0] += v.x;
             P[1] += v.y;
             P[2] += v.z;
@@ -436,20 +533,27 @@ __global__ __launch_bounds__(256) void k_mgemm_reduce(MGemmArgs g, Layout lay, u
     }
 }
 
-template <bool BIP>
-static hipError_t launch_mgemm_pol(const MGemmArgs &g, const Layout &lay, uint8_t *ws,
-                                   hipStream_t st) {
-    const unsigned tiles = (unsigned)(g.batch * lay.MT * lay.NT);
+template <bool BIP, int WB>
+static hipError_t launch_mgemm_tile(const MGemmArgs &g, const Layout &lay, uint8_t *ws,
+                                    hipStream_t st) {
+    const unsigned tiles = (unsigned)(g.batch * lay.MT * (lay.NT / (WB / BN)));
     if (g.S == 1) {
-        hipLaunchKernelGGL((k_mgemm<BIP, false>), dim3(tiles), dim3(256), 0, st, g, lay, ws);
+        hipLaunchKernelGGL((k_mgemm<BIP, false, WB>), dim3(tiles), dim3(256), 0, st, g, lay, ws);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((k_mgemm<BIP, true>), dim3(tiles * (unsigned)g.S), dim3(256), 0, st, g, lay,
+    hipLaunchKernelGGL((k_mgemm<BIP, true, WB>), dim3(tiles * (unsigned)g.S), dim3(256), 0, st, g, lay,
                        ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_mgemm_reduce<BIP>), dim3(tiles * 4u), dim3(256), 0, st, g, lay, ws);
+    hipLaunchKernelGGL((k_mgemm_reduce<BIP, WB>), dim3(tiles * 4u), dim3(256), 0, st, g, lay, ws);
     return hipGetLastError();
+}
+
+template <bool BIP>
+static hipError_t launch_mgemm_pol(const MGemmArgs &g, const Layout &lay, uint8_t *ws,
+                                   hipStream_t st) {
+    if (lay.mbn == 256) return launch_mgemm_tile<BIP, 256>(g, lay, ws, st);
+    return launch_mgemm_tile<BIP, 128>(g, lay, ws, st);
 }
 
 hipError_t launch_mgemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
