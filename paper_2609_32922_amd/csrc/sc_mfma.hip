@@ -90,20 +90,36 @@ __global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
     const int8_t *Xb = a.X + (size_t)b * a.strideX;
     const uint16_t *CA = CBSG ? ws_ptr<uint16_t>(ws, a.off_CA) : nullptr;
 
-    // 1. element parameters: one wave reads the 64 bytes of one row at a time
+    // 1. element parameters.  Wave w takes rows m = w + 4k, k < 32: lane k first loads
+    //    row k's index and length (one vector load), then the wave issues the 32 element
+    //    loads (64 bytes of one row each) back to back before using any of them.
     const int d = qg * 64 + lane;
-    for (int m = w; m < BM; m += 4) {
-        const int p = t * BM + m;
-        int row, Lr;
+    int rowv = -1, Lv = 0;
+    if (lane < 32) {
+        const int p = t * BM + w + 4 * lane;
         if (a.per_row) {
-            row = perm[p];
-            Lr = row >= 0 ? Ls[p] : 0;
+            rowv = perm[p];
+            Lv = rowv >= 0 ? Ls[p] : 0;
         } else {
-            row = p < a.rows ? p : -1;
-            Lr = a.uniformL;
+            rowv = p < a.rows ? p : -1;
+            Lv = a.uniformL;
         }
+    }
+    // padding rows and elements read row 0 / element 0 (present whenever this kernel
+    // runs: rows >= 1, K >= 1) and are zeroed below, so no load sits behind a branch
+    int qv[32];
+    const int dd = d < a.K ? d : 0;
+#pragma unroll
+    for (int k = 0; k < 32; ++k) {
+        const int row = max(__builtin_amdgcn_readlane(rowv, k), 0);
+        qv[k] = (int)Xb[(size_t)row * a.ld + dd];
+    }
+#pragma unroll
+    for (int k = 0; k < 32; ++k) {
+        const int m = w + 4 * k;
+        const int row = __builtin_amdgcn_readlane(rowv, k), Lr = __builtin_amdgcn_readlane(Lv, k);
         const bool valid = row >= 0 && d < a.K;
-        const int q = valid ? (int)Xb[(size_t)row * a.ld + d] : 0;
+        const int q = valid ? qv[k] : 0;
         const int beta = POL == SC_BIPOLAR_XNOR ? beta_bipolar(q) : beta_unipolar(q);
         uint32_t pk;
         if (CBSG) {
