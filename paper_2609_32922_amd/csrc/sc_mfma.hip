@@ -67,6 +67,7 @@ __global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
     __shared__ uint32_t lut[OCH * CA_COLS];      // comparator: 8 nibbles per octet and beta
     __shared__ uint32_t spread[256];             // interval: 8-bit mask -> 8 nibbles of +1
     __shared__ uint32_t rr[OCH * MSTEP];         // comparator: the block's draws
+    __shared__ int rowok[BM];                    // row of the tile holds data (not padding)
     const int t = blockIdx.x / a.nchunk, ch = blockIdx.x % a.nchunk;
     const int qg = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -107,6 +108,7 @@ __global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
     }
     // padding rows and elements read row 0 / element 0 (present whenever this kernel
     // runs: rows >= 1, K >= 1) and are zeroed below, so no load sits behind a branch
+    if (lane < 32) rowok[w + 4 * lane] = rowv >= 0;
     int qv[32];
     const int dd = d < a.K ? d : 0;
 #pragma unroll
@@ -164,9 +166,12 @@ __global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
     __syncthreads();
 
     // 3. planes: thread (half h = tid / 128, row m = tid % 128) writes the 16 bytes of
-    //    row m in slot (octet, quad 2 * pair + h); one wave stores 1 KB contiguously
+    //    row m in slot (octet, quad 2 * pair + h); one wave stores 1 KB contiguously.
+    //    Padding rows (beyond M or N) are not written: the GEMM reads them (in bounds,
+    //    and every e2m1 code is finite) only into outputs that are never stored.
     u4 *planes = reinterpret_cast<u4 *>(ws_ptr<uint32_t>(wsb, a.off_planes) + off);
     const int m = tid & (BM - 1), h = tid >> 7;
+    const bool store_row = rowok[m] != 0;
     for (int o = 0; o < no; ++o) {
         const int oa = o0 + o, c0 = oa * MSTEP;
         for (int pr = 0; pr < 8; ++pr) {
@@ -190,7 +195,7 @@ __global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
                 }
                 v[e] = (pk >> 31) ? negate_nibbles(x) : x;
             }
-            planes[((size_t)oa * a.KQP + qd) * BM + m] = v;
+            if (store_row) planes[((size_t)oa * a.KQP + qd) * BM + m] = v;
         }
     }
 }
@@ -537,6 +542,8 @@ __global__ __launch_bounds__(256) void k_mgemm_reduce(MGemmArgs g, Layout lay, u
         const int rl = quarter * 32 + idx / (WB / 4), cq = idx % (WB / 4);
         const int j0 = tw * WB + 4 * cq;
         if (j0 >= g.N) continue;
+        // padding rows hold sums of unwritten plane rows: never read them
+        if (ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_perm)[tm * BM + rl] < 0) continue;
         int32_t P[4] = {0, 0, 0, 0};
         for (int s = 0; s < g.S; ++s) {
             const int4 v = base[((size_t)s * BM + rl) * (WB / 4) + cq];
