@@ -213,6 +213,25 @@ __device__ __forceinline__ void popc_acc(int32_t &acc, uint32_t x) {
 // ----------------------------------------------------------------------------
 // per-row length scheduler (one 1024-thread block per batch entry)
 // ----------------------------------------------------------------------------
+// Adds 1 to hist[l] for every active lane and returns the lane's old value (its place
+// in bucket l).  The lanes that share the first active lane's l take one LDS atomic
+// together, the others one each: equal lengths (the common case) cost one atomic per
+// wave instead of one per row, and mixed lengths cost what single atomics cost.
+__device__ int wave_bucket_add(int *hist, int l, bool active) {
+    const int lane = threadIdx.x & 63;
+    const uint64_t act = __ballot(active);
+    if (act == 0) return 0;
+    const int leader = __ffsll((unsigned long long)act) - 1;
+    const int lv = __builtin_amdgcn_readlane(l, leader);
+    const bool mine = active && l == lv;
+    const uint64_t grp = __ballot(mine);
+    int base = 0;
+    if (lane == leader) base = atomicAdd(&hist[lv], __popcll(grp));
+    base = __builtin_amdgcn_readlane(base, leader);
+    if (mine) return base + __popcll(grp & ((1ull << lane) - 1));
+    return active ? atomicAdd(&hist[l], 1) : 0;
+}
+
 __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L, int64_t strideL,
                                                    int M, int L_max, Layout lay, uint8_t *ws) {
     __shared__ int hist[SC_L_MAX_LIMIT + 1];
@@ -228,13 +247,14 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 
     for (int v = tid; v <= L_max; v += 1024) hist[v] = 0;
     __syncthreads();
-    for (int i = tid; i < M; i += 1024) {
-        int l = Lb[i];
+    for (int i0 = 0; i0 < M; i0 += 1024) {
+        const int i = i0 + tid;
+        int l = i < M ? Lb[i] : 0;
         if (l < 0 || l > L_max) {
             atomicOr(status, STATUS_BAD_LENGTH);
             l = 0;
         }
-        atomicAdd(&hist[l], 1);
+        wave_bucket_add(hist, l, i < M);
     }
     __syncthreads();
     // start position of each length bucket, longest lengths first
@@ -248,13 +268,16 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         carry += tot;
         __syncthreads();
     }
-    for (int i = tid; i < M; i += 1024) {
-        int l = Lb[i];
+    for (int i0 = 0; i0 < M; i0 += 1024) {
+        const int i = i0 + tid;
+        int l = i < M ? Lb[i] : 0;
         if (l < 0 || l > L_max) l = 0;
-        const int pos = atomicAdd(&hist[l], 1);
-        perm[pos] = i;
-        Ls[pos] = l;
-        RA[pos] = 0;
+        const int pos = wave_bucket_add(hist, l, i < M);
+        if (i < M) {
+            perm[pos] = i;
+            Ls[pos] = l;
+            RA[pos] = 0;
+        }
     }
     for (int p = M + tid; p < lay.MT * BM; p += 1024) {
         perm[p] = -1;

@@ -527,31 +527,44 @@ __global__ __launch_bounds__(256, 2) void k_mgemm(MGemmArgs g, Layout lay, uint8
 }
 
 // sums the partial counts of every split of a tile and decodes (four blocks per tile,
-// 32 rows each; thread = row x four adjacent columns)
+// 32 rows each; thread = row x four adjacent columns).  The partial tiles are full-size,
+// so every load is in bounds and all of a split's loads are issued together; padding
+// rows and columns are dropped only at the decode.
 template <bool BIP, int WB>
 __global__ __launch_bounds__(256) void k_mgemm_reduce(MGemmArgs g, Layout lay, uint8_t *ws) {
+    constexpr int NK = 32 * (WB / 4) / 256;           // row x column-quad items per thread
     const int NTW = lay.NT / (WB / BN);
     const int tile = blockIdx.x >> 2, quarter = blockIdx.x & 3;
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tm = tb / g.batch;
     const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part) +
-                                                      (size_t)tile * g.S * BM * WB);
-    for (int k = 0; k < 32 * (WB / 4) / 256; ++k) {
+                                                      (size_t)tile * g.S * BM * WB) +
+                       (size_t)quarter * 32 * (WB / 4) + threadIdx.x;
+    int4 sum[NK];
+#pragma unroll
+    for (int k = 0; k < NK; ++k) sum[k] = make_int4(0, 0, 0, 0);
+    for (int s = 0; s < g.S; ++s) {
+        const int4 *src = base + (size_t)s * BM * (WB / 4);
+        int4 v[NK];
+#pragma unroll
+        for (int k = 0; k < NK; ++k) v[k] = src[256 * k];
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+            sum[k].x += v[k].x;
+            sum[k].y += v[k].y;
+            sum[k].z += v[k].z;
+            sum[k].w += v[k].w;
+        }
+    }
+    const int32_t *perm = ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_perm);
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
         const int idx = threadIdx.x + 256 * k;        // 32 rows x WB/4 column quads
         const int rl = quarter * 32 + idx / (WB / 4), cq = idx % (WB / 4);
         const int j0 = tw * WB + 4 * cq;
-        if (j0 >= g.N) continue;
-        // padding rows hold sums of unwritten plane rows: never read them
-        if (ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_perm)[tm * BM + rl] < 0) continue;
-        int32_t P[4] = {0, 0, 0, 0};
-        for (int s = 0; s < g.S; ++s) {
-            const int4 v = base[((size_t)s * BM + rl) * (WB / 4) + cq];
-            P[0] += v.x;
-            P[1] += v.y;
-            P[2] += v.z;
-            P[3] += v.w;
-        }
+        if (j0 >= g.N || perm[tm * BM + rl] < 0) continue;
+        const int32_t P[4] = {sum[k].x, sum[k].y, sum[k].z, sum[k].w};
         mdecode4<BIP>(P, tm * BM + rl, j0, min(4, g.N - j0), b, g, lay, ws);
     }
 }
