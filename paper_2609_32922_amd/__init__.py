@@ -9,7 +9,7 @@ back to the CPU: without the built library every call raises.
 """
 from __future__ import annotations
 
-from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_L_MAX_LIMIT, SC_OK,  # noqa: F401
+from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_ERR_ENGINE, SC_L_MAX_LIMIT, SC_OK,  # noqa: F401
                    SC_ENGINE_AUTO, SC_ENGINE_MFMA, SC_ENGINE_VALU, SC_RNG_LFSR32,
                    SC_RNG_SOBOL8_CBSG, SC_UNIPOLAR_AND_SM, ScError, ScGemmDesc, load, sc_comparator_sequence,
                    sc_gemm, sc_gemm_status, sc_gemm_workspace_size, sc_mp_lengths, sc_quantize,

@@ -356,3 +356,35 @@ def test_cbsg_workload_vitb16_fc1_mp64(dev, oracle_mod):
 
 def test_cbsg_workload_ditxl2_proj_mlp_group96(dev, oracle_mod):
     _check_workload(W.ditxl2_proj_mlp_group96(), dev, oracle_mod, nrows=16, ncols=48, seq=1)
+
+
+# --------------------------------------------------------------------------
+# the MFMA engine's exactness bound: fp32 sums of +-1 products stay exact while every
+# partial sum is an integer of magnitude <= K * L <= 2^24
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("polarity", [0, 1])
+def test_mfma_exact_at_the_bound(dev, oracle_mod, polarity):
+    import paper_2609_32922_amd as scg
+    rng = np.random.default_rng(171 + polarity)
+    K, L = 65536, 256                          # K * L = 2^24 exactly
+    g = W.random_gemm(rng, 1, 3, 5, K, L, polarity, 171, L_lo=L)
+    # saturated operands drive the counts to their extremes (|2X - K L| up to K L)
+    g.A[0, 0] = 127
+    g.B[0, 0] = 127 if polarity == 0 else -127
+    g.A[0, 1] = -127
+    _note("mfma at K*L = 2^24, polarity %d" % polarity)
+    out, cnt = _run(g, dev, engine=scg.SC_ENGINE_MFMA)
+    _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "bound")
+
+
+def test_auto_engine_past_the_bound(dev, oracle_mod):
+    """K * L_max = 2^25: AUTO runs the VALU engine (int32 counts), MFMA is refused."""
+    import paper_2609_32922_amd as scg
+    rng = np.random.default_rng(181)
+    g = W.random_gemm(rng, 1, 2, 3, 65536, 512, 0, 181, L_lo=500)
+    _note("auto engine at K*L_max = 2^25")
+    out, cnt = _run(g, dev, engine=scg.SC_ENGINE_AUTO)
+    _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "auto past bound")
+    with pytest.raises(scg.ScError) as ei:
+        _run(g, dev, engine=scg.SC_ENGINE_MFMA)
+    assert ei.value.code == scg.SC_ERR_ENGINE
