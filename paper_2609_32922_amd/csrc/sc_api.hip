@@ -1,6 +1,7 @@
 // Host side of libscgemm: argument checks, workspace layout and the launch sequence.
 // Every check runs before anything is enqueued; the library allocates nothing.
 #include <limits.h>
+#include <math.h>
 
 #include "sc_internal.h"
 
@@ -37,6 +38,8 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.NT = (d.N + BN - 1) / BN;
     l.mbn = l.NT > 1 ? 2 * BN : BN;
     if (mfma) l.NT = (int)round_up(l.NT, l.mbn / BN);
+    l.mbm = (mfma && l.MT > 1 && l.mbn == 2 * BN) ? 2 * BM : BM;
+    if (l.mbm == 2 * BM) l.MT = (int)round_up(l.MT, 2);
     l.LBS = (int)round_up(d.L_max, LCH);
     l.LP = (int)round_up(d.L_max, LSTEP);
     l.nbB = (d.strideB == 0) ? 1 : d.batch;
@@ -101,23 +104,60 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     if (!mul_ok(bb, (size_t)l.nbB, &totB)) return false;
     off += totB;
 
-    // split count of the GEMM tiles.  Estimated time of split s: the busiest slot (a
-    // resident block) runs ceil(units/slots) units of average work, plus the excess of
-    // the heaviest unit over the average (row tiles run as long as their longest row: up
-    // to L_max when the lengths vary, while the average follows the mean length L_hint),
-    // plus, for s > 1, writing and summing s partial tiles.  Units are dealt to the
-    // eight XCDs round-robin, so s is a power of two: each XCD then keeps one k-range of
-    // its tiles, and its L2 serves that range to all of them.  Rates are the measured
-    // order of magnitude: VALU engine 2.8e12 bit pairs/s per CU; MFMA engine 4.8e12
-    // products/s per resident block (two per CU); partial sums at 3e12 B/s.
-    const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * l.MT * (mfma ? l.NT / (l.mbn / BN) : l.NT);
+    // Division of the GEMM tiles into work units.
+    const bool quad = mfma && l.mbm == 2 * BM;
+    const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * (l.MT / (l.mbm / BM)) *
+                          (mfma ? l.NT / (l.mbn / BN) : l.NT);
     const int kunits = mfma ? l.KQP / 2 : l.KB;     // indivisible steps along K per cycle
-    const int slots = mfma ? CUS * MFMA_BLOCKS_PER_CU : CUS;
-    const double rate = mfma ? 4.8e12 : 2.8e12;
-    const double tile_bytes = (double)BM * (mfma ? l.mbn : BN) * 4.0;
+    const double tile_bytes = (double)l.mbm * (mfma ? l.mbn : BN) * 4.0;
+    const double Lmean = d.L_hint > 0 ? d.L_hint : d.L_max;
     l.S = 1;
-    if (tiles > 0 && kunits > 1) {
-        const double Lmean = d.L_hint > 0 ? d.L_hint : d.L_max;
+    l.F = 0;
+    if (quad && tiles > 0) {
+        // 256 x 256 tiles, one block per CU, taking whole tiles or parts of tiles.  The
+        // estimated makespan of a division is the larger of its rounds of average units and
+        // its longest unit (a tile pair runs as long as its longest row: up to L_max, while
+        // the mean follows L_hint), plus writing and summing the partial sums of the split
+        // tiles.  Candidates: every tile split s ways (F = 0), or whole tiles in full rounds
+        // with the tiles of a last partial round split to fill one round.
+        const double per_L = (double)l.mbm * l.mbn * 4.0 * l.KQP / MFMA_QUAD_RATE;
+        const double avgT = per_L * Lmean, maxT = per_L * d.L_max;
+        const auto red = [&](int64_t split_tiles, int s) {
+            return s > 1 ? (double)split_tiles * (2 * s) * tile_bytes / 3e12 + 5e-6 : 0.0;
+        };
+        double best = 0.0;
+        for (int s = 1; s <= MAX_SPLIT && s <= (kunits > 0 ? kunits : 1); ++s) {
+            const int64_t units = tiles * s;
+            const double est = fmax((double)((units + CUS - 1) / CUS) * avgT / s, maxT / s) + red(tiles, s);
+            if (s == 1 || est < best * 0.97) {
+                best = est;
+                l.S = s;
+            }
+        }
+        const int64_t R = tiles % CUS;
+        int s2 = R > 0 ? (int)(CUS / R) : 1;
+        s2 = s2 > MAX_SPLIT ? MAX_SPLIT : s2;
+        if (s2 > kunits) s2 = kunits;
+        if (tiles >= CUS && R > 0 && s2 > 1) {
+            const double est = fmax((double)(tiles / CUS) * avgT + avgT / s2, maxT) + red(R, s2);
+            if (est < best * 0.97) {
+                best = est;
+                l.F = (int)(tiles - R);
+                l.S = s2;
+            }
+        }
+        if (l.S == 1) l.F = (int)tiles;
+    } else if (tiles > 0 && kunits > 1) {
+        // 128-row tiles: every tile split s ways.  Estimated time of split s: the busiest
+        // slot (a resident block) runs ceil(units/slots) units of average work, plus the
+        // excess of the heaviest unit over the average, plus, for s > 1, writing and summing
+        // s partial tiles.  MFMA units are dealt to the eight XCDs round-robin, so s is a
+        // power of two: each XCD then keeps one k-range of its tiles, and its L2 serves that
+        // range to all of them.  Rates are the measured order of magnitude: VALU engine
+        // 2.8e12 bit pairs/s per CU; MFMA engine 4.8e12 products/s per resident block (two
+        // per CU); partial sums at 3e12 B/s.
+        const int slots = mfma ? CUS * MFMA_BLOCKS_PER_CU : CUS;
+        const double rate = mfma ? 4.8e12 : 2.8e12;
         const double per_L = mfma ? (double)BM * l.mbn * 4.0 * l.KQP : (double)BM * BN * 32.0 * l.KB;
         double best = 0.0;
         for (int s = 1; s <= MAX_SPLIT && s <= kunits; s = mfma ? 2 * s : s + 1) {
@@ -136,7 +176,8 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.off_part = off;
     if (l.S > 1) {
         size_t partb;
-        if (!mul_ok((size_t)tiles * (size_t)l.S, (size_t)BM * (mfma ? l.mbn : BN) * 4, &partb)) return false;
+        const int64_t split_tiles = quad ? tiles - l.F : tiles;
+        if (!mul_ok((size_t)split_tiles * (size_t)l.S, (size_t)tile_bytes, &partb)) return false;
         off = align256(off + partb);
     }
 

@@ -9,7 +9,8 @@
 //     perm[MT*BM]      sorted position -> original row (or -1 for padding)
 //     Ls[MT*BM]        stream length at each sorted position
 //     RA[MT*BM]        row marginal  sum_d sum_{l<L} zA   (bipolar, both sequences)
-//     tileL[MT]        cycles the GEMM runs for row tile t (max L in tile, padded to 4)
+//     tileL[MT]        cycles the GEMM runs for row tile t (max L in tile, padded to 4; MFMA
+//                      engine with 256-row blocks: max L of the tile pair, padded to 8)
 //     tileOff[MT]      word offset of tile t's planes inside Ap
 //     Ap               bit planes of A: for tile t, words [KB][tileL[t]][BM]
 //     SA               sign planes of A (unipolar; bipolar C-BSG): [MT][KB][BM]
@@ -58,7 +59,8 @@ constexpr int MODE_CBSG = 2;     // bipolar C-BSG: popc((D & Z) ^ sA) plus A's m
 // MFMA engine
 constexpr int MSTEP = 8;         // cycles per octet (tile lengths padded to it)
 constexpr int MSTAGE = 4;        // slots per LDS stage of the MFMA GEMM (2 MFMA k-steps)
-constexpr int MFMA_BLOCKS_PER_CU = 2;   // resident MFMA GEMM blocks per CU (LDS bound)
+constexpr int MFMA_BLOCKS_PER_CU = 2;   // resident 128-row MFMA GEMM blocks per CU (LDS bound)
+constexpr double MFMA_QUAD_RATE = 1.1e13;  // products/s of one 256 x 256 GEMM block (one per CU)
 constexpr int OCH = 8;           // octets per block of the nibble-plane generator
 constexpr int64_t MFMA_EXACT = 1ll << 24;   // K * L_max bound for exact fp32 counts
 
@@ -90,6 +92,9 @@ struct Layout {
     int KQP;           // MFMA: element quads per octet, ceil(K/4) rounded up to 4
     int tstep;         // tile cycle counts are rounded up to this (LSTEP or MSTEP)
     int mbn;           // MFMA engine: columns of B per GEMM block (256, or 128 when N <= 128)
+    int mbm;           // MFMA engine: rows of A per GEMM block: 256 (row tiles taken in pairs
+                       // that run at the pair's longest length; MT even) when mbn = 256 and
+                       // MT > 1, else 128
     int64_t words_per_L;   // plane words of one 128-row tile per cycle of its length
     size_t off_rA, off_rB, off_status, off_CA;
     size_t off_perm, off_Ls, off_RA, off_tileL, off_tileOff, off_Ap, off_SA;
@@ -97,7 +102,8 @@ struct Layout {
     size_t off_Bp, off_SB, off_RB;
     size_t stride_batchB;          // bytes per B batch entry block
     int S;             // splits of the element blocks per GEMM tile (1 = no split)
-    size_t off_part;   // partial counts of split tiles: [tiles][S][256 threads][64] int32
+    int F;             // 256-row GEMM: tiles 0 .. F-1 run whole, tiles F.. in S parts each
+    size_t off_part;   // partial counts of split tiles: [split tiles][S][tile rows][tile columns]
     size_t total;
 };
 

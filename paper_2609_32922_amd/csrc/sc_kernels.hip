@@ -286,13 +286,15 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     }
     __threadfence_block();
     __syncthreads();
-    // tile lengths (first sorted row of a tile holds its longest length) and offsets
+    // tile lengths (first sorted row of a tile holds its longest length; a pair of tiles
+    // that one 256-row block takes runs at the pair's longest length) and offsets
     carry = 0;
     for (int c = 0; c < lay.MT; c += 1024) {
         const int t = c + tid;
         int tl = 0;
         if (t < lay.MT) {
-            tl = (int)round_up(Ls[(size_t)t * BM], lay.tstep);
+            const int t0 = lay.mbm == 2 * BM ? (t & ~1) : t;
+            tl = (int)round_up(Ls[(size_t)t0 * BM], lay.tstep);
             tileL[t] = tl;
         }
         int64_t tot;

@@ -17,12 +17,17 @@
 //   k_mplanes     nibble planes of A (sorted rows, per-row lengths) or B, one block per
 //                 128-row tile x 64 cycles x 64 elements; element parameters and an
 //                 8-cycle lookup table in LDS, 16-byte stores, 1 KB per wave
-//   k_mgemm       128x256 output tile per 256-thread block, 64x128 per wave as 2x4
-//                 32x32 MFMA blocks (128x128 and 64x64 when N <= 128), 4 slots (2 MFMA
-//                 k-steps of 64) per LDS stage, two LDS buffers (48 KB: two blocks per
-//                 CU).  The 32x32x64 form keeps the matrix cores fed at two waves per
-//                 SIMD, where the 16x16x128 form loses several cycles per instruction to
-//                 issue; the wide wave tile reads 6 KB of LDS per 8 MFMAs.
+//   k_qgemm       256x256 output tile per 256-thread block, one block per CU, 128x128
+//                 per wave as 4x4 32x32 MFMA blocks, three LDS buffers of 4 slots (96 KB),
+//                 memory instructions interleaved one per MFMA; taken when N > 128 and
+//                 M > 128.  Whole tiles in full rounds, the tiles of a last partial round
+//                 (or every tile, when row lengths vary) split along k.
+//   k_qgemm_reduce sums the partial counts of its split tiles and decodes
+//   k_mgemm       128x256 output tile per 256-thread block (128x128 and 64x64 when N <=
+//                 128), 64x128 per wave as 2x4 32x32 MFMA blocks, 4 slots (2 MFMA k-steps
+//                 of 64) per LDS stage, two LDS buffers (48 KB: two blocks per CU).  The
+//                 32x32x64 form keeps the matrix cores fed where the 16x16x128 form loses
+//                 several cycles per instruction to issue.
 //   k_mgemm_reduce sums the partial counts of split tiles and decodes
 #include "sc_internal.h"
 
@@ -263,7 +268,7 @@ hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t
 // MFMA GEMM
 // ----------------------------------------------------------------------------
 struct MGemmArgs {
-    int M, N, K, KQP, LBS, nbB, batch, S;
+    int M, N, K, KQP, LBS, nbB, batch, S, F;
     const float *sA, *sB;
     int64_t strideSA, strideSB, strideO, ldo;
     float *out;
@@ -585,9 +590,298 @@ static hipError_t launch_mgemm_tile(const MGemmArgs &g, const Layout &lay, uint8
     return hipGetLastError();
 }
 
+// ----------------------------------------------------------------------------
+// 256 x 256 GEMM tile: a pair of A row tiles (equal cycle counts) x a pair of B tiles,
+// one 256-thread block per CU.  Wave w owns rows 128 (w / 2).., columns 128 (w % 2).. as
+// 4 x 4 32x32 MFMA blocks (its 256 accumulator registers); per MFMA k-step it reads 8 KB
+// of LDS for 16 MFMAs, two thirds of what the 128-row tile needs per product.  A stage
+// is QSTAGE slots (two k-steps) in one of three LDS buffers: stage st computes from
+// buffer st % 3 while stage st + 2 is written into the third buffer, so the first
+// fragments of stage st + 1 can be read before the barrier that ends stage st.
+// ----------------------------------------------------------------------------
+constexpr int QSTAGE = 4;                     // slots per stage
+constexpr int QKS = QSTAGE / 2;               // MFMA k-steps per stage
+constexpr int QBUF = QSTAGE * 512;            // u4 per LDS buffer: A [QSTAGE][256], B [QSTAGE][256]
+constexpr int QNBUF = 3;
+
+struct QRegs {
+    u4 a[QSTAGE], b[QSTAGE];
+};
+struct QFrags {
+    u4 a[4], b[4];
+};
+
+// Thread tid loads row tid % 128 of A tile tid / 128 of the pair (and the same of B) for
+// each slot of the stage starting at slot ks.  A short last stage re-reads its last slot
+// (never used), so every load is in bounds.
+__device__ __forceinline__ void q_load(const u4 *pa, const u4 *pb, int64_t ks, int64_t k1, QRegs &r) {
+    const int last = (int)min((int64_t)QSTAGE, k1 - ks) - 1;
+    const u4 *a = pa + ks * BM, *b = pb + ks * BN;
+#pragma unroll
+    for (int k = 0; k < QSTAGE; ++k) r.a[k] = a[min(k, last) * BM];
+#pragma unroll
+    for (int k = 0; k < QSTAGE; ++k) r.b[k] = b[min(k, last) * BN];
+}
+
+__device__ __forceinline__ void q_store(u4 *buf, int tid, const QRegs &r) {
+#pragma unroll
+    for (int k = 0; k < QSTAGE; ++k) buf[256 * k + tid] = r.a[k];
+#pragma unroll
+    for (int k = 0; k < QSTAGE; ++k) buf[QSTAGE * 256 + 256 * k + tid] = r.b[k];
+}
+
+// fragments of k-step j: A rows wr + 32i + l%32, B columns wc + 32c + l%32, slot 2j + l/32
+__device__ __forceinline__ void q_frags(const u4 *buf, int j, int grp, int wr, int wc, int i32,
+                                        QFrags &f) {
+    const u4 *As = buf + (2 * j + grp) * 256, *Bs = buf + QSTAGE * 256 + (2 * j + grp) * 256;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f.a[i] = As[wr + 32 * i + i32];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) f.b[c] = Bs[wc + 32 * c + i32];
+}
+
+__device__ __forceinline__ void q_mma(v16f (&acc)[4][4], const QFrags &f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            acc[i][c] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(frag(f.a[i]), frag(f.b[c]),
+                                                                        acc[i][c], 4, 4, 0, 127, 0, 127);
+}
+
+// Stage st.  On entry buffer cb = st % 3 holds stage st and the next buffer stage st + 1
+// (both visible), fragment set 0 holds the first k-step of stage st, register set 1 - PR
+// stage st + 2 and set PR is free.  The stage loads stage st + 3 into set PR and writes
+// set 1 - PR into the third buffer.  A FULL stage (both k-steps present: one branch-free
+// region) interleaves its memory instructions one per MFMA: with one wave per SIMD the
+// wave issues in order, and a burst of LDS or global instructions would hold back the
+// next MFMA (measured: 0.83 against 1.20 ms for the 6304 x 768 x 3072 layer at L = 128).
+template <int PR, bool FULL>
+__device__ __forceinline__ void q_stage(int st, int nst, int64_t k0, int64_t k1, int cb, const u4 *pa,
+                                        const u4 *pb, u4 *smem, int tid, int grp, int wr, int wc,
+                                        int i32, v16f (&acc)[4][4], QFrags (&f)[2], QRegs (&r)[2]) {
+    static_assert(QKS == 2, "the interleave below is written for two k-steps per stage");
+    const int64_t klast = k0 + (int64_t)(nst - 1) * QSTAGE;
+    const int64_t ks = k0 + (int64_t)st * QSTAGE;
+    const int nb = cb == QNBUF - 1 ? 0 : cb + 1, wb = nb == QNBUF - 1 ? 0 : nb + 1;
+    const u4 *buf = smem + cb * QBUF;
+    u4 *wbuf = smem + wb * QBUF;
+    const u4 *nbuf = smem + nb * QBUF;
+    if (FULL) {
+        q_frags(buf, 1, grp, wr, wc, i32, f[1]);
+        q_load(pa, pb, min(ks + 3 * QSTAGE, klast), k1, r[PR]);
+        q_mma(acc, f[0]);
+        q_store(wbuf, tid, r[1 - PR]);
+        q_frags(nbuf, 0, grp, wr, wc, i32, f[0]);
+        q_mma(acc, f[1]);
+        // issue order: k-step 0 with the reads of k-step 1's fragments, then the global
+        // loads; k-step 1 with the LDS writes, then the reads of the next stage's first
+        // fragments
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global load
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // LDS write
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+    } else {
+        const int nk = (int)min((int64_t)QSTAGE, k1 - ks) / 2;
+        q_load(pa, pb, min(ks + 3 * QSTAGE, klast), k1, r[PR]);
+        q_frags(buf, 1, grp, wr, wc, i32, f[1]);
+        q_store(wbuf, tid, r[1 - PR]);
+        q_mma(acc, f[0]);
+        q_frags(nbuf, 0, grp, wr, wc, i32, f[0]);
+        if (nk > 1) q_mma(acc, f[1]);
+    }
+    __syncthreads();
+}
+
+// One work unit: tile `tile` (pair tp of batch entry b x B pair tw) over k-steps
+// [s, s + 1) / S of the pair's k-steps.  Units 0 .. F-1 are the whole tiles 0 .. F-1,
+// decoded here; unit F + v is part v % S of tile F + v / S, stored as a partial sum.
+template <bool BIP>
+__global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
+    static_assert(QKS % 2 == 0, "the fragment sets alternate within a stage");
+    __shared__ u4 smem[QNBUF * QBUF];
+    const int NTW = lay.NT / 2;
+    const int u = blockIdx.x;
+    const bool split = u >= g.F;
+    const int v = u - g.F;
+    const int s = split ? v % g.S : 0;
+    const int S = split ? g.S : 1;
+    const int tile = split ? g.F + v / g.S : u;
+    const int tw = tile % NTW;
+    const int tb = tile / NTW;
+    const int b = tb % g.batch, tp = tb / g.batch;
+    const int bB = g.nbB == 1 ? 0 : b;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int grp = lane >> 5, i32 = lane & 31;
+    const int wr = (w >> 1) * 128, wc = (w & 1) * 128;
+    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
+    uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
+    const int Lloop = ws_ptr<int32_t>(wsa, lay.off_tileL)[2 * tp];
+    const int64_t nsteps = (int64_t)(Lloop / MSTEP) * g.KQP / 2;
+    const int64_t k0 = (int64_t)s * nsteps / S * 2, k1 = (int64_t)(s + 1) * nsteps / S * 2;
+    const int half = tid >> 7;
+    const u4 *pa = reinterpret_cast<const u4 *>(ws_ptr<uint32_t>(wsa, lay.off_Ap) +
+                                                ws_ptr<int64_t>(wsa, lay.off_tileOff)[2 * tp + half]) +
+                   (tid & (BM - 1));
+    const size_t btile = (size_t)(g.LBS / MSTEP) * g.KQP * BN;
+    const u4 *pb = reinterpret_cast<const u4 *>(ws_ptr<uint32_t>(wsbB, lay.off_Bp)) +
+                   (size_t)(2 * tw + half) * btile + (tid & (BN - 1));
+
+    v16f acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[i][c] = v16f{};
+
+    QRegs r[2];
+    QFrags f[2];
+    const int nst = (int)((k1 - k0 + QSTAGE - 1) / QSTAGE);
+    if (nst > 0) {
+        const int64_t klast = k0 + (int64_t)(nst - 1) * QSTAGE;
+        q_load(pa, pb, k0, k1, r[0]);
+        q_load(pa, pb, min(k0 + QSTAGE, klast), k1, r[1]);
+        q_store(smem, tid, r[0]);
+        q_store(smem + QBUF, tid, r[1]);
+        q_load(pa, pb, min(k0 + 2 * QSTAGE, klast), k1, r[1]);
+    }
+    __syncthreads();
+    if (nst > 0) q_frags(smem, 0, grp, wr, wc, i32, f[0]);
+    // the first fragments complete before the loop, so that its first MFMAs need no wait
+    __syncthreads();
+    // pairs of full stages (neither is the last one), then the last one or two stages:
+    // the loop body is branch-free and its back edge always carries the same loads
+    int st = 0, cb = 0;
+    for (; st + 2 < nst; st += 2) {
+        q_stage<0, true>(st, nst, k0, k1, cb, pa, pb, smem, tid, grp, wr, wc, i32, acc, f, r);
+        cb = cb == QNBUF - 1 ? 0 : cb + 1;
+        q_stage<1, true>(st + 1, nst, k0, k1, cb, pa, pb, smem, tid, grp, wr, wc, i32, acc, f, r);
+        cb = cb == QNBUF - 1 ? 0 : cb + 1;
+    }
+    if (st < nst) {
+        q_stage<0, false>(st, nst, k0, k1, cb, pa, pb, smem, tid, grp, wr, wc, i32, acc, f, r);
+        cb = cb == QNBUF - 1 ? 0 : cb + 1;
+    }
+    if (st + 1 < nst) q_stage<1, false>(st + 1, nst, k0, k1, cb, pa, pb, smem, tid, grp, wr, wc, i32, acc, f, r);
+
+    if (split) {
+        // partial sums of this unit as int32 [256 rows][256 columns]
+        int32_t *part = ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    part[(wr + 32 * i + 8 * (e >> 2) + 4 * grp + (e & 3)) * 256 + wc + 32 * c + i32] =
+                        (int32_t)acc[i][c][e];
+    } else {
+        // transpose through LDS, 64 rows at a time, so that each thread decodes four
+        // adjacent columns of one row
+        constexpr int TS = 256 + 4, TR = 64;
+        static_assert(TR * TS * 4 <= QNBUF * QBUF * 16, "the epilogue transpose must fit the LDS buffers");
+        int32_t *T = reinterpret_cast<int32_t *>(smem);
+        for (int h = 0; h < 256 / TR; ++h) {
+            __syncthreads();
+            // rows 64h .. 64h + 63: MFMA blocks i = 2 (h % 2), 2 (h % 2) + 1 of the waves at wr = 128 (h / 2)
+            if (wr == 128 * (h >> 1)) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if ((i >> 1) != (h & 1)) continue;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+#pragma unroll
+                        for (int e = 0; e < 16; ++e)
+                            T[(32 * (i & 1) + 8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] =
+                                (int32_t)acc[i][c][e];
+                }
+            }
+            __syncthreads();
+            for (int k = 0; k < TR * 64 / 256; ++k) {
+                const int idx = tid + 256 * k;        // 64 rows x 64 column quads
+                const int rl = idx >> 6, cq = idx & 63;
+                const int j0 = tw * 256 + 4 * cq;
+                if (j0 >= g.N) continue;
+                const int4 q = *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]);
+                const int32_t P[4] = {q.x, q.y, q.z, q.w};
+                mdecode4<BIP>(P, tp * 256 + TR * h + rl, j0, min(4, g.N - j0), b, g, lay, ws);
+            }
+        }
+    }
+}
+
+// sums the partial counts of every part of the split tiles F.. and decodes (eight blocks
+// per tile, 32 rows each; thread = row x four adjacent columns)
+template <bool BIP>
+__global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, uint8_t *ws) {
+    constexpr int NK = 32 * 64 / 256;
+    const int NTW = lay.NT / 2;
+    const int tile = g.F + (blockIdx.x >> 3), part8 = blockIdx.x & 7;
+    const int tw = tile % NTW;
+    const int tb = tile / NTW;
+    const int b = tb % g.batch, tp = tb / g.batch;
+    const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part) +
+                                                      (size_t)(tile - g.F) * g.S * 256 * 256) +
+                       (size_t)part8 * 32 * 64 + threadIdx.x;
+    int4 sum[NK];
+#pragma unroll
+    for (int k = 0; k < NK; ++k) sum[k] = make_int4(0, 0, 0, 0);
+    for (int s = 0; s < g.S; ++s) {
+        const int4 *src = base + (size_t)s * 256 * 64;
+        int4 q[NK];
+#pragma unroll
+        for (int k = 0; k < NK; ++k) q[k] = src[256 * k];
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+            sum[k].x += q[k].x;
+            sum[k].y += q[k].y;
+            sum[k].z += q[k].z;
+            sum[k].w += q[k].w;
+        }
+    }
+    const int32_t *perm = ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_perm);
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+        const int idx = threadIdx.x + 256 * k;
+        const int rl = part8 * 32 + (idx >> 6), cq = idx & 63;
+        const int j0 = tw * 256 + 4 * cq;
+        if (j0 >= g.N || perm[tp * 256 + rl] < 0) continue;
+        const int32_t P[4] = {sum[k].x, sum[k].y, sum[k].z, sum[k].w};
+        mdecode4<BIP>(P, tp * 256 + rl, j0, min(4, g.N - j0), b, g, lay, ws);
+    }
+}
+
+template <bool BIP>
+static hipError_t launch_qgemm(const MGemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
+    const unsigned tiles = (unsigned)(g.batch * (lay.MT / 2) * (lay.NT / 2));
+    const unsigned tail = tiles - (unsigned)g.F;
+    hipLaunchKernelGGL((k_qgemm<BIP>), dim3((unsigned)g.F + tail * (unsigned)g.S), dim3(256), 0, st, g,
+                       lay, ws);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || tail == 0) return e;
+    hipLaunchKernelGGL((k_qgemm_reduce<BIP>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
+    return hipGetLastError();
+}
+
 template <bool BIP>
 static hipError_t launch_mgemm_pol(const MGemmArgs &g, const Layout &lay, uint8_t *ws,
                                    hipStream_t st) {
+    if (lay.mbm == 256) return launch_qgemm<BIP>(g, lay, ws, st);
     if (lay.mbn == 256) return launch_mgemm_tile<BIP, 256>(g, lay, ws, st);
     return launch_mgemm_tile<BIP, 128>(g, lay, ws, st);
 }
@@ -603,6 +897,7 @@ hipError_t launch_mgemm(const sc_gemm_desc &d, const Layout &lay, const float *s
     g.nbB = lay.nbB;
     g.batch = d.batch;
     g.S = lay.S;
+    g.F = lay.F;
     g.sA = sA;
     g.sB = sB;
     g.strideSA = d.strideSA;

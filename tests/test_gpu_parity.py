@@ -165,6 +165,21 @@ def test_deterministic_repeat_and_engines_agree(dev):
     assert np.array_equal(c1, c3) and np.array_equal(o1.view(np.uint32), o3.view(np.uint32))
 
 
+@pytest.mark.parametrize("name", ["vitb16_fc1_L128", "vitb16_fc1_mp64", "ditxl2_proj_mlp_group96"])
+def test_engines_agree_full_size(dev, name):
+    # Every output of the full-size layers: the MFMA engine (256 x 256 tiles, whole tiles
+    # plus a split tail at uniform L, every tile split when the lengths vary) against the
+    # VALU engine, bit for bit.  Each engine is pinned to the oracle by the tests above.
+    w = W.WORKLOADS[name]()
+    for g in w.gemms:
+        _note("engines agree %s/%s" % (name, g.name))
+        o_m, c_m = _run(g, dev, engine=2)
+        o_v, c_v = _run(g, dev, engine=1)
+        bad = np.argwhere(c_m != c_v)
+        assert bad.size == 0, "%s/%s: %d count mismatches, first at %s" % (name, g.name, len(bad), bad[0])
+        assert np.array_equal(o_m.view(np.uint32), o_v.view(np.uint32)), name + ": decoded floats differ"
+
+
 # --------------------------------------------------------------------------
 # full-size workloads: sampled rows x columns against the oracle
 # --------------------------------------------------------------------------
