@@ -597,7 +597,8 @@ static hipError_t launch_mgemm_tile(const MGemmArgs &g, const Layout &lay, uint8
 // of LDS for 16 MFMAs, two thirds of what the 128-row tile needs per product.  A stage
 // is QSTAGE slots (two k-steps) in one of three LDS buffers: stage st computes from
 // buffer st % 3 while stage st + 2 is written into the third buffer, so the first
-// fragments of stage st + 1 can be read before the barrier that ends stage st.
+// fragments of stage st + 1 can be read before the barrier that ends stage st; three
+// register sets carry the global loads two stages ahead.
 // ----------------------------------------------------------------------------
 constexpr int QSTAGE = 4;                     // slots per stage
 constexpr int QKS = QSTAGE / 2;               // MFMA k-steps per stage
@@ -612,15 +613,23 @@ struct QFrags {
 };
 
 // Thread tid loads row tid % 128 of A tile tid / 128 of the pair (and the same of B) for
-// each slot of the stage starting at slot ks.  A short last stage re-reads its last slot
-// (never used), so every load is in bounds.
-__device__ __forceinline__ void q_load(const u4 *pa, const u4 *pb, int64_t ks, int64_t k1, QRegs &r) {
+// each slot of the stage starting at slot ks, as buffer loads: one descriptor per wave
+// spanning exactly its plane tile (a load past it would read zero), the slot as a scalar
+// offset and the row as the one vector offset, so the loads need no 64-bit address
+// arithmetic.  A short last stage re-reads its last slot (never used), so every load is in
+// bounds.
+struct QSrc {
+    __amdgpu_buffer_rsrc_t a, b;   // this wave's A and B plane tiles
+    int voff;                      // byte offset of the thread's row within a slot
+};
+__device__ __forceinline__ void q_load(const QSrc &q, int64_t ks, int64_t k1, QRegs &r) {
     const int last = (int)min((int64_t)QSTAGE, k1 - ks) - 1;
-    const u4 *a = pa + ks * BM, *b = pb + ks * BN;
 #pragma unroll
-    for (int k = 0; k < QSTAGE; ++k) r.a[k] = a[min(k, last) * BM];
+    for (int k = 0; k < QSTAGE; ++k)
+        r.a[k] = __builtin_amdgcn_raw_buffer_load_b128(q.a, q.voff, (int)(ks + min(k, last)) * (BM * 16), 0);
 #pragma unroll
-    for (int k = 0; k < QSTAGE; ++k) r.b[k] = b[min(k, last) * BN];
+    for (int k = 0; k < QSTAGE; ++k)
+        r.b[k] = __builtin_amdgcn_raw_buffer_load_b128(q.b, q.voff, (int)(ks + min(k, last)) * (BN * 16), 0);
 }
 
 __device__ __forceinline__ void q_store(u4 *buf, int tid, const QRegs &r) {
@@ -649,17 +658,21 @@ __device__ __forceinline__ void q_mma(v16f (&acc)[4][4], const QFrags &f) {
                                                                         acc[i][c], 4, 4, 0, 127, 0, 127);
 }
 
-// Stage st.  On entry buffer cb = st % 3 holds stage st and the next buffer stage st + 1
-// (both visible), fragment set 0 holds the first k-step of stage st, register set 1 - PR
-// stage st + 2 and set PR is free.  The stage loads stage st + 3 into set PR and writes
-// set 1 - PR into the third buffer.  A FULL stage (both k-steps present: one branch-free
-// region) interleaves its memory instructions one per MFMA: with one wave per SIMD the
-// wave issues in order, and a burst of LDS or global instructions would hold back the
-// next MFMA (measured: 0.83 against 1.20 ms for the 6304 x 768 x 3072 layer at L = 128).
-template <int PR, bool FULL>
-__device__ __forceinline__ void q_stage(int st, int nst, int64_t k0, int64_t k1, int cb, const u4 *pa,
-                                        const u4 *pb, u4 *smem, int tid, int grp, int wr, int wc,
-                                        int i32, v16f (&acc)[4][4], QFrags (&f)[2], QRegs (&r)[2]) {
+// Stage st, with CB = st % 3 the LDS buffer it computes from.  On entry the next buffer
+// holds stage st + 1 (visible), fragment set 0 the first k-step of stage st, and the
+// three register sets stages st + 2 (set (CB + 2) % 3, loaded two stages ago), st + 3
+// (set CB, in flight) and nothing (set (CB + 1) % 3).  The stage loads stage st + 4 into
+// the free set and writes stage st + 2 into the third buffer, so every load has two
+// stages to arrive.  A FULL stage (both k-steps present: one branch-free region)
+// interleaves its memory instructions one per MFMA: with one wave per SIMD the wave issues
+// in order, and a burst of LDS or global instructions would hold back the next MFMA
+// (measured on the 6304 x 768 x 3072 layer at L = 128: 1.20 ms unordered, 0.83 with one
+// instruction per MFMA, 0.77 with the global loads spread over 16 MFMAs).
+template <int CB, bool FULL>
+__device__ __forceinline__ void q_stage(int st, int nst, int64_t k0, int64_t k1, const QSrc &q,
+                                        u4 *smem, int tid, int grp, int wr, int wc,
+                                        int i32, v16f (&acc)[4][4], QFrags (&f)[2], QRegs (&r)[3]) {
+    constexpr int RL = (CB + 1) % 3, RW = (CB + 2) % 3, cb = CB;
     static_assert(QKS == 2, "the interleave below is written for two k-steps per stage");
     const int64_t klast = k0 + (int64_t)(nst - 1) * QSTAGE;
     const int64_t ks = k0 + (int64_t)st * QSTAGE;
@@ -669,14 +682,14 @@ __device__ __forceinline__ void q_stage(int st, int nst, int64_t k0, int64_t k1,
     const u4 *nbuf = smem + nb * QBUF;
     if (FULL) {
         q_frags(buf, 1, grp, wr, wc, i32, f[1]);
-        q_load(pa, pb, min(ks + 3 * QSTAGE, klast), k1, r[PR]);
+        q_load(q, min(ks + 4 * QSTAGE, klast), k1, r[RL]);
         q_mma(acc, f[0]);
-        q_store(wbuf, tid, r[1 - PR]);
+        q_store(wbuf, tid, r[RW]);
         q_frags(nbuf, 0, grp, wr, wc, i32, f[0]);
         q_mma(acc, f[1]);
-        // issue order: k-step 0 with the reads of k-step 1's fragments, then the global
-        // loads; k-step 1 with the LDS writes, then the reads of the next stage's first
-        // fragments
+        // k-step 0: the reads of k-step 1's fragments, then global loads and LDS writes
+        // alternating over the next 16 MFMAs; k-step 1 ends with the reads of the next
+        // stage's first fragments
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
@@ -686,9 +699,6 @@ __device__ __forceinline__ void q_stage(int st, int nst, int64_t k0, int64_t k1,
         for (int k = 0; k < 8; ++k) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global load
-        }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // LDS write
         }
@@ -699,9 +709,9 @@ __device__ __forceinline__ void q_stage(int st, int nst, int64_t k0, int64_t k1,
         }
     } else {
         const int nk = (int)min((int64_t)QSTAGE, k1 - ks) / 2;
-        q_load(pa, pb, min(ks + 3 * QSTAGE, klast), k1, r[PR]);
+        q_load(q, min(ks + 4 * QSTAGE, klast), k1, r[RL]);
         q_frags(buf, 1, grp, wr, wc, i32, f[1]);
-        q_store(wbuf, tid, r[1 - PR]);
+        q_store(wbuf, tid, r[RW]);
         q_mma(acc, f[0]);
         q_frags(nbuf, 0, grp, wr, wc, i32, f[0]);
         if (nk > 1) q_mma(acc, f[1]);
@@ -735,13 +745,16 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
     const int Lloop = ws_ptr<int32_t>(wsa, lay.off_tileL)[2 * tp];
     const int64_t nsteps = (int64_t)(Lloop / MSTEP) * g.KQP / 2;
     const int64_t k0 = (int64_t)s * nsteps / S * 2, k1 = (int64_t)(s + 1) * nsteps / S * 2;
-    const int half = tid >> 7;
-    const u4 *pa = reinterpret_cast<const u4 *>(ws_ptr<uint32_t>(wsa, lay.off_Ap) +
-                                                ws_ptr<int64_t>(wsa, lay.off_tileOff)[2 * tp + half]) +
-                   (tid & (BM - 1));
+    const int half = wave_uniform(tid >> 7);
     const size_t btile = (size_t)(g.LBS / MSTEP) * g.KQP * BN;
-    const u4 *pb = reinterpret_cast<const u4 *>(ws_ptr<uint32_t>(wsbB, lay.off_Bp)) +
-                   (size_t)(2 * tw + half) * btile + (tid & (BN - 1));
+    QSrc q;
+    q.a = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint32_t *>(ws_ptr<uint32_t>(wsa, lay.off_Ap) + ws_ptr<int64_t>(wsa, lay.off_tileOff)[2 * tp + half]),
+        0, (int)((Lloop / MSTEP) * g.KQP * BM * 16), 0x00020000);
+    q.b = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<u4 *>(ws_ptr<uint32_t>(wsbB, lay.off_Bp)) + (size_t)(2 * tw + half) * btile, 0,
+        (int)(btile * 16), 0x00020000);
+    q.voff = (tid & (BM - 1)) * 16;
 
     v16f acc[4][4];
 #pragma unroll
@@ -749,35 +762,34 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[i][c] = v16f{};
 
-    QRegs r[2];
+    QRegs r[3];
     QFrags f[2];
     const int nst = (int)((k1 - k0 + QSTAGE - 1) / QSTAGE);
     if (nst > 0) {
         const int64_t klast = k0 + (int64_t)(nst - 1) * QSTAGE;
-        q_load(pa, pb, k0, k1, r[0]);
-        q_load(pa, pb, min(k0 + QSTAGE, klast), k1, r[1]);
+        q_load(q, k0, k1, r[0]);
+        q_load(q, min(k0 + QSTAGE, klast), k1, r[1]);
         q_store(smem, tid, r[0]);
         q_store(smem + QBUF, tid, r[1]);
-        q_load(pa, pb, min(k0 + 2 * QSTAGE, klast), k1, r[1]);
+        q_load(q, min(k0 + 2 * QSTAGE, klast), k1, r[2]);
+        q_load(q, min(k0 + 3 * QSTAGE, klast), k1, r[0]);
     }
     __syncthreads();
     if (nst > 0) q_frags(smem, 0, grp, wr, wc, i32, f[0]);
     // the first fragments complete before the loop, so that its first MFMAs need no wait
     __syncthreads();
-    // pairs of full stages (neither is the last one), then the last one or two stages:
-    // the loop body is branch-free and its back edge always carries the same loads
-    int st = 0, cb = 0;
-    for (; st + 2 < nst; st += 2) {
-        q_stage<0, true>(st, nst, k0, k1, cb, pa, pb, smem, tid, grp, wr, wc, i32, acc, f, r);
-        cb = cb == QNBUF - 1 ? 0 : cb + 1;
-        q_stage<1, true>(st + 1, nst, k0, k1, cb, pa, pb, smem, tid, grp, wr, wc, i32, acc, f, r);
-        cb = cb == QNBUF - 1 ? 0 : cb + 1;
+    // triples of full stages (none is the last one), so that buffers and register sets are
+    // fixed at compile time, then the last one to three stages: the loop body is
+    // branch-free and its back edge always carries the same loads
+    int st = 0;
+    for (; st + 3 < nst; st += 3) {
+        q_stage<0, true>(st, nst, k0, k1, q, smem, tid, grp, wr, wc, i32, acc, f, r);
+        q_stage<1, true>(st + 1, nst, k0, k1, q, smem, tid, grp, wr, wc, i32, acc, f, r);
+        q_stage<2, true>(st + 2, nst, k0, k1, q, smem, tid, grp, wr, wc, i32, acc, f, r);
     }
-    if (st < nst) {
-        q_stage<0, false>(st, nst, k0, k1, cb, pa, pb, smem, tid, grp, wr, wc, i32, acc, f, r);
-        cb = cb == QNBUF - 1 ? 0 : cb + 1;
-    }
-    if (st + 1 < nst) q_stage<1, false>(st + 1, nst, k0, k1, cb, pa, pb, smem, tid, grp, wr, wc, i32, acc, f, r);
+    if (st < nst) q_stage<0, false>(st, nst, k0, k1, q, smem, tid, grp, wr, wc, i32, acc, f, r);
+    if (st + 1 < nst) q_stage<1, false>(st + 1, nst, k0, k1, q, smem, tid, grp, wr, wc, i32, acc, f, r);
+    if (st + 2 < nst) q_stage<2, false>(st + 2, nst, k0, k1, q, smem, tid, grp, wr, wc, i32, acc, f, r);
 
     if (split) {
         // partial sums of this unit as int32 [256 rows][256 columns]
