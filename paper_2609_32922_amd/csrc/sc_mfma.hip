@@ -177,15 +177,23 @@ __global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
     u4 *planes = reinterpret_cast<u4 *>(ws_ptr<uint32_t>(wsb, a.off_planes) + off);
     const int m = tid & (BM - 1), h = tid >> 7;
     const bool store_row = rowok[m] != 0;
+    // the thread's 8 quads x 4 elements of row m, the same for every octet
+    uint32_t pks[8][4];
+#pragma unroll
+    for (int pr = 0; pr < 8; ++pr)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pks[pr][e] = prm[(4 * (2 * pr + h) + e) * PRM_STRIDE + m];
+    const int npr = min(8, (a.KQP - qg * 16 - h + 1) / 2);     // quads 2 pr + h below KQP
     for (int o = 0; o < no; ++o) {
         const int oa = o0 + o, c0 = oa * MSTEP;
+#pragma unroll
         for (int pr = 0; pr < 8; ++pr) {
             const int dq = 2 * pr + h, qd = qg * 16 + dq;
-            if (qd >= a.KQP) break;
+            if (pr >= npr) break;
             u4 v;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const uint32_t pk = prm[(4 * dq + e) * PRM_STRIDE + m];
+                const uint32_t pk = pks[pr][e];
                 uint32_t x;
                 if (CBSG) {
                     const int lo = (int)(pk & 511u), hi = (int)((pk >> 9) & 511u);
