@@ -38,6 +38,10 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.NT = (d.N + BN - 1) / BN;
     l.mbn = l.NT > 1 ? 2 * BN : BN;
     if (mfma) l.NT = (int)round_up(l.NT, l.mbn / BN);
+    // N <= 128 (one B tile): every A plane would be used once, so the GEMM generates the
+    // fragments itself (comparator streams; operand offsets must fit 31 bits)
+    l.fused = mfma && l.mbn == BN && d.rng == SC_RNG_LFSR32 &&
+              fused_extent(d.M, d.lda, d.K) < INT_MAX - 4 && fused_extent(d.N, d.ldb, d.K) < INT_MAX - 4;
     l.mbm = (mfma && l.MT > 1 && l.mbn == 2 * BN) ? 2 * BM : BM;
     if (l.mbm == 2 * BM) l.MT = (int)round_up(l.MT, 2);
     l.LBS = (int)round_up(d.L_max, LCH);
@@ -78,6 +82,7 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     // largest planes of one batch entry: every tile at L_max rounded up to its step
     if (!mul_ok((size_t)l.MT * (size_t)l.words_per_L, (size_t)round_up(d.L_max, l.tstep) * 4, &sz))
         return false;
+    if (l.fused) sz = 0;
     a = align256(a + sz);
     l.off_SA = a;
     if (signsA) a = align256(a + rowsA * (size_t)l.KB * 4);
@@ -92,6 +97,7 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     size_t bb = 0;
     l.off_Bp = bb;
     if (!mul_ok((size_t)l.NT * (size_t)l.words_per_L, (size_t)l.LBS * 4, &sz)) return false;
+    if (l.fused) sz = 0;
     (void)rowsB;
     bb = align256(bb + sz);
     l.off_SB = bb;
@@ -299,13 +305,16 @@ int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const in
     const bool mfma = lay.engine == SC_ENGINE_MFMA;
     if (!mfma && lay.mode == MODE_AND && (e = launch_marginals(d, lay, A, B, ws, st)) != hipSuccess)
         return SC_ERR_HIP;
-    e = mfma ? launch_mplanes(d, lay, A, B, ws, st) : launch_planes(d, lay, A, B, ws, st);
-    if (e != hipSuccess) return SC_ERR_HIP;
+    if (!lay.fused) {
+        e = mfma ? launch_mplanes(d, lay, A, B, ws, st) : launch_planes(d, lay, A, B, ws, st);
+        if (e != hipSuccess) return SC_ERR_HIP;
+    }
     if (d.prof_event_begin != nullptr &&
         hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_begin), st) != hipSuccess)
         return SC_ERR_HIP;
-    e = mfma ? launch_mgemm(d, lay, sA, sB, out, counts, ws, st)
-             : launch_gemm(d, lay, sA, sB, out, counts, ws, st);
+    e = lay.fused ? launch_fgemm(d, lay, A, B, sA, sB, out, counts, ws, st)
+                  : mfma ? launch_mgemm(d, lay, sA, sB, out, counts, ws, st)
+                         : launch_gemm(d, lay, sA, sB, out, counts, ws, st);
     if (e != hipSuccess) return SC_ERR_HIP;
     if (d.prof_event_end != nullptr &&
         hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_end), st) != hipSuccess)

@@ -92,6 +92,8 @@ struct Layout {
     int KQP;           // MFMA: element quads per octet, ceil(K/4) rounded up to 4
     int tstep;         // tile cycle counts are rounded up to this (LSTEP or MSTEP)
     int mbn;           // MFMA engine: columns of B per GEMM block (256, or 128 when N <= 128)
+    int fused;         // MFMA engine, N <= 128, comparator streams: the GEMM builds its fp4
+                       // fragments from the int8 operands (no planes in the workspace)
     int mbm;           // MFMA engine: rows of A per GEMM block: 256 (row tiles taken in pairs
                        // that run at the pair's longest length; MT even) when mbn = 256 and
                        // MT > 1, else 128
@@ -128,6 +130,14 @@ hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t
                           const int8_t *B, uint8_t *ws, hipStream_t st);
 hipError_t launch_mgemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
                         float *out, int32_t *counts, uint8_t *ws, hipStream_t st);
+hipError_t launch_fgemm(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
+                        const float *sA, const float *sB, float *out, int32_t *counts, uint8_t *ws,
+                        hipStream_t st);
+
+// bytes of one batch entry of an operand from its first byte: (rows - 1) * ld + K
+__host__ __device__ inline int64_t fused_extent(int rows, int64_t ld, int K) {
+    return rows > 0 && K > 0 ? (int64_t)(rows - 1) * ld + K : 0;
+}
 
 // thresholds and ladder of the per-row length policy, passed by value to the kernel
 struct MpParams {

@@ -599,6 +599,270 @@ static hipError_t launch_mgemm_tile(const MGemmArgs &g, const Layout &lay, uint8
 }
 
 // ----------------------------------------------------------------------------
+// Fused generation for N <= 128 (one B tile) with comparator streams: every A plane
+// would be written once and read once, so the block builds its fp4 fragments in LDS
+// straight from the int8 operands instead.  Block = 128 rows of A x 128 columns of B,
+// four waves of 64 x 64 (2 x 2 MFMA blocks); a stage is 4 slots = 4 element quads of one
+// octet, so one 8-cycle lookup table per operand serves the whole stage.  Thread tid < 128
+// builds row tid of A, thread 128 + j builds row j of B: one 16-byte window of its int8
+// row per stage (two aligned buffer loads, so rows need no alignment), 16 table lookups,
+// the row-length mask and the sign, four 16-byte LDS stores.
+// ----------------------------------------------------------------------------
+constexpr int FWB = 128;                         // columns of B per fused block
+constexpr int FBUF = MSTAGE * (BM + FWB);        // u4 per LDS stage buffer
+
+struct FArgs {
+    const int8_t *A, *B;
+    int64_t lda, ldb, strideA, strideB;
+    uint32_t bytesA, bytesB;    // extent of one batch entry of A / B from its first byte,
+                                // rounded up to a whole dword
+    int nbB, L_max;
+};
+
+// Stages per unit and the octet / first quad of a stage: stage index st of the tile covers
+// slots 4 st .. 4 st + 3, all in octet (4 st) / KQP (KQP is a multiple of 4).
+__device__ __forceinline__ void f_stage_pos(int st, int KQP, int &o, int &dq0) {
+    const int ks = 4 * st;
+    o = ks / KQP;
+    dq0 = ks - o * KQP;
+}
+
+// the 20-byte aligned window holding bytes [off, off + 16) of the operand
+struct FWin {
+    u4 lo;
+    uint32_t hi;
+};
+__device__ __forceinline__ void f_load(__amdgpu_buffer_rsrc_t rs, int off, FWin &w) {
+    const int a0 = off & ~3;
+    w.lo = __builtin_amdgcn_raw_buffer_load_b128(rs, a0, 0, 0);
+    w.hi = __builtin_amdgcn_raw_buffer_load_b32(rs, a0 + 16, 0, 0);
+}
+
+// Table of octet o for both operands, indexed by the int8 value itself (as a byte):
+// lut[side * 256 + byte] = the 8 nibbles of cycles 8o .. 8o + 7 (cycle c at bits 4c..4c+3),
+// sign included (unipolar), so generating a slot row needs no boundary arithmetic
+constexpr int FLUT = 512;
+template <int POL>
+__device__ __forceinline__ void f_build_lut(uint32_t *lut, const uint32_t *rA, const uint32_t *rB, int o,
+                                            int tid) {
+    const uint32_t zero_nib = POL == SC_BIPOLAR_XNOR ? NIB_NEG : 0u;
+    for (int e = tid; e < FLUT; e += 256) {
+        const int side = e >> 8;
+        const int q = (int)(int8_t)(uint8_t)(e & 255);
+        const uint32_t *r = (side ? rB : rA) + 8 * o;
+        const uint32_t beta = (uint32_t)(POL == SC_BIPOLAR_XNOR ? beta_bipolar(q) : beta_unipolar(q));
+        uint32_t x = 0;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) x |= (r[c] < beta ? NIB_POS : zero_nib) << (4 * c);
+        lut[e] = (POL == SC_UNIPOLAR_AND_SM && q < 0) ? negate_nibbles(x) : x;
+    }
+}
+
+// the four slot rows of one stage for this thread's row, written into LDS at dst
+// (slot k at dst + k * dstride); lut points at this operand's 256 entries
+__device__ __forceinline__ void f_gen(const FWin &win, int sh, int elem0, int K, int Lr, bool rowok,
+                                      int o, const uint32_t *lut, u4 *dst, int dstride) {
+    // bytes [sh, sh + 16) of the window, four per dword
+    uint32_t wd[4];
+    const uint32_t v[5] = {win.lo[0], win.lo[1], win.lo[2], win.lo[3], win.hi};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) wd[k] = __builtin_amdgcn_alignbyte(v[k + 1], v[k], (uint32_t)sh);
+    // cycles at or beyond the row's length and padding rows give zero nibbles
+    const int rem = Lr - MSTEP * o;
+    const uint32_t lmask =
+        (!rowok || rem <= 0) ? 0u : (rem >= 8 ? 0xFFFFFFFFu : (1u << (4 * rem)) - 1u);
+    u4 out[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) out[k][e] = lut[(wd[k] >> (8 * e)) & 255u] & lmask;
+    // elements at or beyond K (only in a row's last quads; the same for every thread)
+    if (elem0 + 16 > K) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (elem0 + 4 * k + e >= K) out[k][e] = 0u;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) dst[k * dstride] = out[k];
+}
+
+__device__ __forceinline__ int f_octet(int st, int KQP) { return (4 * st) / KQP; }
+
+// window load of (unit-relative) stage st, clamped to the unit's last stage
+__device__ __forceinline__ void f_load_stage(__amdgpu_buffer_rsrc_t rs, int rowoff, int st0, int st, int nst,
+                                             int KQP, FWin &wv) {
+    int o, dq0;
+    f_stage_pos(st0 + min(st, nst - 1), KQP, o, dq0);
+    f_load(rs, rowoff + 4 * dq0, wv);
+}
+
+struct FRow {
+    int rowoff, Lr, lside;
+    bool rowok;
+    __amdgpu_buffer_rsrc_t rs;
+    u4 *gdst0;
+};
+
+template <int POL>
+__device__ __forceinline__ void f_gen_stage(const FRow &fr, const FWin &wv, int st0, int st, int KQP, int K,
+                                            const uint32_t (*lut)[FLUT], u4 *dst) {
+    int o, dq0;
+    f_stage_pos(st0 + st, KQP, o, dq0);
+    f_gen(wv, (fr.rowoff + 4 * dq0) & 3, 4 * dq0, K, fr.Lr, fr.rowok, o, &lut[o & 1][fr.lside], dst, BM);
+}
+
+// Stage st (parity P): MFMAs of stage st from buffer P, generation of stage st + 1 into
+// buffer 1 - P from window 1 - P, which then loads stage st + 3; the table of stage st + 2
+// is built first when that stage opens an octet (its parity differs from the table stage
+// st + 1 uses, and the stages that last used it are finished).
+template <int POL, int P>
+__device__ __forceinline__ void f_stage(int st, int st0, int nst, const MGemmArgs &g, const FRow &fr,
+                                        const uint32_t *rA, const uint32_t *rB, uint32_t (*lut)[FLUT],
+                                        u4 *smem, int tid, int grp, int wr, int wc, int i32,
+                                        v16f (&acc)[2][2], Frags<FWB> (&fg)[2], FWin (&win)[2]) {
+    if (st + 2 < nst) {
+        const int o2 = f_octet(st0 + st + 2, g.KQP);
+        if (o2 != f_octet(st0 + st + 1, g.KQP)) f_build_lut<POL>(lut[o2 & 1], rA, rB, o2, tid);
+    }
+    const u4 *buf = smem + P * FBUF;
+    read_frags<FWB>(buf, 1, grp, wr, wc, i32, fg[1]);
+    mma<FWB>(acc, fg[0]);
+    if (st + 1 < nst) {
+        f_gen_stage<POL>(fr, win[1 - P], st0, st + 1, g.KQP, g.K, lut, fr.gdst0 + (1 - P) * FBUF);
+        f_load_stage(fr.rs, fr.rowoff, st0, st + 3, nst, g.KQP, win[1 - P]);
+    }
+    mma<FWB>(acc, fg[1]);
+    __syncthreads();
+    if (st + 1 < nst) read_frags<FWB>(smem + (1 - P) * FBUF, 0, grp, wr, wc, i32, fg[0]);
+}
+
+template <int POL, bool SPLIT>
+__global__ __launch_bounds__(256, 2) void k_fgemm(MGemmArgs g, FArgs f, Layout lay, uint8_t *ws) {
+    constexpr bool BIP = POL == SC_BIPOLAR_XNOR;
+    __shared__ u4 smem[2 * FBUF];
+    __shared__ uint32_t lut[2][FLUT];            // [octet parity][side * 256 + byte]
+    const int u = blockIdx.x;
+    const int s = u % g.S;
+    const int tile = u / g.S;                     // one B tile: tile = tm * batch + b
+    const int b = tile % g.batch, tm = tile / g.batch;
+    const int bB = f.nbB == 1 ? 0 : b;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int grp = lane >> 5, i32 = lane & 31;
+    const int wr = (w >> 1) * 64, wc = (w & 1) * 64;
+    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
+    const int Lloop = ws_ptr<int32_t>(wsa, lay.off_tileL)[tm];
+    const int nstg = (Lloop / MSTEP) * (g.KQP / MSTAGE);
+    const int st0 = (int)((int64_t)s * nstg / g.S), nst = (int)((int64_t)(s + 1) * nstg / g.S) - st0;
+    const uint32_t *rA = ws_ptr<uint32_t>(ws, lay.off_rA), *rB = ws_ptr<uint32_t>(ws, lay.off_rB);
+
+    // this thread's generation row: waves 0-1 rows of A (sorted order), waves 2-3 rows of B
+    const bool isA = wave_uniform(tid >> 7) == 0;
+    const int r = tid & (BM - 1);
+    FRow fr;
+    int row;
+    if (isA) {
+        const int p = tm * BM + r;
+        row = ws_ptr<int32_t>(wsa, lay.off_perm)[p];
+        fr.Lr = row >= 0 ? ws_ptr<int32_t>(wsa, lay.off_Ls)[p] : 0;
+    } else {
+        row = r < g.N ? r : -1;
+        fr.Lr = f.L_max;
+    }
+    fr.rowok = row >= 0;
+    const int8_t *base = isA ? f.A + (size_t)b * f.strideA : f.B + (size_t)bB * f.strideB;
+    fr.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t *>(base), 0, (int)(isA ? f.bytesA : f.bytesB),
+                                              0x00020000);
+    fr.rowoff = fr.rowok ? (int)((int64_t)row * (isA ? f.lda : f.ldb)) : 0;
+    fr.lside = isA ? 0 : 256;
+    fr.gdst0 = smem + (isA ? 0 : MSTAGE * BM) + r;
+
+    v16f acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) acc[i][c] = v16f{};
+
+    FWin win[2];
+    Frags<FWB> fg[2];
+    if (nst > 0) {
+        f_load_stage(fr.rs, fr.rowoff, st0, 0, nst, g.KQP, win[0]);
+        f_load_stage(fr.rs, fr.rowoff, st0, 1, nst, g.KQP, win[1]);
+        const int o0 = f_octet(st0, g.KQP), o1 = f_octet(st0 + min(1, nst - 1), g.KQP);
+        f_build_lut<POL>(lut[o0 & 1], rA, rB, o0, tid);
+        if (o1 != o0) f_build_lut<POL>(lut[o1 & 1], rA, rB, o1, tid);
+        __syncthreads();
+        f_gen_stage<POL>(fr, win[0], st0, 0, g.KQP, g.K, lut, fr.gdst0);
+        f_load_stage(fr.rs, fr.rowoff, st0, 2, nst, g.KQP, win[0]);
+    }
+    __syncthreads();
+    if (nst > 0) read_frags<FWB>(smem, 0, grp, wr, wc, i32, fg[0]);
+    for (int st = 0; st < nst; st += 2) {
+        f_stage<POL, 0>(st, st0, nst, g, fr, rA, rB, lut, smem, tid, grp, wr, wc, i32, acc, fg, win);
+        if (st + 1 < nst)
+            f_stage<POL, 1>(st + 1, st0, nst, g, fr, rA, rB, lut, smem, tid, grp, wr, wc, i32, acc, fg, win);
+    }
+
+    if (SPLIT) {
+        // partial sums of this split as int32 [tile][split][128][128], as the 128-row GEMM
+        int32_t *part = ws_ptr<int32_t>(ws, lay.off_part) + ((size_t)tile * g.S + s) * BM * FWB;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    part[(wr + 32 * i + 8 * (e >> 2) + 4 * grp + (e & 3)) * FWB + wc + 32 * c + i32] =
+                        (int32_t)acc[i][c][e];
+    } else {
+        constexpr int TS = FWB + 4, TR = 32;
+        static_assert(TR * TS * 4 <= 2 * FBUF * 16, "the epilogue transpose must fit the LDS buffers");
+        int32_t *T = reinterpret_cast<int32_t *>(smem);
+        for (int h = 0; h < BM / TR; ++h) {
+            __syncthreads();
+            if (wr == 64 * (h >> 1)) {
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    if (i != (h & 1)) continue;
+#pragma unroll
+                    for (int c = 0; c < 2; ++c)
+#pragma unroll
+                        for (int e = 0; e < 16; ++e)
+                            T[(8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] = (int32_t)acc[i][c][e];
+                }
+            }
+            __syncthreads();
+            for (int k = 0; k < TR * (FWB / 4) / 256; ++k) {
+                const int idx = tid + 256 * k;        // 32 rows x 32 column quads
+                const int rl = idx / (FWB / 4), cq = idx % (FWB / 4);
+                const int j0 = 4 * cq;
+                if (j0 >= g.N) continue;
+                const int4 v = *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]);
+                const int32_t P[4] = {v.x, v.y, v.z, v.w};
+                mdecode4<BIP>(P, tm * BM + TR * h + rl, j0, min(4, g.N - j0), b, g, lay, ws);
+            }
+        }
+    }
+}
+
+template <int POL>
+static hipError_t launch_fgemm_pol(const MGemmArgs &g, const FArgs &f, const Layout &lay, uint8_t *ws,
+                                   hipStream_t st) {
+    const unsigned tiles = (unsigned)(g.batch * lay.MT);
+    if (g.S == 1) {
+        hipLaunchKernelGGL((k_fgemm<POL, false>), dim3(tiles), dim3(256), 0, st, g, f, lay, ws);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL((k_fgemm<POL, true>), dim3(tiles * (unsigned)g.S), dim3(256), 0, st, g, f, lay, ws);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_mgemm_reduce<POL == SC_BIPOLAR_XNOR, FWB>), dim3(tiles * 4u), dim3(256), 0, st, g,
+                       lay, ws);
+    return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
 // 256 x 256 GEMM tile: a pair of A row tiles (equal cycle counts) x a pair of B tiles,
 // one 256-thread block per CU.  Wave w owns rows 128 (w / 2).., columns 128 (w % 2).. as
 // 4 x 4 32x32 MFMA blocks (its 256 accumulator registers); per MFMA k-step it reads 8 KB
@@ -904,6 +1168,50 @@ static hipError_t launch_mgemm_pol(const MGemmArgs &g, const Layout &lay, uint8_
     if (lay.mbm == 256) return launch_qgemm<BIP>(g, lay, ws, st);
     if (lay.mbn == 256) return launch_mgemm_tile<BIP, 256>(g, lay, ws, st);
     return launch_mgemm_tile<BIP, 128>(g, lay, ws, st);
+}
+
+static MGemmArgs make_gemm_args(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
+                                float *out, int32_t *counts) {
+    MGemmArgs g{};
+    g.M = d.M;
+    g.N = d.N;
+    g.K = d.K;
+    g.KQP = lay.KQP;
+    g.LBS = lay.LBS;
+    g.nbB = lay.nbB;
+    g.batch = d.batch;
+    g.S = lay.S;
+    g.F = lay.F;
+    g.sA = sA;
+    g.sB = sB;
+    g.strideSA = d.strideSA;
+    g.strideSB = d.strideSB;
+    g.strideO = d.strideO;
+    g.ldo = d.ldo;
+    g.out = out;
+    g.counts = counts;
+    return g;
+}
+
+hipError_t launch_fgemm(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
+                        const float *sA, const float *sB, float *out, int32_t *counts, uint8_t *ws,
+                        hipStream_t st) {
+    const MGemmArgs g = make_gemm_args(d, lay, sA, sB, out, counts);
+    FArgs f{};
+    f.A = A;
+    f.B = B;
+    f.lda = d.lda;
+    f.ldb = d.ldb;
+    f.strideA = d.strideA;
+    f.strideB = d.strideB;
+    // buffer loads check whole dwords against the extent, so it is rounded up to the dword
+    // that holds the last byte (same page; the bytes past it are masked as elements >= K)
+    f.bytesA = (uint32_t)round_up(fused_extent(d.M, d.lda, d.K), 4);
+    f.bytesB = (uint32_t)round_up(fused_extent(d.N, d.ldb, d.K), 4);
+    f.nbB = lay.nbB;
+    f.L_max = d.L_max;
+    if (d.polarity == SC_BIPOLAR_XNOR) return launch_fgemm_pol<SC_BIPOLAR_XNOR>(g, f, lay, ws, st);
+    return launch_fgemm_pol<SC_UNIPOLAR_AND_SM>(g, f, lay, ws, st);
 }
 
 hipError_t launch_mgemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,

@@ -105,6 +105,13 @@ FUZZ = [
     (2, 140, 131, 65, 48, 0, 1, True, 19),
     (1, 64, 64, 1000, 24, 0, 1, False, 21),
     (1, 200, 150, 7, 512, 400, 0, False, 23),
+    # N <= 128: the MFMA engine builds its fp4 fragments from the int8 rows (unaligned rows,
+    # broadcast B, a split k-range with few tiles, the octet table changing every stage)
+    (1, 300, 100, 33, 70, 0, 0, False, 25),
+    (2, 257, 128, 65, 300, 10, 1, True, 27),
+    (3, 70, 64, 130, 64, 0, 0, False, 29),
+    (1, 140, 1, 5, 4096, 0, 0, False, 31),
+    (2, 129, 127, 12, 200, 0, 1, False, 33),
 ]
 
 
@@ -163,6 +170,22 @@ def test_deterministic_repeat_and_engines_agree(dev):
     # the two engines give bit-identical counts and decoded floats
     o3, c3 = _run(g, dev, engine=1)
     assert np.array_equal(c1, c3) and np.array_equal(o1.view(np.uint32), o3.view(np.uint32))
+
+
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
+@pytest.mark.parametrize("polarity", [0, 1])
+def test_longest_streams(dev, oracle_mod, polarity, engine):
+    # L_max at the library's limit (4096 cycles), rows at exactly L_max and at 0, on a
+    # ragged 300 x 270 shape (an odd count of 128-row tiles, so the 256-row MFMA blocks
+    # take a padded pair); every output against the oracle
+    import paper_2609_32922_amd as scg
+    rng = np.random.default_rng(201 + polarity)
+    g = W.random_gemm(rng, 1, 300, 270, 100, scg.SC_L_MAX_LIMIT, polarity, 201 + polarity)
+    g.L[0, :7] = scg.SC_L_MAX_LIMIT
+    g.L[0, 7:11] = 0
+    _note("longest streams polarity %d engine %d" % (polarity, engine))
+    out, cnt = _run(g, dev, engine=engine)
+    _compare(g, 0, np.arange(300), np.arange(270), out, cnt, oracle_mod, "Lmax%d pol%d" % (g.L_max, polarity))
 
 
 @pytest.mark.parametrize("name", ["vitb16_fc1_L128", "vitb16_fc1_mp64", "ditxl2_proj_mlp_group96"])
