@@ -17,17 +17,21 @@
 //   k_mplanes     nibble planes of A (sorted rows, per-row lengths) or B, one block per
 //                 128-row tile x 64 cycles x 64 elements; element parameters and an
 //                 8-cycle lookup table in LDS, 16-byte stores, 1 KB per wave
+//   k_fgemm       N <= 128 with comparator streams: 128x128 tile, the fp4 fragments of
+//                 both operands built in LDS from the int8 rows (an 8-cycle table per
+//                 octet indexed by the int8 byte), so no planes are written or read
 //   k_qgemm       256x256 output tile per 256-thread block, one block per CU, 128x128
 //                 per wave as 4x4 32x32 MFMA blocks, three LDS buffers of 4 slots (96 KB),
 //                 memory instructions interleaved one per MFMA; taken when N > 128 and
 //                 M > 128.  Whole tiles in full rounds, the tiles of a last partial round
 //                 (or every tile, when row lengths vary) split along k.
 //   k_qgemm_reduce sums the partial counts of its split tiles and decodes
-//   k_mgemm       128x256 output tile per 256-thread block (128x128 and 64x64 when N <=
-//                 128), 64x128 per wave as 2x4 32x32 MFMA blocks, 4 slots (2 MFMA k-steps
-//                 of 64) per LDS stage, two LDS buffers (48 KB: two blocks per CU).  The
-//                 32x32x64 form keeps the matrix cores fed where the 16x16x128 form loses
-//                 several cycles per instruction to issue.
+//   k_mgemm       the rest (M <= 128, or N <= 128 with C-BSG streams): 128x256 output
+//                 tile per 256-thread block (128x128 and 64x64 when N <= 128), 64x128 per
+//                 wave as 2x4 32x32 MFMA blocks, 4 slots (2 MFMA k-steps of 64) per LDS
+//                 stage, two LDS buffers (48 KB: two blocks per CU).  The 32x32x64 form
+//                 keeps the matrix cores fed where the 16x16x128 form loses several cycles
+//                 per instruction to issue.
 //   k_mgemm_reduce sums the partial counts of split tiles and decodes
 #include "sc_internal.h"
 
