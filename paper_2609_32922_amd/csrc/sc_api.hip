@@ -120,32 +120,36 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.S = 1;
     l.F = 0;
     if (quad && tiles > 0) {
-        // 256 x 256 tiles, one block per CU, taking whole tiles or parts of tiles.  The
-        // estimated makespan of a division is the larger of its rounds of average units and
-        // its longest unit (a tile pair runs as long as its longest row: up to L_max, while
-        // the mean follows L_hint), plus writing and summing the partial sums of the split
-        // tiles.  Candidates: every tile split s ways (F = 0), or whole tiles in full rounds
-        // with the tiles of a last partial round split to fill one round.
-        const double per_L = (double)l.mbm * l.mbn * 4.0 * l.KQP / MFMA_QUAD_RATE;
-        const double avgT = per_L * Lmean, maxT = per_L * d.L_max;
-        const auto red = [&](int64_t split_tiles, int s) {
-            return s > 1 ? (double)split_tiles * (2 * s) * tile_bytes / 3e12 + 5e-6 : 0.0;
-        };
+        // 256 x 256 tiles, one block per CU, taking whole tiles or parts of tiles
+        // (quad_split_time).  Candidates: every tile split s ways (F = 0), or whole tiles in
+        // full rounds with the tiles of a last partial round split to fill one round.  Split
+        // counts are powers of two: units are dealt to the eight XCDs round-robin, so each
+        // XCD then holds units of one k-range, whose operand slots its blocks read
+        // together from its L2 (three-way splits measured slower than four-way).  With
+        // F = 0 the GEMM kernels may lower s again with the actual longest tile pair
+        // (measured: 6304 x 768 x 3072 with L in [16, 256], mean 64, longest 172: the GEMM
+        // takes 0.49 ms split two ways against 0.61 ms three ways).
+        l.q_perL = (double)l.mbm * l.mbn * 4.0 * l.KQP / MFMA_QUAD_RATE;
+        l.q_Lmean = Lmean;
+        l.q_one = Lmean >= d.L_max;
+        const double avgT = l.q_perL * Lmean, maxT = l.q_perL * d.L_max;
         double best = 0.0;
-        for (int s = 1; s <= MAX_SPLIT && s <= (kunits > 0 ? kunits : 1); ++s) {
-            const int64_t units = tiles * s;
-            const double est = fmax((double)((units + CUS - 1) / CUS) * avgT / s, maxT / s) + red(tiles, s);
+        for (int s = 1; s <= MAX_SPLIT && s <= (kunits > 0 ? kunits : 1); s *= 2) {
+            const double est = quad_split_time(tiles, s, l.q_perL, Lmean, d.L_max, l.q_one != 0);
             if (s == 1 || est < best * 0.97) {
                 best = est;
                 l.S = s;
             }
         }
+        // (the tail's split fills the last round as closely as it can: its units are few
+        // and short, so balance counts for more there than a shared k-range per XCD)
         const int64_t R = tiles % CUS;
         int s2 = R > 0 ? (int)(CUS / R) : 1;
         s2 = s2 > MAX_SPLIT ? MAX_SPLIT : s2;
         if (s2 > kunits) s2 = kunits;
         if (tiles >= CUS && R > 0 && s2 > 1) {
-            const double est = fmax((double)(tiles / CUS) * avgT + avgT / s2, maxT) + red(R, s2);
+            const double red = (double)R * (2 * s2) * tile_bytes / PART_BW + 5e-6;
+            const double est = fmax((double)(tiles / CUS) * avgT + avgT / s2, maxT) + red;
             if (est < best * 0.97) {
                 best = est;
                 l.F = (int)(tiles - R);

@@ -2,7 +2,8 @@
 //
 // Data layout in device memory (all inside the caller's workspace):
 //
-//   status     one uint32 (bit 0: some L_i out of range)
+//   status     one uint32 (bit 0: some L_i out of range), then one uint32: the longest
+//              tile-pair cycle count of the call (256-row MFMA GEMM), both cleared by k_draws
 //   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
 //   CA         C-BSG only: CA[L][beta] = #{l < L : rA_l < beta}, uint16 [L_max+1][257]
 //   per batch entry b of A (batch entries):
@@ -61,6 +62,22 @@ constexpr int MSTEP = 8;         // cycles per octet (tile lengths padded to it)
 constexpr int MSTAGE = 4;        // slots per LDS stage of the MFMA GEMM (2 MFMA k-steps)
 constexpr int MFMA_BLOCKS_PER_CU = 2;   // resident 128-row MFMA GEMM blocks per CU (LDS bound)
 constexpr double MFMA_QUAD_RATE = 1.1e13;  // products/s of one 256 x 256 GEMM block (one per CU)
+constexpr double PART_BW = 3e12;           // bytes/s of writing and summing partial sums
+
+// Estimated time of the 256-row GEMM with every tile split s ways (F = 0): the larger of
+// the load per CU and the longest unit, plus writing and summing the partial sums.  With
+// one row length the units are equal and the load is whole rounds of them; with varying
+// lengths the tiles come longest first, so the blocks fill in behind the long units and
+// the load is the total over the CUs.  The host evaluates it with L_max, the GEMM kernels
+// again with the longest tile pair of the call (both pick the same way among s).
+__host__ __device__ inline double quad_split_time(int64_t tiles, int s, double perL, double Lmean,
+                                                  double Lmax, bool one_length) {
+    const double avgT = perL * Lmean, maxT = perL * Lmax;
+    const double load = one_length ? (double)((tiles * s + CUS - 1) / CUS) * avgT / s
+                                   : (double)tiles * avgT / CUS;
+    const double red = s > 1 ? (double)tiles * (2 * s) * 256.0 * 256.0 * 4.0 / PART_BW + 5e-6 : 0.0;
+    return (load > maxT / s ? load : maxT / s) + red;
+}
 constexpr int OCH = 8;           // octets per block of the nibble-plane generator
 constexpr int64_t MFMA_EXACT = 1ll << 24;   // K * L_max bound for exact fp32 counts
 
@@ -105,6 +122,8 @@ struct Layout {
     size_t stride_batchB;          // bytes per B batch entry block
     int S;             // splits of the element blocks per GEMM tile (1 = no split)
     int F;             // 256-row GEMM: tiles 0 .. F-1 run whole, tiles F.. in S parts each
+    double q_perL, q_Lmean;   // 256-row GEMM split model: seconds per cycle of one tile, mean L
+    int q_one;                // 256-row GEMM split model: all rows have one length
     size_t off_part;   // partial counts of split tiles: [split tiles][S][tile rows][tile columns]
     size_t total;
 };

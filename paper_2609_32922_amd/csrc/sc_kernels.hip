@@ -99,7 +99,10 @@ __global__ __launch_bounds__(256) void k_draws(uint64_t seed, int rng, int n, ui
                                                uint32_t *status) {
     const int l = blockIdx.x * blockDim.x + threadIdx.x;
     const int op = op_only >= 0 ? op_only : (int)blockIdx.y;
-    if (status != nullptr && l == 0 && blockIdx.y == 0) *status = 0u;
+    if (status != nullptr && l == 0 && blockIdx.y == 0) {
+        status[0] = 0u;
+        status[1] = 0u;   // longest tile pair of the call
+    }
     if (l >= n) return;
     const uint64_t h = splitmix64(2ull * seed + (uint64_t)op);
     uint32_t v = 0;
@@ -302,6 +305,8 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         if (t < lay.MT) tileOff[t] = carry + ex;
         carry += tot;
     }
+    // the first tile pair holds the batch entry's longest rows
+    if (tid == 0 && lay.mbm == 2 * BM) atomicMax(status + 1, (uint32_t)tileL[0]);
 }
 
 hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L, uint8_t *ws,

@@ -995,20 +995,45 @@ __device__ __forceinline__ void q_stage(int st, int nst, int64_t k0, int64_t k1,
     __syncthreads();
 }
 
+// The division of the call's tiles into units: (F, S) from the host, or, when the host
+// split every tile (F = 0), the split count chosen again with the longest tile pair the
+// scheduler found (never above the host's, for which grid and partial sums are sized).
+__device__ __forceinline__ void q_division(const MGemmArgs &g, const Layout &lay, uint8_t *ws, int &F, int &S) {
+    const int tiles = g.batch * (lay.MT / 2) * (lay.NT / 2);
+    F = g.F;
+    S = g.S;
+    if (F == 0 && S > 1) {
+        const double Lmax = (double)ws_ptr<uint32_t>(ws, lay.off_status)[1];
+        double best = 0.0;
+        for (int s = 1; s <= g.S; s *= 2) {
+            const double est = quad_split_time(tiles, s, lay.q_perL, lay.q_Lmean, Lmax, lay.q_one != 0);
+            if (s == 1 || est < best * 0.97) {
+                best = est;
+                S = s;
+            }
+        }
+        if (S == 1) F = tiles;
+    }
+}
+
 // One work unit: tile `tile` (pair tp of batch entry b x B pair tw) over k-steps
 // [s, s + 1) / S of the pair's k-steps.  Units 0 .. F-1 are the whole tiles 0 .. F-1,
-// decoded here; unit F + v is part v % S of tile F + v / S, stored as a partial sum.
+// decoded here; unit F + v is part v % S of tile F + v / S, stored as a partial sum;
+// units beyond those (a grid sized for a larger split) return at once.
 template <bool BIP>
 __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
     static_assert(QKS % 2 == 0, "the fragment sets alternate within a stage");
     __shared__ u4 smem[QNBUF * QBUF];
     const int NTW = lay.NT / 2;
+    int F, SS;
+    q_division(g, lay, ws, F, SS);
     const int u = blockIdx.x;
-    const bool split = u >= g.F;
-    const int v = u - g.F;
-    const int s = split ? v % g.S : 0;
-    const int S = split ? g.S : 1;
-    const int tile = split ? g.F + v / g.S : u;
+    if (u >= F + (g.batch * (lay.MT / 2) * NTW - F) * SS) return;
+    const bool split = u >= F;
+    const int v = u - F;
+    const int s = split ? v % SS : 0;
+    const int S = split ? SS : 1;
+    const int tile = split ? F + v / SS : u;
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
@@ -1119,17 +1144,20 @@ template <bool BIP>
 __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, uint8_t *ws) {
     constexpr int NK = 32 * 64 / 256;
     const int NTW = lay.NT / 2;
-    const int tile = g.F + (blockIdx.x >> 3), part8 = blockIdx.x & 7;
+    int F, SS;
+    q_division(g, lay, ws, F, SS);
+    const int tile = F + (blockIdx.x >> 3), part8 = blockIdx.x & 7;
+    if (tile >= g.batch * (lay.MT / 2) * NTW) return;
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
     const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part) +
-                                                      (size_t)(tile - g.F) * g.S * 256 * 256) +
+                                                      (size_t)(tile - F) * SS * 256 * 256) +
                        (size_t)part8 * 32 * 64 + threadIdx.x;
     int4 sum[NK];
 #pragma unroll
     for (int k = 0; k < NK; ++k) sum[k] = make_int4(0, 0, 0, 0);
-    for (int s = 0; s < g.S; ++s) {
+    for (int s = 0; s < SS; ++s) {
         const int4 *src = base + (size_t)s * 256 * 64;
         int4 q[NK];
 #pragma unroll
