@@ -712,6 +712,11 @@ struct FRow {
 template <int POL>
 __device__ __forceinline__ void f_gen_stage(const FRow &fr, const FWin &wv, int st0, int st, int KQP, int K,
                                             const uint32_t (*lut)[FLUT], u4 *dst) {
+    if (!fr.rowok) {      // padding row (a whole wave of B rows when N <= 64): zero nibbles
+#pragma unroll
+        for (int k = 0; k < 4; ++k) dst[k * BM] = u4{0u, 0u, 0u, 0u};
+        return;
+    }
     int o, dq0;
     f_stage_pos(st0 + st, KQP, o, dq0);
     f_gen(wv, (fr.rowoff + 4 * dq0) & 3, 4 * dq0, K, fr.Lr, fr.rowok, o, &lut[o & 1][fr.lside], dst, BM);
