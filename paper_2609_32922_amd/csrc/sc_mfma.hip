@@ -16,7 +16,8 @@
 //
 //   k_mplanes     nibble planes of A (sorted rows, per-row lengths) or B, one block per
 //                 128-row tile x 64 cycles x 64 elements; element parameters and an
-//                 8-cycle lookup table in LDS, 16-byte stores, 1 KB per wave
+//                 8-cycle lookup table in LDS, 16-byte stores, 1 KB per wave; with
+//                 comparator streams both operands in one launch (k_mplanes2)
 //   k_fgemm       N <= 128 with comparator streams: 128x128 tile, the fp4 fragments of
 //                 both operands built in LDS from the int8 rows (an 8-cycle table per
 //                 octet indexed by the int8 byte), so no planes are written or read
@@ -70,15 +71,22 @@ struct MPlaneArgs {
 // else -1 (bipolar) or 0 (unipolar, then times sign(q)); 0 at cycles >= L_row and for
 // padding.  Interval mode (CBSG = true, A side): nibble at counter k is sgn for
 // lo_d <= k < hi_d, else 0 (see the header comment).
+struct MPlaneShared {
+    uint32_t prm[64 * PRM_STRIDE];    // [element][row] packed parameters
+    uint32_t lut[OCH * CA_COLS];      // comparator: 8 nibbles per octet and beta
+    uint32_t spread[256];             // interval: 8-bit mask -> 8 nibbles of +1
+    uint32_t rr[OCH * MSTEP];         // comparator: the block's draws
+    int rowok[BM];                    // row of the tile holds data (not padding)
+};
+
+// block (x, y = element group, z = batch entry) of one side's grid
 template <int POL, bool CBSG>
-__global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
-    __shared__ uint32_t prm[64 * PRM_STRIDE];    // [element][row] packed parameters
-    __shared__ uint32_t lut[OCH * CA_COLS];      // comparator: 8 nibbles per octet and beta
-    __shared__ uint32_t spread[256];             // interval: 8-bit mask -> 8 nibbles of +1
-    __shared__ uint32_t rr[OCH * MSTEP];         // comparator: the block's draws
-    __shared__ int rowok[BM];                    // row of the tile holds data (not padding)
-    const int t = blockIdx.x / a.nchunk, ch = blockIdx.x % a.nchunk;
-    const int qg = blockIdx.y, b = blockIdx.z;
+__device__ __forceinline__ void mplanes_block(const MPlaneArgs &a, uint8_t *ws, MPlaneShared &sh, int bx,
+                                              int by, int bz) {
+    uint32_t *prm = sh.prm, *lut = sh.lut, *spread = sh.spread, *rr = sh.rr;
+    int *rowok = sh.rowok;
+    const int t = bx / a.nchunk, ch = bx % a.nchunk;
+    const int qg = by, b = bz;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     uint8_t *wsb = ws + (size_t)b * a.stride_batch;
 
@@ -217,6 +225,27 @@ __global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
     }
 }
 
+template <int POL, bool CBSG>
+__global__ __launch_bounds__(256) void k_mplanes(MPlaneArgs a, uint8_t *ws) {
+    __shared__ MPlaneShared sh;
+    mplanes_block<POL, CBSG>(a, ws, sh, blockIdx.x, blockIdx.y, blockIdx.z);
+}
+
+// both sides in one launch (comparator streams): blocks [0, nA) are A's grid
+// (gxA x gy x batch), the rest B's (gxB x gy x nbB), so B's blocks fill A's last wave
+template <int POL>
+__global__ __launch_bounds__(256) void k_mplanes2(MPlaneArgs a, MPlaneArgs bb, int gxA, int gxB, int gy,
+                                                  int nA, uint8_t *ws) {
+    __shared__ MPlaneShared sh;
+    const int bid = blockIdx.x;
+    if (bid < nA) {
+        mplanes_block<POL, false>(a, ws, sh, bid % gxA, (bid / gxA) % gy, bid / (gxA * gy));
+    } else {
+        const int v = bid - nA;
+        mplanes_block<POL, false>(bb, ws, sh, v % gxB, (v / gxB) % gy, v / (gxB * gy));
+    }
+}
+
 template <bool CBSG>
 static void launch_mplanes_side(int polarity, dim3 grid, const MPlaneArgs &pa, uint8_t *ws,
                                 hipStream_t st) {
@@ -251,12 +280,11 @@ hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t
     pa.off_r = lay.off_rA;
     pa.off_CA = lay.off_CA;
     const dim3 gA((unsigned)(lay.MT * pa.nchunk), qgroups, (unsigned)d.batch);
-    if (cbsg)
+    if (cbsg) {
         launch_mplanes_side<true>(d.polarity, gA, pa, ws, st);
-    else
-        launch_mplanes_side<false>(d.polarity, gA, pa, ws, st);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
 
     MPlaneArgs pb = pa;
     pb.X = B;
@@ -272,7 +300,17 @@ hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t
     pb.off_r = lay.off_rB;
     pb.off_CA = 0;
     const dim3 gB((unsigned)(lay.NT * pb.nchunk), qgroups, (unsigned)lay.nbB);
-    launch_mplanes_side<false>(d.polarity, gB, pb, ws, st);
+    if (cbsg) {
+        launch_mplanes_side<false>(d.polarity, gB, pb, ws, st);
+        return hipGetLastError();
+    }
+    const int nA = (int)(gA.x * gA.y * gA.z), nB = (int)(gB.x * gB.y * gB.z);
+    if (d.polarity == SC_BIPOLAR_XNOR)
+        hipLaunchKernelGGL((k_mplanes2<SC_BIPOLAR_XNOR>), dim3((unsigned)(nA + nB)), dim3(256), 0, st, pa, pb,
+                           (int)gA.x, (int)gB.x, (int)qgroups, nA, ws);
+    else
+        hipLaunchKernelGGL((k_mplanes2<SC_UNIPOLAR_AND_SM>), dim3((unsigned)(nA + nB)), dim3(256), 0, st, pa, pb,
+                           (int)gA.x, (int)gB.x, (int)qgroups, nA, ws);
     return hipGetLastError();
 }
 
