@@ -99,7 +99,11 @@ __device__ __forceinline__ void mplanes_block(const MPlaneArgs &a, uint8_t *ws, 
         perm = ws_ptr<int32_t>(wsb, a.off_perm);
         Ls = ws_ptr<int32_t>(wsb, a.off_Ls);
     } else {
+        // B: every cycle up to L_max, or only up to the longest tile pair of the call when
+        // the scheduler recorded it (256-row GEMM): no tile reads B's planes beyond it
         Lloop = a.LBS;
+        const int longest = (int)ws_ptr<uint32_t>(ws, 0)[1];
+        if (longest > 0 && longest < Lloop) Lloop = longest;
         off = (int64_t)t * a.LBS * a.KQP * 64;
     }
     const int o0 = ch * OCH;
