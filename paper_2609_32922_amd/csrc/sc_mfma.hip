@@ -1063,6 +1063,33 @@ __device__ __forceinline__ void q_division(const MGemmArgs &g, const Layout &lay
     }
 }
 
+// XCDs of the chip: the dispatcher hands workgroup u to XCD u % 8, and each XCD has its own L2
+constexpr int NXCD = 8;
+// pair rows per band in the order of the whole tiles
+constexpr int QG = 4;
+
+// The whole tile that unit u (< F) computes.  Units are regrouped so that the 8 C units
+// that run at once on the 8 XCDs take 8 runs of C consecutive tiles, one run per XCD, in
+// the same overall order as before (so tiles of similar length still run together), and
+// consecutive tiles go column by column through bands of QG pair rows: a run of 32 tiles
+// covers 4 A pairs and 8 B pairs, which then hit in that XCD's L2.  Both steps are
+// permutations of 0 .. F-1 (tiles past the last full run, or past the last full row of
+// pair tiles, keep their place).
+__device__ __forceinline__ int q_whole_tile(int u, int F, int NTW) {
+    const int C = min(32, F / NXCD);
+    if (C >= 2 && u < F / (NXCD * C) * (NXCD * C)) {
+        const int j = u / NXCD, x = u % NXCD;
+        u = ((j / C) * NXCD + x) * C + j % C;
+    }
+    const int R = F / NTW;
+    if (u < R * NTW) {
+        const int gb = u / (QG * NTW), idx = u % (QG * NTW);
+        const int gs = min(QG, R - gb * QG);
+        return (gb * QG + idx % gs) * NTW + idx / gs;
+    }
+    return u;
+}
+
 // One work unit: tile `tile` (pair tp of batch entry b x B pair tw) over k-steps
 // [s, s + 1) / S of the pair's k-steps.  Units 0 .. F-1 are the whole tiles 0 .. F-1,
 // decoded here; unit F + v is part v % S of tile F + v / S, stored as a partial sum;
@@ -1080,7 +1107,7 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
     const int v = u - F;
     const int s = split ? v % SS : 0;
     const int S = split ? SS : 1;
-    const int tile = split ? F + v / SS : u;
+    const int tile = split ? F + v / SS : q_whole_tile(u, F, NTW);
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
