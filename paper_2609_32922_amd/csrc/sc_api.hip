@@ -44,6 +44,10 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
               fused_extent(d.M, d.lda, d.K) < INT_MAX - 4 && fused_extent(d.N, d.ldb, d.K) < INT_MAX - 4;
     l.mbm = (mfma && l.MT > 1 && l.mbn == 2 * BN) ? 2 * BM : BM;
     if (l.mbm == 2 * BM) l.MT = (int)round_up(l.MT, 2);
+    // 256 x 256 blocks with comparator streams: fragments from int8 chunks and a table of
+    // each 32-cycle group, so the operands are read as bytes instead of fp4 planes
+    l.rgen = l.mbm == 2 * BM && d.rng == SC_RNG_LFSR32;
+    l.KC = (d.K + 31) / 32;
     l.LBS = (int)round_up(d.L_max, LCH);
     l.LP = (int)round_up(d.L_max, LSTEP);
     l.nbB = (d.strideB == 0) ? 1 : d.batch;
@@ -57,7 +61,7 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     // the status word is always the first word of the workspace
     size_t off = 0;
     l.off_status = off;
-    off = align256(off + 4);
+    off = align256(off + 3 * 4);
     l.off_rA = off;
     off = align256(off + (size_t)l.LBS * 4);
     l.off_rB = off;
@@ -83,6 +87,7 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     if (!mul_ok((size_t)l.MT * (size_t)l.words_per_L, (size_t)round_up(d.L_max, l.tstep) * 4, &sz))
         return false;
     if (l.fused) sz = 0;
+    if (l.rgen && !mul_ok(rowsA, (size_t)l.KC * 32, &sz)) return false;
     a = align256(a + sz);
     l.off_SA = a;
     if (signsA) a = align256(a + rowsA * (size_t)l.KB * 4);
@@ -98,7 +103,7 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.off_Bp = bb;
     if (!mul_ok((size_t)l.NT * (size_t)l.words_per_L, (size_t)l.LBS * 4, &sz)) return false;
     if (l.fused) sz = 0;
-    (void)rowsB;
+    if (l.rgen && !mul_ok(rowsB, (size_t)l.KC * 32, &sz)) return false;
     bb = align256(bb + sz);
     l.off_SB = bb;
     if (signsB) bb = align256(bb + rowsB * (size_t)l.KB * 4);
@@ -114,7 +119,8 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     const bool quad = mfma && l.mbm == 2 * BM;
     const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * (l.MT / (l.mbm / BM)) *
                           (mfma ? l.NT / (l.mbn / BN) : l.NT);
-    const int kunits = mfma ? l.KQP / 2 : l.KB;     // indivisible steps along K per cycle
+    // indivisible steps along K per cycle (chunks of every 32-cycle group with rgen)
+    const int kunits = l.rgen ? l.KC * (l.LBS / 32) : mfma ? l.KQP / 2 : l.KB;
     const double tile_bytes = (double)l.mbm * (mfma ? l.mbn : BN) * 4.0;
     const double Lmean = d.L_hint > 0 ? d.L_hint : d.L_max;
     l.S = 1;
@@ -309,7 +315,9 @@ int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const in
     const bool mfma = lay.engine == SC_ENGINE_MFMA;
     if (!mfma && lay.mode == MODE_AND && (e = launch_marginals(d, lay, A, B, ws, st)) != hipSuccess)
         return SC_ERR_HIP;
-    if (!lay.fused) {
+    if (lay.rgen) {
+        if ((e = launch_rchunks(d, lay, A, B, ws, st)) != hipSuccess) return SC_ERR_HIP;
+    } else if (!lay.fused) {
         e = mfma ? launch_mplanes(d, lay, A, B, ws, st) : launch_planes(d, lay, A, B, ws, st);
         if (e != hipSuccess) return SC_ERR_HIP;
     }

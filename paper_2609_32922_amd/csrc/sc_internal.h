@@ -3,7 +3,8 @@
 // Data layout in device memory (all inside the caller's workspace):
 //
 //   status     one uint32 (bit 0: some L_i out of range), then one uint32: the longest
-//              tile-pair cycle count of the call (256-row MFMA GEMM), both cleared by k_draws
+//              tile-pair cycle count of the call (256-row MFMA GEMM), then one uint32: nonzero
+//              when some L_i is not a multiple of 32; all cleared by k_draws
 //   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
 //   CA         C-BSG only: CA[L][beta] = #{l < L : rA_l < beta}, uint16 [L_max+1][257]
 //   per batch entry b of A (batch entries):
@@ -32,6 +33,12 @@
 // value +1 (0x2), -1 (0xA) or 0.  Slots are ordered s = o * KQP + dq and each slot
 // stores its 128 rows contiguously: A tile t is uint4 [Lloop/8 * KQP][128], B tile is
 // uint4 [LBS/8 * KQP][128].  A row of length L has zero nibbles at cycles >= L.
+//
+// MFMA engine, 256 x 256 GEMM blocks with comparator streams (rgen): no planes.  Ap and Bp
+// hold the int8 operands in 32-element chunks instead: pair t of 256 rows (A in the
+// scheduler's order) is bytes [KC][256][32], byte e of row r of chunk c = element 32c + e,
+// with -128 read as -127 (the same comparator boundaries) and 0x80 (-128) marking an
+// element >= K or a padding row.  The GEMM builds the fp4 fragments from them.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -114,6 +121,9 @@ struct Layout {
     int mbm;           // MFMA engine: rows of A per GEMM block: 256 (row tiles taken in pairs
                        // that run at the pair's longest length; MT even) when mbn = 256 and
                        // MT > 1, else 128
+    int rgen;          // 256-row GEMM with comparator streams: fragments built in the GEMM
+                       // from int8 chunks and a per-group table (no planes)
+    int KC;            // 32-element chunks per row, ceil(K/32)
     int64_t words_per_L;   // plane words of one 128-row tile per cycle of its length
     size_t off_rA, off_rB, off_status, off_CA;
     size_t off_perm, off_Ls, off_RA, off_tileL, off_tileOff, off_Ap, off_SA;
@@ -152,6 +162,8 @@ hipError_t launch_mgemm(const sc_gemm_desc &d, const Layout &lay, const float *s
 hipError_t launch_fgemm(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
                         const float *sA, const float *sB, float *out, int32_t *counts, uint8_t *ws,
                         hipStream_t st);
+hipError_t launch_rchunks(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
+                          uint8_t *ws, hipStream_t st);
 
 // bytes of one batch entry of an operand from its first byte: (rows - 1) * ld + K
 __host__ __device__ inline int64_t fused_extent(int rows, int64_t ld, int K) {

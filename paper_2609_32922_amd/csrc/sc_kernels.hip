@@ -102,6 +102,7 @@ __global__ __launch_bounds__(256) void k_draws(uint64_t seed, int rng, int n, ui
     if (status != nullptr && l == 0 && blockIdx.y == 0) {
         status[0] = 0u;
         status[1] = 0u;   // longest tile pair of the call
+        status[2] = 0u;   // some row length is not a multiple of 32
     }
     if (l >= n) return;
     const uint64_t h = splitmix64(2ull * seed + (uint64_t)op);
@@ -250,6 +251,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 
     for (int v = tid; v <= L_max; v += 1024) hist[v] = 0;
     __syncthreads();
+    bool ragged = false;
     for (int i0 = 0; i0 < M; i0 += 1024) {
         const int i = i0 + tid;
         int l = i < M ? Lb[i] : 0;
@@ -257,9 +259,10 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
             atomicOr(status, STATUS_BAD_LENGTH);
             l = 0;
         }
+        ragged = ragged || (l % 32) != 0;
         wave_bucket_add(hist, l, i < M);
     }
-    __syncthreads();
+    if (__syncthreads_or(ragged) && tid == 0) atomicOr(status + 2, 1u);
     // start position of each length bucket, longest lengths first
     int64_t carry = 0;
     for (int c = 0; c <= L_max; c += 1024) {

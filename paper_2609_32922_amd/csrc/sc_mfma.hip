@@ -34,6 +34,8 @@
 //                 keeps the matrix cores fed where the 16x16x128 form loses several cycles
 //                 per instruction to issue.
 //   k_mgemm_reduce sums the partial counts of split tiles and decodes
+#include <limits.h>
+
 #include "sc_internal.h"
 
 namespace scg {
@@ -322,7 +324,7 @@ hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t
 // MFMA GEMM
 // ----------------------------------------------------------------------------
 struct MGemmArgs {
-    int M, N, K, KQP, LBS, nbB, batch, S, F;
+    int M, N, K, KQP, LBS, nbB, batch, S, F, KC;
     const float *sA, *sB;
     int64_t strideSA, strideSB, strideO, ldo;
     float *out;
@@ -1268,10 +1270,352 @@ static hipError_t launch_qgemm(const MGemmArgs &g, const Layout &lay, uint8_t *w
     return hipGetLastError();
 }
 
+// ----------------------------------------------------------------------------
+// 256 x 256 GEMM with fragments built from int8 chunks (comparator streams)
+// ----------------------------------------------------------------------------
+// One comparator sequence per operand makes the 32 stream bits of an element over the
+// cycles 32G .. 32G + 31 a function of its int8 value alone: one 16-byte fp4 slot row.  The
+// GEMM keeps that table for its current cycle group G in LDS and builds every MFMA
+// fragment with one table read indexed by the element's byte, so the operands stream in
+// as bytes (k_rchunks lays them out) instead of as fp4 planes 8 L times their size.
+// Slot rows: a k-step takes one element per lane half (lanes 0-31 the elements 0..15 of
+// their row's chunk, lanes 32-63 the elements 16..31, one element per k-step) over the 32
+// cycles of the group; both operands use the same order, so the k-step sums the products
+// of matching elements and cycles.
+constexpr int RCH = 32;          // elements per chunk, cycles per group
+constexpr int RREP = 8;          // copies of each table entry (16-byte reads spread over the banks)
+constexpr int RPAD = 0x80;       // chunk byte of a padding element or row: the table gives zero
+
+// chunks of one operand: thread = (row r of the tile order, element e of chunk c)
+__global__ __launch_bounds__(256) void k_rchunks(const int8_t *X, int64_t ld, int64_t strideX, int rows, int K,
+                                                 int KC, size_t stride_batch, size_t off_perm, int permuted,
+                                                 size_t off_out, uint8_t *ws) {
+    const int b = blockIdx.z, c = blockIdx.y;
+    const int r = blockIdx.x * 8 + (threadIdx.x >> 5), e = threadIdx.x & 31;
+    uint8_t *wsb = ws + (size_t)b * stride_batch;
+    const int src = permuted ? ws_ptr<int32_t>(wsb, off_perm)[r] : (r < rows ? r : -1);
+    const int d = c * RCH + e;
+    int v = -RPAD;
+    if (src >= 0 && d < K) {
+        v = X[(size_t)b * strideX + (size_t)src * ld + d];
+        v = v < -127 ? -127 : v;
+    }
+    ws_ptr<uint8_t>(wsb, off_out)[(((size_t)(r >> 8) * KC + c) * 256 + (r & 255)) * RCH + e] = (uint8_t)v;
+}
+
+hipError_t launch_rchunks(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
+                          uint8_t *ws, hipStream_t st) {
+    if (lay.KC == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_rchunks, dim3((unsigned)(lay.MT * BM / 8), (unsigned)lay.KC, (unsigned)d.batch),
+                       dim3(256), 0, st, A, d.lda, d.strideA, d.M, d.K, lay.KC, lay.stride_batchA,
+                       lay.off_perm, 1, lay.off_Ap, ws);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_rchunks, dim3((unsigned)(lay.NT * BN / 8), (unsigned)lay.KC, (unsigned)lay.nbB),
+                       dim3(256), 0, st, B, d.ldb, d.strideB, d.N, d.K, lay.KC, lay.stride_batchB,
+                       (size_t)0, 0, lay.off_Bp, ws);
+    return hipGetLastError();
+}
+
+// the nibbles of cycles 32G .. 32G+31 that lie below a row length L (cycle order as in the table)
+__device__ __forceinline__ u4 r_len_mask(int L, int G) {
+    const int rem = L - RCH * G;
+    u4 m;
+#pragma unroll
+    for (int dw = 0; dw < 4; ++dw) {
+        const int n = rem - 8 * dw;
+        m[dw] = n >= 8 ? 0xFFFFFFFFu : (n <= 0 ? 0u : (1u << (4 * n)) - 1u);
+    }
+    return m;
+}
+
+// Table of cycle group G: entry (byte, operand) holds the 32 nibbles of cycles 32G .. 32G+31
+// (cycle 32G + k at bits 4 (k % 8) of dword k / 8), sign folded in (unipolar), zero for the
+// padding byte.  Entry copies are laid out [byte][operand][copy], so a read's byte
+// address is byte * 256 + operand * 128 + copy * 16.
+template <bool BIP>
+__device__ __forceinline__ void r_build_lut(u4 *lut, const uint32_t *rA, const uint32_t *rB, int G, int tid) {
+    const uint32_t zero_nib = BIP ? NIB_NEG : 0u;
+    const int byte = tid;
+    const int q = (int)(int8_t)(uint8_t)byte;
+    const uint32_t beta = (uint32_t)(BIP ? beta_bipolar(q) : beta_unipolar(q));
+#pragma unroll
+    for (int side = 0; side < 2; ++side) {
+        const uint32_t *r = (side ? rB : rA) + RCH * G;
+        u4 x = u4{0u, 0u, 0u, 0u};
+        if (byte != RPAD) {
+#pragma unroll
+            for (int dw = 0; dw < 4; ++dw) {
+                uint32_t w = 0;
+#pragma unroll
+                for (int c = 0; c < 8; ++c) w |= (r[8 * dw + c] < beta ? NIB_POS : zero_nib) << (4 * c);
+                x[dw] = (!BIP && q < 0) ? negate_nibbles(w) : w;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < RREP; ++k) lut[byte * 16 + side * RREP + k] = x;
+    }
+}
+
+struct RData {
+    u4 a[4], b[4];     // 16 elements of the lane's 4 A rows and 4 B columns (one chunk)
+};
+struct RSrc {
+    __amdgpu_buffer_rsrc_t a, b;   // the pair's A chunks and the B pair's chunks
+    int voffA, voffB;              // the lane's row and half within a chunk
+    uint32_t loA, loB;             // the lane's table copies of A and B (low address byte)
+    const char *lut;
+    int KC;
+};
+
+__device__ __forceinline__ void r_load(const RSrc &q, int c, RData &d) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        d.a[i] = __builtin_amdgcn_raw_buffer_load_b128(q.a, q.voffA, c * 256 * RCH + i * 32 * RCH, 0);
+        d.b[i] = __builtin_amdgcn_raw_buffer_load_b128(q.b, q.voffB, c * 256 * RCH + i * 32 * RCH, 0);
+    }
+}
+
+// rows that have ended before this cycle group read the padding byte, whose table row is zero
+__device__ __forceinline__ void r_finish(RData &d, const bool (&fin)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        if (fin[i]) d.a[i] = u4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
+}
+
+// the table row of element E (0..15) of a lane's 16: address byte 1 = the element's byte,
+// byte 0 = the copy (from lo)
+template <int E>
+__device__ __forceinline__ u4 r_look(const RSrc &q, uint32_t word, uint32_t lo) {
+    constexpr uint32_t sel = 0x0C0C0000u | ((4u + (E & 3)) << 8);
+    return *reinterpret_cast<const u4 *>(q.lut + __builtin_amdgcn_perm(word, lo, sel));
+}
+template <int E>
+__device__ __forceinline__ uint32_t r_word(const u4 &v) {
+    return v[E >> 2];
+}
+
+// fragments of k-step E (element E of the lane's 16) from chunk data d
+template <int E, bool MASK>
+__device__ __forceinline__ void r_frags(const RSrc &q, const RData &d, const u4 (&m)[4], QFrags &f) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) f.b[c] = r_look<E>(q, r_word<E>(d.b[c]), q.loB);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f.a[i] = r_look<E>(q, r_word<E>(d.a[i]), q.loA);
+        if (MASK) f.a[i] &= m[i];
+    }
+}
+
+// Stage S (k-steps 2S, 2S+1) of a chunk: fragment set 0 holds k-step 2S on entry and the
+// next k-step (2S + 2, or the next chunk's first) on exit; stage 0 loads the next chunk.
+// MASK: the A fragments are masked with the rows' lengths (some row of the pair ends
+// inside a cycle group); else rows that have ended read the padding byte (r_finish).
+template <int S, bool MASK>
+__device__ __forceinline__ void r_stage(const RSrc &q, int cnext, RData &cur, RData &nxt, const u4 (&m)[4],
+                                        const bool (&fin)[4], v16f (&acc)[4][4], QFrags (&f)[2]) {
+    if (S == 0) r_load(q, cnext, nxt);
+    r_frags<2 * S + 1, MASK>(q, cur, m, f[1]);
+    q_mma(acc, f[0]);
+    if (S < 7) {
+        r_frags<2 * S + 2, MASK>(q, cur, m, f[0]);
+    } else {
+        if (!MASK) r_finish(nxt, fin);
+        r_frags<0, MASK>(q, nxt, m, f[0]);
+    }
+    q_mma(acc, f[1]);
+    // each half: the 8 table reads of the next fragments (with their address bytes, and
+    // the masks) in the first 8 MFMAs; the chunk loads go with the first half of stage 0
+    constexpr int NV = MASK ? 3 : 1;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, NV, 0);  // VALU
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (S == 0 && h == 0) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global load
+        }
+    }
+}
+
+// chunks c .. ce-1 of one cycle group; on exit cur holds the chunk after them (chunk ce, or
+// chunk 0 of the next group) and fragment set 0 its first k-step (from this group's table)
+template <bool MASK>
+__device__ __forceinline__ void r_chunks(const RSrc &q, int c, int ce, RData &cur, RData &nxt,
+                                         const u4 (&m)[4], const bool (&fin)[4], v16f (&acc)[4][4],
+                                         QFrags (&f)[2]) {
+    for (; c < ce; ++c) {
+        const int x = c + 1 < q.KC ? c + 1 : 0;
+        r_stage<0, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage<1, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage<2, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage<3, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage<4, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage<5, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage<6, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage<7, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        cur = nxt;
+    }
+}
+
+// One work unit, as in k_qgemm: tile `tile` over chunk steps [s, s + 1) / S of the pair's
+// (group, chunk) steps, whole tiles decoded here, parts stored as partial sums.  Both
+// variants are launched and one returns at once: MASK runs when some row length of the
+// call is not a multiple of 32 (a row ends inside a cycle group, so every A fragment is
+// masked with its row's length), the other when all are (rows that have ended read the
+// padding byte, whose table row is zero, and nothing else is masked).
+template <bool BIP, bool MASK>
+__global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
+    __shared__ u4 lut[256 * 2 * RREP];     // 64 KB; the epilogue's transpose reuses it
+    if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
+    const int NTW = lay.NT / 2;
+    int F, SS;
+    q_division(g, lay, ws, F, SS);
+    const int u = blockIdx.x;
+    if (u >= F + (g.batch * (lay.MT / 2) * NTW - F) * SS) return;
+    const bool split = u >= F;
+    const int v = u - F;
+    const int s = split ? v % SS : 0;
+    const int S = split ? SS : 1;
+    const int tile = split ? F + v / SS : q_whole_tile(u, F, NTW);
+    const int tw = tile % NTW;
+    const int tb = tile / NTW;
+    const int b = tb % g.batch, tp = tb / g.batch;
+    const int bB = g.nbB == 1 ? 0 : b;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int grp = lane >> 5, i32 = lane & 31;
+    const int wr = (w >> 1) * 128, wc = (w & 1) * 128;
+    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
+    uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
+    const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm) + tp * 256;
+    const int32_t *Ls = ws_ptr<int32_t>(wsa, lay.off_Ls) + tp * 256;
+    const int ngroups = (int)(round_up(ws_ptr<int32_t>(wsa, lay.off_tileL)[2 * tp], RCH) / RCH);
+    const int64_t nch = (int64_t)ngroups * g.KC;
+    const int64_t x0 = (int64_t)s * nch / S, x1 = (int64_t)(s + 1) * nch / S;
+
+    // the lane's A rows' lengths (padding rows: never end)
+    int Lr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = wr + 32 * i + i32;
+        Lr[i] = perm[row] >= 0 ? Ls[row] : INT_MAX;
+    }
+
+    const size_t pairb = (size_t)g.KC * 256 * RCH;
+    RSrc q;
+    q.a = __builtin_amdgcn_make_buffer_rsrc(ws_ptr<uint8_t>(wsa, lay.off_Ap) + (size_t)tp * pairb, 0, (int)pairb,
+                                            0x00020000);
+    q.b = __builtin_amdgcn_make_buffer_rsrc(ws_ptr<uint8_t>(wsbB, lay.off_Bp) + (size_t)tw * pairb, 0, (int)pairb,
+                                            0x00020000);
+    q.voffA = (wr + i32) * RCH + grp * 16;
+    q.voffB = (wc + i32) * RCH + grp * 16;
+    q.loA = 16u * (uint32_t)(lane & (RREP - 1));
+    q.loB = q.loA + 16u * RREP;
+    q.lut = reinterpret_cast<const char *>(lut);
+    q.KC = g.KC > 0 ? g.KC : 1;
+    const uint32_t *rA = ws_ptr<uint32_t>(ws, lay.off_rA), *rB = ws_ptr<uint32_t>(ws, lay.off_rB);
+
+    v16f acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[i][c] = v16f{};
+
+    RData cur, nxt;
+    QFrags f[2];
+    u4 m[4];
+    if (x0 < x1) r_load(q, (int)(x0 % q.KC), cur);
+    for (int64_t x = x0; x < x1;) {
+        const int G = (int)(x / g.KC);
+        const int64_t xe = min(x1, (int64_t)(G + 1) * g.KC);
+        // every read of the previous group's table is done before it is replaced
+        __syncthreads();
+        r_build_lut<BIP>(lut, rA, rB, G, tid);
+        __syncthreads();
+        // length masks of the lane's A rows, or which of them have ended
+        bool fin[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (MASK) m[i] = r_len_mask(Lr[i], G);
+            fin[i] = Lr[i] <= RCH * G;
+        }
+        if (!MASK) r_finish(cur, fin);
+        r_frags<0, MASK>(q, cur, m, f[0]);
+        r_chunks<MASK>(q, (int)(x - (int64_t)G * g.KC), (int)(xe - (int64_t)G * g.KC), cur, nxt, m, fin, acc,
+                       f);
+        x = xe;
+    }
+
+    if (split) {
+        int32_t *part = ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    part[(wr + 32 * i + 8 * (e >> 2) + 4 * grp + (e & 3)) * 256 + wc + 32 * c + i32] =
+                        (int32_t)acc[i][c][e];
+    } else {
+        // transpose through LDS, 32 rows at a time, so that each thread decodes four
+        // adjacent columns of one row
+        constexpr int TS = 256 + 4, TR = 32;
+        static_assert(TR * TS * 4 <= (int)sizeof(lut), "the epilogue transpose must fit the table");
+        int32_t *T = reinterpret_cast<int32_t *>(lut);
+        for (int h = 0; h < 256 / TR; ++h) {
+            __syncthreads();
+            // rows 32h .. 32h + 31: MFMA block i = h % 4 of the waves at wr = 128 (h / 4)
+            if (wr == 128 * (h >> 2)) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (i != (h & 3)) continue;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+#pragma unroll
+                        for (int e = 0; e < 16; ++e)
+                            T[(8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] = (int32_t)acc[i][c][e];
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int k = 0; k < TR * 64 / 256; ++k) {
+                const int idx = tid + 256 * k;        // 32 rows x 64 column quads
+                const int rl = idx >> 6, cq = idx & 63;
+                const int j0 = tw * 256 + 4 * cq;
+                if (j0 >= g.N) continue;
+                const int4 qv = *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]);
+                const int32_t P[4] = {qv.x, qv.y, qv.z, qv.w};
+                mdecode4<BIP>(P, tp * 256 + TR * h + rl, j0, min(4, g.N - j0), b, g, lay, ws);
+            }
+        }
+    }
+}
+
+template <bool BIP>
+static hipError_t launch_rgemm(const MGemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
+    const unsigned tiles = (unsigned)(g.batch * (lay.MT / 2) * (lay.NT / 2));
+    const unsigned tail = tiles - (unsigned)g.F;
+    hipLaunchKernelGGL((k_rgemm<BIP, false>), dim3((unsigned)g.F + tail * (unsigned)g.S), dim3(256), 0, st, g,
+                       lay, ws);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_rgemm<BIP, true>), dim3((unsigned)g.F + tail * (unsigned)g.S), dim3(256), 0, st, g,
+                       lay, ws);
+    e = hipGetLastError();
+    if (e != hipSuccess || tail == 0) return e;
+    hipLaunchKernelGGL((k_qgemm_reduce<BIP>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
+    return hipGetLastError();
+}
+
 template <bool BIP>
 static hipError_t launch_mgemm_pol(const MGemmArgs &g, const Layout &lay, uint8_t *ws,
                                    hipStream_t st) {
-    if (lay.mbm == 256) return launch_qgemm<BIP>(g, lay, ws, st);
+    if (lay.mbm == 256) return lay.rgen ? launch_rgemm<BIP>(g, lay, ws, st) : launch_qgemm<BIP>(g, lay, ws, st);
     if (lay.mbn == 256) return launch_mgemm_tile<BIP, 256>(g, lay, ws, st);
     return launch_mgemm_tile<BIP, 128>(g, lay, ws, st);
 }
@@ -1288,6 +1632,7 @@ static MGemmArgs make_gemm_args(const sc_gemm_desc &d, const Layout &lay, const 
     g.batch = d.batch;
     g.S = lay.S;
     g.F = lay.F;
+    g.KC = lay.KC;
     g.sA = sA;
     g.sB = sB;
     g.strideSA = d.strideSA;
@@ -1322,24 +1667,7 @@ hipError_t launch_fgemm(const sc_gemm_desc &d, const Layout &lay, const int8_t *
 
 hipError_t launch_mgemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
                         float *out, int32_t *counts, uint8_t *ws, hipStream_t st) {
-    MGemmArgs g{};
-    g.M = d.M;
-    g.N = d.N;
-    g.K = d.K;
-    g.KQP = lay.KQP;
-    g.LBS = lay.LBS;
-    g.nbB = lay.nbB;
-    g.batch = d.batch;
-    g.S = lay.S;
-    g.F = lay.F;
-    g.sA = sA;
-    g.sB = sB;
-    g.strideSA = d.strideSA;
-    g.strideSB = d.strideSB;
-    g.strideO = d.strideO;
-    g.ldo = d.ldo;
-    g.out = out;
-    g.counts = counts;
+    const MGemmArgs g = make_gemm_args(d, lay, sA, sB, out, counts);
     if (d.polarity == SC_BIPOLAR_XNOR) return launch_mgemm_pol<true>(g, lay, ws, st);
     return launch_mgemm_pol<false>(g, lay, ws, st);
 }
