@@ -30,6 +30,8 @@
  *   bipolar   z = [r_l < beta(q)],  beta(q)   = floor((256 (q+127) + 127) / 254)
  *   unipolar  z = [r_l < beta_u(q)], beta_u(q) = floor((256 |q| + 63) / 127),
  *             sign = (q < 0)
+ *   -128, outside the quantiser's range, gives the same streams as -127 (every
+ *   boundary it would have lies at 0 or at 256 and above).
  *
  * Second comparator source, rng = SC_RNG_SOBOL8_CBSG (Sec. 4.2 "cumulative-indicator
  * C-BSG" and Sec. A.1 Eq. (4)-(6), readings fixed here): A draws from Sobol dimension 1

@@ -90,10 +90,13 @@ constexpr int64_t MFMA_EXACT = 1ll << 24;   // K * L_max bound for exact fp32 co
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
-// comparator boundaries of an int8 value (bipolar, and unipolar magnitude)
+// comparator boundaries of an int8 value (bipolar, and unipolar magnitude).  -128 lies
+// outside the quantiser's range; its boundaries equal those of -127 (0 bipolar, and a
+// magnitude boundary at or above 256 unipolar: a one on every cycle), so the magnitude is
+// capped at 127 and every boundary stays in [0, 256].
 __device__ __forceinline__ int beta_bipolar(int q) { return (256 * (q + 127) + 127) / 254; }
 __device__ __forceinline__ int beta_unipolar(int q) {
-    const int a = q < 0 ? -q : q;
+    const int a = q < 0 ? (q < -127 ? 127 : -q) : q;
     return (256 * a + 63) / 127;
 }
 

@@ -204,6 +204,69 @@ def test_engines_agree_full_size(dev, name):
 
 
 # --------------------------------------------------------------------------
+# 256 x 256 MFMA GEMM with comparator streams: fp4 fragments built from int8 chunks
+# through a table per 32-cycle group.  One variant masks every A fragment with its row's
+# length (some length of the call is not a multiple of 32), the other lets rows that
+# have ended read the padding byte (all lengths multiples of 32).
+# --------------------------------------------------------------------------
+RGEN = [
+    # batch, M, N, K, L_max, lengths, polarity, broadcast_B, seed
+    (1, 300, 270, 100, 160, "mult32", 0, False, 61),   # rows end at group bounds, some at 0
+    (2, 257, 300, 33, 96, "mult32", 1, True, 63),      # K one past a chunk, broadcast B
+    (1, 520, 260, 16, 100, "uniform", 0, False, 65),   # one length inside a group; K < 32
+    (1, 384, 257, 300, 64, "random", 1, False, 67),    # every length; split k-ranges
+    (3, 140, 129, 64, 512, "uniform", 1, False, 69),   # 16 groups, one pair per batch entry
+    (1, 600, 513, 45, 33, "random", 0, False, 71),     # one cycle past the first group
+]
+
+
+def _rgen_gemm(case):
+    batch, M, N, K, L_max, kind, pol, bcast, seed = case
+    rng = np.random.default_rng(seed)
+    g = W.random_gemm(rng, batch, M, N, K, L_max, pol, seed, broadcast_B=bcast)
+    if kind == "mult32":
+        g.L = (rng.integers(0, L_max // 32 + 1, g.L.shape) * 32).astype(np.int32)
+    elif kind == "uniform":
+        g.L = np.full(g.L.shape, L_max, np.int32)
+    return g
+
+
+@pytest.mark.parametrize("case", RGEN, ids=[str(c) for c in RGEN])
+def test_rgen_full_compare(dev, oracle_mod, case):
+    g = _rgen_gemm(case)
+    _note("int8-chunk GEMM %s" % (case,))
+    out, cnt = _run(g, dev, engine=2)
+    for b in range(g.batch):
+        _compare(g, b, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "rgen%s b%d" % (case, b))
+
+
+INT8_MIN_SHAPES = [
+    # M, N, rng: int8-chunk GEMM, 128-row planes GEMM (M <= 128), fragments from int8 rows
+    # (N <= 128), 256-row planes GEMM (C-BSG)
+    (290, 300, 0), (100, 300, 0), (290, 100, 0), (290, 300, 1),
+]
+
+
+@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
+@pytest.mark.parametrize("polarity", [0, 1])
+@pytest.mark.parametrize("shape", INT8_MIN_SHAPES, ids=[str(x) for x in INT8_MIN_SHAPES])
+def test_int8_min(dev, oracle_mod, shape, polarity, engine):
+    # -128 lies outside the documented [-127, 127] but has the comparator boundaries of
+    # -127 in both polarities (a unipolar magnitude boundary past 256: a one on every
+    # cycle); every path must match the oracle on it, rows that end early included
+    M, N, rng_kind = shape
+    seed = 81 + 2 * polarity + rng_kind
+    rng = np.random.default_rng(seed)
+    g = W.random_gemm(rng, 1, M, N, 70, 80, polarity, seed)
+    g.A[0, ::5, ::3] = -128
+    g.B[0, ::7, 1::4] = -128
+    _note("int8 minimum %s polarity %d engine %d" % (shape, polarity, engine))
+    out, cnt = _run(g, dev, rng=rng_kind, engine=engine)
+    _compare(g, 0, np.arange(M), np.arange(N), out, cnt, oracle_mod, "int8min %s pol%d" % (shape, polarity),
+             rng=rng_kind)
+
+
+# --------------------------------------------------------------------------
 # full-size workloads: sampled rows x columns against the oracle
 # --------------------------------------------------------------------------
 def _sample(n, rng, k):
