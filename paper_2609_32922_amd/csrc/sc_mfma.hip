@@ -1286,34 +1286,99 @@ constexpr int RCH = 32;          // elements per chunk, cycles per group
 constexpr int RREP = 8;          // copies of each table entry (16-byte reads spread over the banks)
 constexpr int RPAD = 0x80;       // chunk byte of a padding element or row: the table gives zero
 
-// chunks of one operand: thread = (row r of the tile order, element e of chunk c)
-__global__ __launch_bounds__(256) void k_rchunks(const int8_t *X, int64_t ld, int64_t strideX, int rows, int K,
-                                                 int KC, size_t stride_batch, size_t off_perm, int permuted,
-                                                 size_t off_out, uint8_t *ws) {
-    const int b = blockIdx.z, c = blockIdx.y;
-    const int r = blockIdx.x * 8 + (threadIdx.x >> 5), e = threadIdx.x & 31;
-    uint8_t *wsb = ws + (size_t)b * stride_batch;
-    const int src = permuted ? ws_ptr<int32_t>(wsb, off_perm)[r] : (r < rows ? r : -1);
-    const int d = c * RCH + e;
-    int v = -RPAD;
-    if (src >= 0 && d < K) {
-        v = X[(size_t)b * strideX + (size_t)src * ld + d];
-        v = v < -127 ? -127 : v;
+// bytes equal to 0x80 (-128) become 0x81 (-127): same comparator boundaries, and 0x80 stays
+// free to mark padding
+__device__ __forceinline__ uint32_t r_clamp4(uint32_t x) {
+    const uint32_t t = x ^ 0x80808080u;                                      // 0 where x was 0x80
+    const uint32_t nz = (((t & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | t) & 0x80808080u;  // 0x80 where t != 0
+    return x | ((~nz & 0x80808080u) >> 7);
+}
+
+struct RChunkArgs {
+    const int8_t *X[2];
+    int64_t ld[2], strideX[2];
+    int rows[2], rows_pad[2], nb[2];
+    size_t stride_batch[2], off_out[2];
+    size_t off_perm;      // side 0 (A) takes its rows in the scheduler's order
+    int K, KC;
+    int vec[2];           // 16-byte loads are aligned (base and row stride multiples of 16)
+};
+
+// Chunks of both operands: thread = (row r of the tile order, half h) of chunk blockIdx.y,
+// side and batch entry from blockIdx.z; each thread copies one 16-byte half.
+__global__ __launch_bounds__(256) void k_rchunks(RChunkArgs a, uint8_t *ws) {
+    const int side = blockIdx.z >= (unsigned)a.nb[0];
+    const int b = side ? blockIdx.z - a.nb[0] : blockIdx.z;
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    const int r = t >> 1, h = t & 1;
+    if (r >= a.rows_pad[side]) return;
+    uint8_t *wsb = ws + (size_t)b * a.stride_batch[side];
+    const int src = side == 0 ? ws_ptr<int32_t>(wsb, a.off_perm)[r] : (r < a.rows[side] ? r : -1);
+    const int8_t *xrow = src >= 0 ? a.X[side] + (size_t)b * a.strideX[side] + (size_t)src * a.ld[side] : nullptr;
+    u4 *out = reinterpret_cast<u4 *>(ws_ptr<uint8_t>(wsb, a.off_out[side])) + (size_t)(r >> 8) * a.KC * 512 +
+              (r & 255) * 2 + h;
+    {
+        const int c = blockIdx.y;
+        const int d0 = c * RCH + 16 * h;
+        u4 v = u4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
+        if (xrow != nullptr && d0 < a.K) {
+            if (a.vec[side] && d0 + 16 <= a.K) {
+                v = *reinterpret_cast<const u4 *>(xrow + d0);
+            } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    uint32_t w = 0;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int d = d0 + 4 * k + j;
+                        w |= (uint32_t)(d < a.K ? (uint8_t)xrow[d] : (uint8_t)RPAD) << (8 * j);
+                    }
+                    v[k] = w;
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = r_clamp4(v[k]);
+            if (d0 + 16 > a.K) {          // the elements past K keep the padding byte
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (d0 + 4 * k + j >= a.K) v[k] = (v[k] & ~(0xFFu << (8 * j))) | ((uint32_t)RPAD << (8 * j));
+            }
+        }
+        out[(size_t)c * 512] = v;
     }
-    ws_ptr<uint8_t>(wsb, off_out)[(((size_t)(r >> 8) * KC + c) * 256 + (r & 255)) * RCH + e] = (uint8_t)v;
 }
 
 hipError_t launch_rchunks(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
                           uint8_t *ws, hipStream_t st) {
     if (lay.KC == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_rchunks, dim3((unsigned)(lay.MT * BM / 8), (unsigned)lay.KC, (unsigned)d.batch),
-                       dim3(256), 0, st, A, d.lda, d.strideA, d.M, d.K, lay.KC, lay.stride_batchA,
-                       lay.off_perm, 1, lay.off_Ap, ws);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_rchunks, dim3((unsigned)(lay.NT * BN / 8), (unsigned)lay.KC, (unsigned)lay.nbB),
-                       dim3(256), 0, st, B, d.ldb, d.strideB, d.N, d.K, lay.KC, lay.stride_batchB,
-                       (size_t)0, 0, lay.off_Bp, ws);
+    RChunkArgs a{};
+    a.X[0] = A;
+    a.X[1] = B;
+    a.ld[0] = d.lda;
+    a.ld[1] = d.ldb;
+    a.strideX[0] = d.strideA;
+    a.strideX[1] = d.strideB;
+    a.rows[0] = d.M;
+    a.rows[1] = d.N;
+    a.rows_pad[0] = lay.MT * BM;
+    a.rows_pad[1] = lay.NT * BN;
+    a.nb[0] = d.batch;
+    a.nb[1] = lay.nbB;
+    a.stride_batch[0] = lay.stride_batchA;
+    a.stride_batch[1] = lay.stride_batchB;
+    a.off_out[0] = lay.off_Ap;
+    a.off_out[1] = lay.off_Bp;
+    a.off_perm = lay.off_perm;
+    a.K = d.K;
+    a.KC = lay.KC;
+    a.vec[0] = (reinterpret_cast<uintptr_t>(A) % 16 == 0) && d.lda % 16 == 0 && d.strideA % 16 == 0;
+    a.vec[1] = (reinterpret_cast<uintptr_t>(B) % 16 == 0) && d.ldb % 16 == 0 && d.strideB % 16 == 0;
+    const int rows = a.rows_pad[0] > a.rows_pad[1] ? a.rows_pad[0] : a.rows_pad[1];
+    hipLaunchKernelGGL(k_rchunks, dim3((unsigned)((2 * rows + 255) / 256), (unsigned)lay.KC,
+                                       (unsigned)(d.batch + lay.nbB)),
+                       dim3(256), 0, st, a, ws);
     return hipGetLastError();
 }
 

@@ -241,9 +241,9 @@ def test_rgen_full_compare(dev, oracle_mod, case):
 
 
 INT8_MIN_SHAPES = [
-    # M, N, rng: int8-chunk GEMM, 128-row planes GEMM (M <= 128), fragments from int8 rows
-    # (N <= 128), 256-row planes GEMM (C-BSG)
-    (290, 300, 0), (100, 300, 0), (290, 100, 0), (290, 300, 1),
+    # M, N, K, rng: int8-chunk GEMM (rows copied bytewise, then 16 bytes at a time), 128-row
+    # planes GEMM (M <= 128), fragments from int8 rows (N <= 128), 256-row planes GEMM (C-BSG)
+    (290, 300, 70, 0), (290, 300, 96, 0), (100, 300, 70, 0), (290, 100, 70, 0), (290, 300, 70, 1),
 ]
 
 
@@ -254,10 +254,10 @@ def test_int8_min(dev, oracle_mod, shape, polarity, engine):
     # -128 lies outside the documented [-127, 127] but has the comparator boundaries of
     # -127 in both polarities (a unipolar magnitude boundary past 256: a one on every
     # cycle); every path must match the oracle on it, rows that end early included
-    M, N, rng_kind = shape
+    M, N, K, rng_kind = shape
     seed = 81 + 2 * polarity + rng_kind
     rng = np.random.default_rng(seed)
-    g = W.random_gemm(rng, 1, M, N, 70, 80, polarity, seed)
+    g = W.random_gemm(rng, 1, M, N, K, 80, polarity, seed)
     g.A[0, ::5, ::3] = -128
     g.B[0, ::7, 1::4] = -128
     _note("int8 minimum %s polarity %d engine %d" % (shape, polarity, engine))
