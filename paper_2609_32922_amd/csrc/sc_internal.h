@@ -4,7 +4,9 @@
 //
 //   status     one uint32 (bit 0: some L_i out of range), then one uint32: the longest
 //              tile-pair cycle count of the call (256-row MFMA GEMM), then one uint32: nonzero
-//              when some L_i is not a multiple of 32; all cleared by k_draws
+//              when some 256-row pair holds more than RSLOTS distinct lengths that are not
+//              multiples of 32 (the int8-chunk GEMM then masks its fragments); all cleared by
+//              k_draws
 //   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
 //   CA         C-BSG only: CA[L][beta] = #{l < L : rA_l < beta}, uint16 [L_max+1][257]
 //   per batch entry b of A (batch entries):
@@ -86,6 +88,7 @@ __host__ __device__ inline double quad_split_time(int64_t tiles, int s, double p
     return (load > maxT / s ? load : maxT / s) + red;
 }
 constexpr int OCH = 8;           // octets per block of the nibble-plane generator
+constexpr int RSLOTS = 4;        // int8-chunk GEMM: tables masked to a row length, per cycle group
 constexpr int64_t MFMA_EXACT = 1ll << 24;   // K * L_max bound for exact fp32 counts
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }

@@ -102,7 +102,7 @@ __global__ __launch_bounds__(256) void k_draws(uint64_t seed, int rng, int n, ui
     if (status != nullptr && l == 0 && blockIdx.y == 0) {
         status[0] = 0u;
         status[1] = 0u;   // longest tile pair of the call
-        status[2] = 0u;   // some row length is not a multiple of 32
+        status[2] = 0u;   // some row pair holds more than RSLOTS lengths inside a cycle group
     }
     if (l >= n) return;
     const uint64_t h = splitmix64(2ull * seed + (uint64_t)op);
@@ -251,7 +251,6 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 
     for (int v = tid; v <= L_max; v += 1024) hist[v] = 0;
     __syncthreads();
-    bool ragged = false;
     for (int i0 = 0; i0 < M; i0 += 1024) {
         const int i = i0 + tid;
         int l = i < M ? Lb[i] : 0;
@@ -259,10 +258,9 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
             atomicOr(status, STATUS_BAD_LENGTH);
             l = 0;
         }
-        ragged = ragged || (l % 32) != 0;
         wave_bucket_add(hist, l, i < M);
     }
-    if (__syncthreads_or(ragged) && tid == 0) atomicOr(status + 2, 1u);
+    __syncthreads();
     // start position of each length bucket, longest lengths first
     int64_t carry = 0;
     for (int c = 0; c <= L_max; c += 1024) {
@@ -310,6 +308,25 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     }
     // the first tile pair holds the batch entry's longest rows
     if (tid == 0 && lay.mbm == 2 * BM) atomicMax(status + 1, (uint32_t)tileL[0]);
+    // The int8-chunk GEMM keeps, per cycle group, a table of A masked to each row length
+    // that ends inside the group: RSLOTS of them.  Rows are sorted, so the distinct lengths
+    // of a pair are the first rows of runs of equal length; a pair with more such lengths
+    // that are not multiples of 32 than tables makes the GEMM mask its fragments instead.
+    if (lay.rgen) {
+        __shared__ int fresh[4];
+        for (int q0 = 0; q0 < lay.MT / 2; q0 += 4) {
+            __syncthreads();
+            if (tid < 4) fresh[tid] = 0;
+            __syncthreads();
+            const int p = q0 * 256 + tid;
+            if (p < lay.MT * BM) {
+                const int l = Ls[p];
+                if (l % 32 != 0 && ((p & 255) == 0 || Ls[p - 1] != l)) atomicAdd(&fresh[tid >> 8], 1);
+            }
+            __syncthreads();
+            if (tid < 4 && fresh[tid] > RSLOTS) atomicOr(status + 2, 1u);
+        }
+    }
 }
 
 hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L, uint8_t *ws,

@@ -1285,6 +1285,9 @@ static hipError_t launch_qgemm(const MGemmArgs &g, const Layout &lay, uint8_t *w
 constexpr int RCH = 32;          // elements per chunk, cycles per group
 constexpr int RREP = 8;          // copies of each table entry (16-byte reads spread over the banks)
 constexpr int RPAD = 0x80;       // chunk byte of a padding element or row: the table gives zero
+constexpr int RREP1 = 4;         // copies of each masked table entry
+constexpr int RGROUPS = SC_L_MAX_LIMIT / RCH;
+static_assert(RSLOTS * RREP1 == 16, "the masked tables fill one 256-byte row per byte value");
 
 // bytes equal to 0x80 (-128) become 0x81 (-127): same comparator boundaries, and 0x80 stays
 // free to mark padding
@@ -1397,9 +1400,13 @@ __device__ __forceinline__ u4 r_len_mask(int L, int G) {
 // Table of cycle group G: entry (byte, operand) holds the 32 nibbles of cycles 32G .. 32G+31
 // (cycle 32G + k at bits 4 (k % 8) of dword k / 8), sign folded in (unipolar), zero for the
 // padding byte.  Entry copies are laid out [byte][operand][copy], so a read's byte
-// address is byte * 256 + operand * 128 + copy * 16.
+// address is byte * 256 + operand * 128 + copy * 16.  A second region (from byte 65536)
+// holds, for the k-th length set in `rems` (bit r: a row of the pair ends r cycles into the
+// group), A's entries masked to that length: [byte][k][copy], address 65536 + byte * 256 +
+// (k * RREP1 + copy) * 16.
 template <bool BIP>
-__device__ __forceinline__ void r_build_lut(u4 *lut, const uint32_t *rA, const uint32_t *rB, int G, int tid) {
+__device__ __forceinline__ void r_build_lut(u4 *lut, const uint32_t *rA, const uint32_t *rB, int G, int tid,
+                                            uint32_t rems) {
     const uint32_t zero_nib = BIP ? NIB_NEG : 0u;
     const int byte = tid;
     const int q = (int)(int8_t)(uint8_t)byte;
@@ -1419,6 +1426,14 @@ __device__ __forceinline__ void r_build_lut(u4 *lut, const uint32_t *rA, const u
         }
 #pragma unroll
         for (int k = 0; k < RREP; ++k) lut[byte * 16 + side * RREP + k] = x;
+        if (side == 0) {
+            int k = 0;
+            for (uint32_t m = rems; m != 0u; m &= m - 1u, ++k) {
+                const u4 xm = x & r_len_mask(__builtin_ctz(m), 0);
+#pragma unroll
+                for (int c = 0; c < RREP1; ++c) lut[256 * 16 + byte * 16 + k * RREP1 + c] = xm;
+            }
+        }
     }
 }
 
@@ -1428,7 +1443,7 @@ struct RData {
 struct RSrc {
     __amdgpu_buffer_rsrc_t a, b;   // the pair's A chunks and the B pair's chunks
     int voffA, voffB;              // the lane's row and half within a chunk
-    uint32_t loA, loB;             // the lane's table copies of A and B (low address byte)
+    uint32_t loA[4], loB;          // table rows of the lane's A rows (copy, region) and of B
     const char *lut;
     int KC;
 };
@@ -1449,10 +1464,10 @@ __device__ __forceinline__ void r_finish(RData &d, const bool (&fin)[4]) {
 }
 
 // the table row of element E (0..15) of a lane's 16: address byte 1 = the element's byte,
-// byte 0 = the copy (from lo)
+// bytes 0 and 2 = the copy and the region (from lo)
 template <int E>
 __device__ __forceinline__ u4 r_look(const RSrc &q, uint32_t word, uint32_t lo) {
-    constexpr uint32_t sel = 0x0C0C0000u | ((4u + (E & 3)) << 8);
+    constexpr uint32_t sel = 0x0C020000u | ((4u + (E & 3)) << 8);
     return *reinterpret_cast<const u4 *>(q.lut + __builtin_amdgcn_perm(word, lo, sel));
 }
 template <int E>
@@ -1467,7 +1482,7 @@ __device__ __forceinline__ void r_frags(const RSrc &q, const RData &d, const u4 
     for (int c = 0; c < 4; ++c) f.b[c] = r_look<E>(q, r_word<E>(d.b[c]), q.loB);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        f.a[i] = r_look<E>(q, r_word<E>(d.a[i]), q.loA);
+        f.a[i] = r_look<E>(q, r_word<E>(d.a[i]), q.loA[i]);
         if (MASK) f.a[i] &= m[i];
     }
 }
@@ -1529,14 +1544,15 @@ __device__ __forceinline__ void r_chunks(const RSrc &q, int c, int ce, RData &cu
 }
 
 // One work unit, as in k_qgemm: tile `tile` over chunk steps [s, s + 1) / S of the pair's
-// (group, chunk) steps, whole tiles decoded here, parts stored as partial sums.  Both
-// variants are launched and one returns at once: MASK runs when some row length of the
-// call is not a multiple of 32 (a row ends inside a cycle group, so every A fragment is
-// masked with its row's length), the other when all are (rows that have ended read the
-// padding byte, whose table row is zero, and nothing else is masked).
+// (group, chunk) steps, whole tiles decoded here, parts stored as partial sums.  Rows that
+// have ended read the padding byte, whose table row is zero; a row that ends inside a
+// cycle group reads there the table masked to its length.  Both variants are launched and
+// one returns at once: MASK runs when some row pair holds more lengths inside a group than
+// there are masked tables (then every A fragment is masked with its row's length instead).
 template <bool BIP, bool MASK>
 __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
-    __shared__ u4 lut[256 * 2 * RREP];     // 64 KB; the epilogue's transpose reuses it
+    __shared__ u4 lut[(MASK ? 1 : 2) * 256 * 16];   // 64 or 128 KB; the epilogue's transpose reuses it
+    __shared__ uint32_t rems[MASK ? 1 : RGROUPS];     // bit r of rems[G]: a row ends r cycles into group G
     if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
     const int NTW = lay.NT / 2;
     int F, SS;
@@ -1563,6 +1579,13 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
     const int64_t nch = (int64_t)ngroups * g.KC;
     const int64_t x0 = (int64_t)s * nch / S, x1 = (int64_t)(s + 1) * nch / S;
 
+    if (!MASK) {
+        if (tid < ngroups) rems[tid] = 0u;
+        __syncthreads();
+        const int Lt = perm[tid] >= 0 ? Ls[tid] : 0;
+        if (Lt % RCH != 0) atomicOr(&rems[Lt / RCH], 1u << (Lt % RCH));
+        __syncthreads();
+    }
     // the lane's A rows' lengths (padding rows: never end)
     int Lr[4];
 #pragma unroll
@@ -1579,8 +1602,8 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
                                             0x00020000);
     q.voffA = (wr + i32) * RCH + grp * 16;
     q.voffB = (wc + i32) * RCH + grp * 16;
-    q.loA = 16u * (uint32_t)(lane & (RREP - 1));
-    q.loB = q.loA + 16u * RREP;
+    const uint32_t lrep = 16u * (uint32_t)(lane & (RREP - 1));
+    q.loB = lrep + 16u * RREP;
     q.lut = reinterpret_cast<const char *>(lut);
     q.KC = g.KC > 0 ? g.KC : 1;
     const uint32_t *rA = ws_ptr<uint32_t>(ws, lay.off_rA), *rB = ws_ptr<uint32_t>(ws, lay.off_rB);
@@ -1598,16 +1621,25 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
     for (int64_t x = x0; x < x1;) {
         const int G = (int)(x / g.KC);
         const int64_t xe = min(x1, (int64_t)(G + 1) * g.KC);
+        const uint32_t rm = MASK ? 0u : rems[G];
         // every read of the previous group's table is done before it is replaced
         __syncthreads();
-        r_build_lut<BIP>(lut, rA, rB, G, tid);
+        r_build_lut<BIP>(lut, rA, rB, G, tid, rm);
         __syncthreads();
-        // length masks of the lane's A rows, or which of them have ended
+        // the lane's A rows: ended, ending inside this group (the masked table of the
+        // length's rank among the group's lengths; with MASK a mask instead) or running on
         bool fin[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            if (MASK) m[i] = r_len_mask(Lr[i], G);
-            fin[i] = Lr[i] <= RCH * G;
+            const int rem = Lr[i] - RCH * G;
+            fin[i] = rem <= 0;
+            q.loA[i] = lrep;
+            if (MASK) {
+                m[i] = r_len_mask(Lr[i], G);
+            } else if (rem > 0 && rem < RCH) {
+                const uint32_t k = (uint32_t)__popc(rm & ((1u << rem) - 1u));
+                q.loA[i] = 0x10000u | (16u * (k * RREP1 + (uint32_t)(lane & (RREP1 - 1))));
+            }
         }
         if (!MASK) r_finish(cur, fin);
         r_frags<0, MASK>(q, cur, m, f[0]);
@@ -1630,7 +1662,7 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
         // transpose through LDS, 32 rows at a time, so that each thread decodes four
         // adjacent columns of one row
         constexpr int TS = 256 + 4, TR = 32;
-        static_assert(TR * TS * 4 <= (int)sizeof(lut), "the epilogue transpose must fit the table");
+        static_assert(TR * TS * 4 <= 256 * 16 * 16, "the epilogue transpose must fit the table");
         int32_t *T = reinterpret_cast<int32_t *>(lut);
         for (int h = 0; h < 256 / TR; ++h) {
             __syncthreads();

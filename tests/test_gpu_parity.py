@@ -240,6 +240,29 @@ def test_rgen_full_compare(dev, oracle_mod, case):
         _compare(g, b, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "rgen%s b%d" % (case, b))
 
 
+LADDERS = [
+    # lengths a row pair may hold: a ladder as the length policy gives (lengths inside a
+    # cycle group read tables masked to them), exactly as many such lengths in one pair as
+    # there are masked tables, and one more (the call then masks every fragment)
+    ("ladder", [0, 5, 24, 48, 96, 192], 192),
+    ("four", [40, 41, 42, 43], 64),
+    ("five", [40, 41, 42, 43, 44], 64),
+]
+
+
+@pytest.mark.parametrize("polarity", [0, 1])
+@pytest.mark.parametrize("case", LADDERS, ids=[c[0] for c in LADDERS])
+def test_rgen_length_ladders(dev, oracle_mod, case, polarity):
+    name, lengths, L_max = case
+    rng = np.random.default_rng(91 + polarity)
+    g = W.random_gemm(rng, 2, 300, 260, 40, L_max, polarity, 91 + polarity)
+    g.L = rng.choice(np.array(lengths, np.int32), g.L.shape).astype(np.int32)
+    _note("length ladder %s polarity %d" % (name, polarity))
+    out, cnt = _run(g, dev, engine=2)
+    for b in range(g.batch):
+        _compare(g, b, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "ladder %s pol%d b%d" % (name, polarity, b))
+
+
 INT8_MIN_SHAPES = [
     # M, N, K, rng: int8-chunk GEMM (rows copied bytewise, then 16 bytes at a time), 128-row
     # planes GEMM (M <= 128), fragments from int8 rows (N <= 128), 256-row planes GEMM (C-BSG)
