@@ -17,16 +17,25 @@
 //   k_mplanes     nibble planes of A (sorted rows, per-row lengths) or B, one block per
 //                 128-row tile x 64 cycles x 64 elements; element parameters and an
 //                 8-cycle lookup table in LDS, 16-byte stores, 1 KB per wave; with
-//                 comparator streams both operands in one launch (k_mplanes2)
+//                 comparator streams (M <= 128) both operands in one launch (k_mplanes2)
 //   k_fgemm       N <= 128 with comparator streams: 128x128 tile, the fp4 fragments of
 //                 both operands built in LDS from the int8 rows (an 8-cycle table per
 //                 octet indexed by the int8 byte), so no planes are written or read
-//   k_qgemm       256x256 output tile per 256-thread block, one block per CU, 128x128
-//                 per wave as 4x4 32x32 MFMA blocks, three LDS buffers of 4 slots (96 KB),
-//                 memory instructions interleaved one per MFMA; taken when N > 128 and
-//                 M > 128.  Whole tiles in full rounds, the tiles of a last partial round
-//                 (or every tile, when row lengths vary) split along k.
-//   k_qgemm_reduce sums the partial counts of its split tiles and decodes
+//   k_rchunks     int8 operands (A in the scheduler's row order) laid out in 32-element
+//                 chunks per 256-row pair, the input of k_rgemm
+//   k_rgemm       N > 128 and M > 128 with comparator streams: the tiles and division of
+//                 k_qgemm, but every fp4 fragment is one LDS table read (a table per
+//                 32-cycle group indexed by the int8 byte), so no planes exist and the
+//                 loop has no stage buffers; rows ending inside a group read tables masked
+//                 to their length (a second variant masks every fragment when a row pair
+//                 holds too many such lengths)
+//   k_qgemm       N > 128 and M > 128 with C-BSG streams: 256x256 output tile per
+//                 256-thread block, one block per CU, 128x128 per wave as 4x4 32x32 MFMA
+//                 blocks, three LDS buffers of 4 slots (96 KB), memory instructions
+//                 interleaved one per MFMA.  Whole tiles in full rounds, the tiles of a last
+//                 partial round (or every tile, when row lengths vary) split along k.
+//   k_qgemm_reduce sums the partial counts of the split tiles of k_qgemm or k_rgemm and
+//                 decodes
 //   k_mgemm       the rest (M <= 128, or N <= 128 with C-BSG streams): 128x256 output
 //                 tile per 256-thread block (128x128 and 64x64 when N <= 128), 64x128 per
 //                 wave as 2x4 32x32 MFMA blocks, 4 slots (2 MFMA k-steps of 64) per LDS
