@@ -1484,6 +1484,16 @@ __device__ __forceinline__ uint32_t r_word(const u4 &v) {
     return v[E >> 2];
 }
 
+// the MFMAs of A blocks 2h, 2h + 1 with every B block
+__device__ __forceinline__ void q_mma_half(v16f (&acc)[4][4], const QFrags &f, int h) {
+#pragma unroll
+    for (int i = 2 * h; i < 2 * h + 2; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            acc[i][c] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(frag(f.a[i]), frag(f.b[c]),
+                                                                        acc[i][c], 4, 4, 0, 127, 0, 127);
+}
+
 // fragments of k-step E (element E of the lane's 16) from chunk data d
 template <int E, bool MASK>
 __device__ __forceinline__ void r_frags(const RSrc &q, const RData &d, const u4 (&m)[4], QFrags &f) {
@@ -1500,36 +1510,56 @@ __device__ __forceinline__ void r_frags(const RSrc &q, const RData &d, const u4 
 // next k-step (2S + 2, or the next chunk's first) on exit; stage 0 loads the next chunk.
 // MASK: the A fragments are masked with the rows' lengths (some row of the pair ends
 // inside a cycle group); else rows that have ended read the padding byte (r_finish).
+__device__ __forceinline__ void r_mask(const u4 (&m)[4], QFrags &f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f.a[i] &= m[i];
+}
+
+template <bool LOADS>
+__device__ __forceinline__ void r_quarter_reads() {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);   // VALU (address)
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+        if (LOADS) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global load
+    }
+    __builtin_amdgcn_sched_barrier(0);
+}
+template <bool MASK>
+__device__ __forceinline__ void r_quarter_masks() {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (MASK) __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // masks
+    }
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Stage S in four quarters of 8 MFMAs: the table reads of the next fragments go with the
+// first quarter of each k-step, their length masks (MASK) with the second, once the reads
+// have landed, so no AND waits on a read in the in-order issue
 template <int S, bool MASK>
 __device__ __forceinline__ void r_stage(const RSrc &q, int cnext, RData &cur, RData &nxt, const u4 (&m)[4],
                                         const bool (&fin)[4], v16f (&acc)[4][4], QFrags (&f)[2]) {
     if (S == 0) r_load(q, cnext, nxt);
-    r_frags<2 * S + 1, MASK>(q, cur, m, f[1]);
-    q_mma(acc, f[0]);
+    r_frags<2 * S + 1, false>(q, cur, m, f[1]);
+    q_mma_half(acc, f[0], 0);
+    r_quarter_reads<S == 0>();
+    if (MASK) r_mask(m, f[1]);
+    q_mma_half(acc, f[0], 1);
+    r_quarter_masks<MASK>();
     if (S < 7) {
-        r_frags<2 * S + 2, MASK>(q, cur, m, f[0]);
+        r_frags<2 * S + 2, false>(q, cur, m, f[0]);
     } else {
         if (!MASK) r_finish(nxt, fin);
-        r_frags<0, MASK>(q, nxt, m, f[0]);
+        r_frags<0, false>(q, nxt, m, f[0]);
     }
-    q_mma(acc, f[1]);
-    // each half: the 8 table reads of the next fragments (with their address bytes, and
-    // the masks) in the first 8 MFMAs; the chunk loads go with the first half of stage 0
-    constexpr int NV = MASK ? 3 : 1;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, NV, 0);  // VALU
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
-        }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            if (S == 0 && h == 0) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global load
-        }
-    }
+    q_mma_half(acc, f[1], 0);
+    r_quarter_reads<false>();
+    if (MASK) r_mask(m, f[0]);
+    q_mma_half(acc, f[1], 1);
+    r_quarter_masks<MASK>();
 }
 
 // chunks c .. ce-1 of one cycle group; on exit cur holds the chunk after them (chunk ce, or
