@@ -313,18 +313,36 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     // of a pair are the first rows of runs of equal length; a pair with more such lengths
     // that are not multiples of 32 than tables makes the GEMM mask its fragments instead.
     if (lay.rgen) {
-        __shared__ int fresh[4];
-        for (int q0 = 0; q0 < lay.MT / 2; q0 += 4) {
+        // After the scatter hist[l] is the end of length l's run of sorted positions, and the
+        // run starts where the run of l + 1 ends.  Each length that is not a multiple of 32
+        // adds one to every pair its run meets (a difference array over pairs, then a scan).
+        const int npairs = lay.MT / 2;
+        __shared__ int dpair[2048 + 1];
+        for (int q0 = 0; q0 < npairs; q0 += 2048) {
+            const int nq = min(npairs - q0, 2048);
             __syncthreads();
-            if (tid < 4) fresh[tid] = 0;
+            for (int q = tid; q <= nq; q += 1024) dpair[q] = 0;
             __syncthreads();
-            const int p = q0 * 256 + tid;
-            if (p < lay.MT * BM) {
-                const int l = Ls[p];
-                if (l % 32 != 0 && ((p & 255) == 0 || Ls[p - 1] != l)) atomicAdd(&fresh[tid >> 8], 1);
+            for (int l = tid; l <= L_max; l += 1024) {
+                const int end = hist[l], start = l == L_max ? 0 : hist[l + 1];
+                if (l % 32 == 0 || end <= start) continue;
+                const int qa = max(start >> 8, q0), qb = min((end - 1) >> 8, q0 + nq - 1);
+                if (qa > qb) continue;
+                atomicAdd(&dpair[qa - q0], 1);
+                atomicAdd(&dpair[qb + 1 - q0], -1);
             }
             __syncthreads();
-            if (tid < 4 && fresh[tid] > RSLOTS) atomicOr(status + 2, 1u);
+            int64_t carry = 0;
+            bool over = false;
+            for (int c = 0; c < nq; c += 1024) {
+                const int q = c + tid;
+                int64_t tot;
+                const int64_t v = q < nq ? dpair[q] : 0;
+                const int64_t ex = block_excl_scan_1024(v, &tot);
+                over = over || (q < nq && carry + ex + v > RSLOTS);
+                carry += tot;
+            }
+            if (__syncthreads_or(over) && tid == 0) atomicOr(status + 2, 1u);
         }
     }
 }
