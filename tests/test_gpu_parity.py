@@ -383,6 +383,54 @@ def test_strided_interleaved_heads(dev, oracle_mod):
         assert np.max(np.abs(oo[nz] - o_ref[nz]) / np.abs(o_ref[nz])) <= 1e-6
 
 
+@pytest.mark.parametrize("polarity", [0, 1])
+def test_rgen_strided(dev, oracle_mod, polarity):
+    """The int8-chunk GEMM on strided operands: A rows padded to a multiple of 16 bytes
+    (16-byte chunk loads), B rows at an odd stride (bytewise), a wider output row stride,
+    two batch entries with their own strides."""
+    import torch
+    import paper_2609_32922_amd as scg
+    rng = np.random.default_rng(71 + polarity)
+    batch, M, N, K, L_max = 2, 270, 300, 96, 80
+    lda, ldb, ldo = 128, 97, N + 8
+    sA_, sB_, sO_ = M * lda + 32, N * ldb + 5, M * ldo + 4
+    Abuf = rng.integers(-127, 128, batch * sA_).astype(np.int8)
+    Bbuf = rng.integers(-127, 128, batch * sB_).astype(np.int8)
+    sa = rng.uniform(0.001, 0.05, (batch, M)).astype(np.float32)
+    sb = rng.uniform(0.001, 0.05, (batch, N)).astype(np.float32)
+    L = rng.integers(0, L_max + 1, (batch, M)).astype(np.int32)
+    L[0, :] = (L[0, :] // 32) * 32            # entry 0: lengths at group bounds
+    d = scg.ScGemmDesc()
+    d.batch, d.M, d.N, d.K = batch, M, N, K
+    d.lda, d.ldb, d.ldo = lda, ldb, ldo
+    d.strideA, d.strideB, d.strideO = sA_, sB_, sO_
+    d.strideSA, d.strideSB, d.strideL = M, N, M
+    d.L_max, d.polarity, d.rng, d.L_hint, d.seed = L_max, polarity, 0, 0, 171
+    d.engine = 2
+    tA, tB, tsa, tsb, tL = (torch.from_numpy(a).to(dev) for a in (Abuf, Bbuf, sa, sb, L))
+    out = torch.zeros(batch * sO_, dtype=torch.float32, device=dev)
+    cnt = torch.zeros(batch * sO_, dtype=torch.int32, device=dev)
+    ws = scg.Workspace(scg.sc_gemm_workspace_size(d), dev)
+    _note("int8-chunk GEMM strided polarity %d" % polarity)
+    sh = int(torch.cuda.current_stream().cuda_stream)
+    rc = scg.sc_gemm(d, tA.data_ptr(), tsa.data_ptr(), tB.data_ptr(), tsb.data_ptr(), tL.data_ptr(),
+                     out.data_ptr(), cnt.data_ptr(), ws.ptr, ws.nbytes, sh)
+    assert rc == 0 and scg.sc_gemm_status(ws.ptr, sh) == 0
+    c, o = cnt.cpu().numpy(), out.cpu().numpy()
+    for b in range(batch):
+        A = np.stack([Abuf[b * sA_ + i * lda: b * sA_ + i * lda + K] for i in range(M)])
+        B = np.stack([Bbuf[b * sB_ + j * ldb: b * sB_ + j * ldb + K] for j in range(N)])
+        c_ref, o_ref = oracle_mod.sc_gemm(A, B, sa[b], sb[b], L[b], L_max, polarity, 171)
+        cg = np.stack([c[b * sO_ + i * ldo: b * sO_ + i * ldo + N] for i in range(M)])
+        og = np.stack([o[b * sO_ + i * ldo: b * sO_ + i * ldo + N] for i in range(M)]).astype(np.float64)
+        assert np.array_equal(cg, c_ref), b
+        nz = o_ref != 0
+        assert np.all(og[~nz] == 0)
+        assert np.max(np.abs(og[nz] - o_ref[nz]) / np.abs(o_ref[nz])) <= 1e-6
+        # the padding between rows and entries is left untouched
+        assert np.all(c[b * sO_ + M * ldo - 8: b * sO_ + M * ldo] == 0) or ldo == N
+
+
 # --------------------------------------------------------------------------
 # Sobol-8 sequences with conditional generation of B's stream (C-BSG)
 # --------------------------------------------------------------------------
