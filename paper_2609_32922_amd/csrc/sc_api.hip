@@ -36,7 +36,10 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.words_per_L = mfma ? (int64_t)l.KQP * 64 : (int64_t)l.KB * BM;
     l.MT = (d.M + BM - 1) / BM;
     l.NT = (d.N + BN - 1) / BN;
-    l.mbn = l.NT > 1 ? 2 * BN : BN;
+    // N <= 64 with comparator streams and M > 128: the int8-chunk GEMM in blocks of
+    // 256 rows x 64 columns (the B side still laid out as one 256-row pair)
+    l.narrow = mfma && d.rng == SC_RNG_LFSR32 && d.N <= 64 && d.M > BM;
+    l.mbn = (l.NT > 1 || l.narrow) ? 2 * BN : BN;
     if (mfma) l.NT = (int)round_up(l.NT, l.mbn / BN);
     // N <= 128 (one B tile): every A plane would be used once, so the GEMM generates the
     // fragments itself (comparator streams; operand offsets must fit 31 bits)
@@ -47,6 +50,7 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     // 256 x 256 blocks with comparator streams: fragments from int8 chunks and a table of
     // each 32-cycle group, so the operands are read as bytes instead of fp4 planes
     l.rgen = l.mbm == 2 * BM && d.rng == SC_RNG_LFSR32;
+    l.rslots = l.narrow ? 0 : RSLOTS;
     l.KC = (d.K + 31) / 32;
     l.LBS = (int)round_up(d.L_max, LCH);
     l.LP = (int)round_up(d.L_max, LSTEP);
@@ -135,13 +139,15 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
         // F = 0 the GEMM kernels may lower s again with the actual longest tile pair
         // (measured: 6304 x 768 x 3072 with L in [16, 256], mean 64, longest 172: the GEMM
         // takes 0.49 ms split two ways against 0.61 ms three ways).
-        l.q_perL = (double)l.mbm * l.mbn * 4.0 * l.KQP / MFMA_QUAD_RATE;
+        // (the 64-column blocks of N <= 64 do a quarter of the work and run two per CU)
+        l.q_perL = (double)l.mbm * (l.narrow ? 64 : l.mbn) * 4.0 * l.KQP / MFMA_QUAD_RATE;
+        l.q_slots = l.narrow ? 2 * CUS : CUS;
         l.q_Lmean = Lmean;
         l.q_one = Lmean >= d.L_max;
         const double avgT = l.q_perL * Lmean, maxT = l.q_perL * d.L_max;
         double best = 0.0;
         for (int s = 1; s <= MAX_SPLIT && s <= (kunits > 0 ? kunits : 1); s *= 2) {
-            const double est = quad_split_time(tiles, s, l.q_perL, Lmean, d.L_max, l.q_one != 0);
+            const double est = quad_split_time(tiles, s, l.q_perL, Lmean, d.L_max, l.q_one != 0, l.q_slots);
             if (s == 1 || est < best * 0.97) {
                 best = est;
                 l.S = s;
@@ -149,13 +155,13 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
         }
         // (the tail's split fills the last round as closely as it can: its units are few
         // and short, so balance counts for more there than a shared k-range per XCD)
-        const int64_t R = tiles % CUS;
-        int s2 = R > 0 ? (int)(CUS / R) : 1;
+        const int64_t R = tiles % l.q_slots;
+        int s2 = R > 0 ? (int)(l.q_slots / R) : 1;
         s2 = s2 > MAX_SPLIT ? MAX_SPLIT : s2;
         if (s2 > kunits) s2 = kunits;
-        if (tiles >= CUS && R > 0 && s2 > 1) {
+        if (tiles >= l.q_slots && R > 0 && s2 > 1) {
             const double red = (double)R * (2 * s2) * tile_bytes / PART_BW + 5e-6;
-            const double est = fmax((double)(tiles / CUS) * avgT + avgT / s2, maxT) + red;
+            const double est = fmax((double)(tiles / l.q_slots) * avgT + avgT / s2, maxT) + red;
             if (est < best * 0.97) {
                 best = est;
                 l.F = (int)(tiles - R);

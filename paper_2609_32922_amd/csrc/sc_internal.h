@@ -4,9 +4,9 @@
 //
 //   status     one uint32 (bit 0: some L_i out of range), then one uint32: the longest
 //              tile-pair cycle count of the call (256-row MFMA GEMM), then one uint32: nonzero
-//              when some 256-row pair holds more than RSLOTS distinct lengths that are not
-//              multiples of 32 (the int8-chunk GEMM then masks its fragments); all cleared by
-//              k_draws
+//              when some 256-row pair holds more distinct lengths that are not multiples of
+//              32 than the int8-chunk GEMM has masked tables (rslots; it then masks its
+//              fragments); all cleared by k_draws
 //   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
 //   CA         C-BSG only: CA[L][beta] = #{l < L : rA_l < beta}, uint16 [L_max+1][257]
 //   per batch entry b of A (batch entries):
@@ -74,16 +74,16 @@ constexpr double MFMA_QUAD_RATE = 1.1e13;  // products/s of one 256 x 256 GEMM b
 constexpr double PART_BW = 3e12;           // bytes/s of writing and summing partial sums
 
 // Estimated time of the 256-row GEMM with every tile split s ways (F = 0): the larger of
-// the load per CU and the longest unit, plus writing and summing the partial sums.  With
+// the load per block slot and the longest unit, plus writing and summing the partial sums.  With
 // one row length the units are equal and the load is whole rounds of them; with varying
 // lengths the tiles come longest first, so the blocks fill in behind the long units and
 // the load is the total over the CUs.  The host evaluates it with L_max, the GEMM kernels
 // again with the longest tile pair of the call (both pick the same way among s).
 __host__ __device__ inline double quad_split_time(int64_t tiles, int s, double perL, double Lmean,
-                                                  double Lmax, bool one_length) {
+                                                  double Lmax, bool one_length, int slots) {
     const double avgT = perL * Lmean, maxT = perL * Lmax;
-    const double load = one_length ? (double)((tiles * s + CUS - 1) / CUS) * avgT / s
-                                   : (double)tiles * avgT / CUS;
+    const double load = one_length ? (double)((tiles * s + slots - 1) / slots) * avgT / s
+                                   : (double)tiles * avgT / slots;
     const double red = s > 1 ? (double)tiles * (2 * s) * 256.0 * 256.0 * 4.0 / PART_BW + 5e-6 : 0.0;
     return (load > maxT / s ? load : maxT / s) + red;
 }
@@ -129,6 +129,8 @@ struct Layout {
                        // MT > 1, else 128
     int rgen;          // 256-row GEMM with comparator streams: fragments built in the GEMM
                        // from int8 chunks and a per-group table (no planes)
+    int narrow;        // rgen with N <= 64: blocks of 256 rows x 64 columns
+    int rslots;        // rgen: tables masked to a row length per cycle group (0 when narrow)
     int KC;            // 32-element chunks per row, ceil(K/32)
     int64_t words_per_L;   // plane words of one 128-row tile per cycle of its length
     size_t off_rA, off_rB, off_status, off_CA;
@@ -140,6 +142,7 @@ struct Layout {
     int F;             // 256-row GEMM: tiles 0 .. F-1 run whole, tiles F.. in S parts each
     double q_perL, q_Lmean;   // 256-row GEMM split model: seconds per cycle of one tile, mean L
     int q_one;                // 256-row GEMM split model: all rows have one length
+    int q_slots;              // 256-row GEMM split model: blocks that run at once
     size_t off_part;   // partial counts of split tiles: [split tiles][S][tile rows][tile columns]
     size_t total;
 };

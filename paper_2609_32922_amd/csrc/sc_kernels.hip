@@ -102,7 +102,7 @@ __global__ __launch_bounds__(256) void k_draws(uint64_t seed, int rng, int n, ui
     if (status != nullptr && l == 0 && blockIdx.y == 0) {
         status[0] = 0u;
         status[1] = 0u;   // longest tile pair of the call
-        status[2] = 0u;   // some row pair holds more than RSLOTS lengths inside a cycle group
+        status[2] = 0u;   // some row pair holds more lengths inside a cycle group than tables
     }
     if (l >= n) return;
     const uint64_t h = splitmix64(2ull * seed + (uint64_t)op);
@@ -339,7 +339,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
                 int64_t tot;
                 const int64_t v = q < nq ? dpair[q] : 0;
                 const int64_t ex = block_excl_scan_1024(v, &tot);
-                over = over || (q < nq && carry + ex + v > RSLOTS);
+                over = over || (q < nq && carry + ex + v > lay.rslots);
                 carry += tot;
             }
             if (__syncthreads_or(over) && tid == 0) atomicOr(status + 2, 1u);

@@ -1064,7 +1064,7 @@ __device__ __forceinline__ void q_division(const MGemmArgs &g, const Layout &lay
         const double Lmax = (double)ws_ptr<uint32_t>(ws, lay.off_status)[1];
         double best = 0.0;
         for (int s = 1; s <= g.S; s *= 2) {
-            const double est = quad_split_time(tiles, s, lay.q_perL, lay.q_Lmean, Lmax, lay.q_one != 0);
+            const double est = quad_split_time(tiles, s, lay.q_perL, lay.q_Lmean, Lmax, lay.q_one != 0, lay.q_slots);
             if (s == 1 || est < best * 0.97) {
                 best = est;
                 S = s;
@@ -1242,7 +1242,10 @@ __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, u
     int4 sum[NK];
 #pragma unroll
     for (int k = 0; k < NK; ++k) sum[k] = make_int4(0, 0, 0, 0);
-    for (int s = 0; s < SS; ++s) {
+    // a thread keeps one column quad; quads past N hold nothing to sum (nor, in the 64-column
+    // blocks, anything written)
+    const bool colok = tw * 256 + 4 * (int)(threadIdx.x & 63) < g.N;
+    for (int s = 0; s < (colok ? SS : 0); ++s) {
         const int4 *src = base + (size_t)s * 256 * 64;
         int4 q[NK];
 #pragma unroll
@@ -1413,11 +1416,11 @@ __device__ __forceinline__ u4 r_len_mask(int L, int G) {
 // holds, for the k-th length set in `rems` (bit r: a row of the pair ends r cycles into the
 // group), A's entries masked to that length: [byte][k][copy], address 65536 + byte * 256 +
 // (k * RREP1 + copy) * 16.
-template <bool BIP>
+template <bool BIP, int NT>
 __device__ __forceinline__ void r_build_lut(u4 *lut, const uint32_t *rA, const uint32_t *rB, int G, int tid,
                                             uint32_t rems) {
     const uint32_t zero_nib = BIP ? NIB_NEG : 0u;
-    const int byte = tid;
+    for (int byte = tid; byte < 256; byte += NT) {
     const int q = (int)(int8_t)(uint8_t)byte;
     const uint32_t beta = (uint32_t)(BIP ? beta_bipolar(q) : beta_unipolar(q));
 #pragma unroll
@@ -1444,10 +1447,17 @@ __device__ __forceinline__ void r_build_lut(u4 *lut, const uint32_t *rA, const u
             }
         }
     }
+    }
 }
 
+// NB: B blocks of 32 columns per wave (4: 128 x 128 per wave; 2: 128 x 64, N <= 64)
+template <int NB>
 struct RData {
-    u4 a[4], b[4];     // 16 elements of the lane's 4 A rows and 4 B columns (one chunk)
+    u4 a[4], b[NB];    // 16 elements of the lane's 4 A rows and NB B columns (one chunk)
+};
+template <int NB>
+struct RFrags {
+    u4 a[4], b[NB];
 };
 struct RSrc {
     __amdgpu_buffer_rsrc_t a, b;   // the pair's A chunks and the B pair's chunks
@@ -1457,16 +1467,19 @@ struct RSrc {
     int KC;
 };
 
-__device__ __forceinline__ void r_load(const RSrc &q, int c, RData &d) {
+template <int NB>
+__device__ __forceinline__ void r_load(const RSrc &q, int c, RData<NB> &d) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 4; ++i)
         d.a[i] = __builtin_amdgcn_raw_buffer_load_b128(q.a, q.voffA, c * 256 * RCH + i * 32 * RCH, 0);
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
         d.b[i] = __builtin_amdgcn_raw_buffer_load_b128(q.b, q.voffB, c * 256 * RCH + i * 32 * RCH, 0);
-    }
 }
 
 // rows that have ended before this cycle group read the padding byte, whose table row is zero
-__device__ __forceinline__ void r_finish(RData &d, const bool (&fin)[4]) {
+template <int NB>
+__device__ __forceinline__ void r_finish(RData<NB> &d, const bool (&fin)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
         if (fin[i]) d.a[i] = u4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
@@ -1485,20 +1498,21 @@ __device__ __forceinline__ uint32_t r_word(const u4 &v) {
 }
 
 // the MFMAs of A blocks 2h, 2h + 1 with every B block
-__device__ __forceinline__ void q_mma_half(v16f (&acc)[4][4], const QFrags &f, int h) {
+template <int NB>
+__device__ __forceinline__ void q_mma_half(v16f (&acc)[4][NB], const RFrags<NB> &f, int h) {
 #pragma unroll
     for (int i = 2 * h; i < 2 * h + 2; ++i)
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+        for (int c = 0; c < NB; ++c)
             acc[i][c] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(frag(f.a[i]), frag(f.b[c]),
                                                                         acc[i][c], 4, 4, 0, 127, 0, 127);
 }
 
 // fragments of k-step E (element E of the lane's 16) from chunk data d
-template <int E, bool MASK>
-__device__ __forceinline__ void r_frags(const RSrc &q, const RData &d, const u4 (&m)[4], QFrags &f) {
+template <int E, bool MASK, int NB>
+__device__ __forceinline__ void r_frags(const RSrc &q, const RData<NB> &d, const u4 (&m)[4], RFrags<NB> &f) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) f.b[c] = r_look<E>(q, r_word<E>(d.b[c]), q.loB);
+    for (int c = 0; c < NB; ++c) f.b[c] = r_look<E>(q, r_word<E>(d.b[c]), q.loB);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         f.a[i] = r_look<E>(q, r_word<E>(d.a[i]), q.loA[i]);
@@ -1510,15 +1524,18 @@ __device__ __forceinline__ void r_frags(const RSrc &q, const RData &d, const u4 
 // next k-step (2S + 2, or the next chunk's first) on exit; stage 0 loads the next chunk.
 // MASK: the A fragments are masked with the rows' lengths (some row of the pair ends
 // inside a cycle group); else rows that have ended read the padding byte (r_finish).
-__device__ __forceinline__ void r_mask(const u4 (&m)[4], QFrags &f) {
+template <int NB>
+__device__ __forceinline__ void r_mask(const u4 (&m)[4], RFrags<NB> &f) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) f.a[i] &= m[i];
 }
 
-template <bool LOADS>
+// a quarter holds 2 NB MFMAs (A blocks 2h, 2h + 1 with every B block)
+template <bool LOADS, int NB>
 __device__ __forceinline__ void r_quarter_reads() {
+    // the 4 + NB table reads of the next fragments with their address bytes
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < 2 * NB; ++k) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
         __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);   // VALU (address)
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
@@ -1526,12 +1543,12 @@ __device__ __forceinline__ void r_quarter_reads() {
     }
     __builtin_amdgcn_sched_barrier(0);
 }
-template <bool MASK>
+template <bool MASK, int NB>
 __device__ __forceinline__ void r_quarter_masks() {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < 2 * NB; ++k) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (MASK) __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // masks
+        if (MASK) __builtin_amdgcn_sched_group_barrier(0x002, 16 / (2 * NB), 0);   // masks
     }
     __builtin_amdgcn_sched_barrier(0);
 }
@@ -1539,16 +1556,17 @@ __device__ __forceinline__ void r_quarter_masks() {
 // Stage S in four quarters of 8 MFMAs: the table reads of the next fragments go with the
 // first quarter of each k-step, their length masks (MASK) with the second, once the reads
 // have landed, so no AND waits on a read in the in-order issue
-template <int S, bool MASK>
-__device__ __forceinline__ void r_stage(const RSrc &q, int cnext, RData &cur, RData &nxt, const u4 (&m)[4],
-                                        const bool (&fin)[4], v16f (&acc)[4][4], QFrags (&f)[2]) {
+template <int S, bool MASK, int NB>
+__device__ __forceinline__ void r_stage(const RSrc &q, int cnext, RData<NB> &cur, RData<NB> &nxt,
+                                        const u4 (&m)[4], const bool (&fin)[4], v16f (&acc)[4][NB],
+                                        RFrags<NB> (&f)[2]) {
     if (S == 0) r_load(q, cnext, nxt);
     r_frags<2 * S + 1, false>(q, cur, m, f[1]);
     q_mma_half(acc, f[0], 0);
-    r_quarter_reads<S == 0>();
+    r_quarter_reads<S == 0, NB>();
     if (MASK) r_mask(m, f[1]);
     q_mma_half(acc, f[0], 1);
-    r_quarter_masks<MASK>();
+    r_quarter_masks<MASK, NB>();
     if (S < 7) {
         r_frags<2 * S + 2, false>(q, cur, m, f[0]);
     } else {
@@ -1556,18 +1574,18 @@ __device__ __forceinline__ void r_stage(const RSrc &q, int cnext, RData &cur, RD
         r_frags<0, false>(q, nxt, m, f[0]);
     }
     q_mma_half(acc, f[1], 0);
-    r_quarter_reads<false>();
+    r_quarter_reads<false, NB>();
     if (MASK) r_mask(m, f[0]);
     q_mma_half(acc, f[1], 1);
-    r_quarter_masks<MASK>();
+    r_quarter_masks<MASK, NB>();
 }
 
 // chunks c .. ce-1 of one cycle group; on exit cur holds the chunk after them (chunk ce, or
 // chunk 0 of the next group) and fragment set 0 its first k-step (from this group's table)
-template <bool MASK>
-__device__ __forceinline__ void r_chunks(const RSrc &q, int c, int ce, RData &cur, RData &nxt,
-                                         const u4 (&m)[4], const bool (&fin)[4], v16f (&acc)[4][4],
-                                         QFrags (&f)[2]) {
+template <bool MASK, int NB>
+__device__ __forceinline__ void r_chunks(const RSrc &q, int c, int ce, RData<NB> &cur, RData<NB> &nxt,
+                                         const u4 (&m)[4], const bool (&fin)[4], v16f (&acc)[4][NB],
+                                         RFrags<NB> (&f)[2]) {
     for (; c < ce; ++c) {
         const int x = c + 1 < q.KC ? c + 1 : 0;
         r_stage<0, MASK>(q, x, cur, nxt, m, fin, acc, f);
@@ -1588,10 +1606,17 @@ __device__ __forceinline__ void r_chunks(const RSrc &q, int c, int ce, RData &cu
 // cycle group reads there the table masked to its length.  Both variants are launched and
 // one returns at once: MASK runs when some row pair holds more lengths inside a group than
 // there are masked tables (then every A fragment is masked with its row's length instead).
-template <bool BIP, bool MASK>
-__global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
-    __shared__ u4 lut[(MASK ? 1 : 2) * 256 * 16];   // 64 or 128 KB; the epilogue's transpose reuses it
-    __shared__ uint32_t rems[MASK ? 1 : RGROUPS];     // bit r of rems[G]: a row ends r cycles into group G
+// NARROW (N <= 64): a block of 2 waves takes the pair's 256 rows x the first 64 columns of
+// the B pair, two blocks per CU; it has no masked tables (every length inside a group makes
+// the call take the MASK variant).
+template <bool BIP, bool MASK, bool NARROW>
+__global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MGemmArgs g, Layout lay,
+                                                                          uint8_t *ws) {
+    constexpr int NT = NARROW ? 128 : 256;            // threads
+    constexpr int NB = NARROW ? 2 : 4;                // B blocks of 32 columns per wave
+    constexpr bool TABLES = !MASK && !NARROW;         // tables masked to row lengths
+    __shared__ u4 lut[(TABLES ? 2 : 1) * 256 * 16];   // 64 or 128 KB; the epilogue's transpose reuses it
+    __shared__ uint32_t rems[TABLES ? RGROUPS : 1];   // bit r of rems[G]: a row ends r cycles into group G
     if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
     const int NTW = lay.NT / 2;
     int F, SS;
@@ -1609,7 +1634,7 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
     const int bB = g.nbB == 1 ? 0 : b;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int grp = lane >> 5, i32 = lane & 31;
-    const int wr = (w >> 1) * 128, wc = (w & 1) * 128;
+    const int wr = NARROW ? 128 * w : (w >> 1) * 128, wc = NARROW ? 0 : (w & 1) * 128;
     uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
     uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
     const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm) + tp * 256;
@@ -1618,7 +1643,7 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
     const int64_t nch = (int64_t)ngroups * g.KC;
     const int64_t x0 = (int64_t)s * nch / S, x1 = (int64_t)(s + 1) * nch / S;
 
-    if (!MASK) {
+    if (TABLES) {
         if (tid < ngroups) rems[tid] = 0u;
         __syncthreads();
         const int Lt = perm[tid] >= 0 ? Ls[tid] : 0;
@@ -1647,23 +1672,23 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
     q.KC = g.KC > 0 ? g.KC : 1;
     const uint32_t *rA = ws_ptr<uint32_t>(ws, lay.off_rA), *rB = ws_ptr<uint32_t>(ws, lay.off_rB);
 
-    v16f acc[4][4];
+    v16f acc[4][NB];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[i][c] = v16f{};
+        for (int c = 0; c < NB; ++c) acc[i][c] = v16f{};
 
-    RData cur, nxt;
-    QFrags f[2];
+    RData<NB> cur, nxt;
+    RFrags<NB> f[2];
     u4 m[4];
     if (x0 < x1) r_load(q, (int)(x0 % q.KC), cur);
     for (int64_t x = x0; x < x1;) {
         const int G = (int)(x / g.KC);
         const int64_t xe = min(x1, (int64_t)(G + 1) * g.KC);
-        const uint32_t rm = MASK ? 0u : rems[G];
+        const uint32_t rm = TABLES ? rems[G] : 0u;
         // every read of the previous group's table is done before it is replaced
         __syncthreads();
-        r_build_lut<BIP>(lut, rA, rB, G, tid, rm);
+        r_build_lut<BIP, NT>(lut, rA, rB, G, tid, rm);
         __syncthreads();
         // the lane's A rows: ended, ending inside this group (the masked table of the
         // length's rank among the group's lengths; with MASK a mask instead) or running on
@@ -1675,7 +1700,7 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
             q.loA[i] = lrep;
             if (MASK) {
                 m[i] = r_len_mask(Lr[i], G);
-            } else if (rem > 0 && rem < RCH) {
+            } else if (TABLES && rem > 0 && rem < RCH) {
                 const uint32_t k = (uint32_t)__popc(rm & ((1u << rem) - 1u));
                 q.loA[i] = 0x10000u | (16u * (k * RREP1 + (uint32_t)(lane & (RREP1 - 1))));
             }
@@ -1692,7 +1717,7 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
+            for (int c = 0; c < NB; ++c)
 #pragma unroll
                 for (int e = 0; e < 16; ++e)
                     part[(wr + 32 * i + 8 * (e >> 2) + 4 * grp + (e & 3)) * 256 + wc + 32 * c + i32] =
@@ -1711,17 +1736,18 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
                 for (int i = 0; i < 4; ++i) {
                     if (i != (h & 3)) continue;
 #pragma unroll
-                    for (int c = 0; c < 4; ++c)
+                    for (int c = 0; c < NB; ++c)
 #pragma unroll
                         for (int e = 0; e < 16; ++e)
                             T[(8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] = (int32_t)acc[i][c][e];
                 }
             }
             __syncthreads();
+            constexpr int NQ = NARROW ? 16 : 64;      // column quads of the block
 #pragma unroll
-            for (int k = 0; k < TR * 64 / 256; ++k) {
-                const int idx = tid + 256 * k;        // 32 rows x 64 column quads
-                const int rl = idx >> 6, cq = idx & 63;
+            for (int k = 0; k < TR * NQ / NT; ++k) {
+                const int idx = tid + NT * k;         // 32 rows x NQ column quads
+                const int rl = idx / NQ, cq = idx % NQ;
                 const int j0 = tw * 256 + 4 * cq;
                 if (j0 >= g.N) continue;
                 const int4 qv = *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]);
@@ -1732,20 +1758,24 @@ __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8
     }
 }
 
-template <bool BIP>
-static hipError_t launch_rgemm(const MGemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
+template <bool BIP, bool NARROW>
+static hipError_t launch_rgemm_w(const MGemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
     const unsigned tiles = (unsigned)(g.batch * (lay.MT / 2) * (lay.NT / 2));
     const unsigned tail = tiles - (unsigned)g.F;
-    hipLaunchKernelGGL((k_rgemm<BIP, false>), dim3((unsigned)g.F + tail * (unsigned)g.S), dim3(256), 0, st, g,
-                       lay, ws);
+    const dim3 grid((unsigned)g.F + tail * (unsigned)g.S), block(NARROW ? 128 : 256);
+    hipLaunchKernelGGL((k_rgemm<BIP, false, NARROW>), grid, block, 0, st, g, lay, ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_rgemm<BIP, true>), dim3((unsigned)g.F + tail * (unsigned)g.S), dim3(256), 0, st, g,
-                       lay, ws);
+    hipLaunchKernelGGL((k_rgemm<BIP, true, NARROW>), grid, block, 0, st, g, lay, ws);
     e = hipGetLastError();
     if (e != hipSuccess || tail == 0) return e;
     hipLaunchKernelGGL((k_qgemm_reduce<BIP>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
     return hipGetLastError();
+}
+
+template <bool BIP>
+static hipError_t launch_rgemm(const MGemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
+    return lay.narrow ? launch_rgemm_w<BIP, true>(g, lay, ws, st) : launch_rgemm_w<BIP, false>(g, lay, ws, st);
 }
 
 template <bool BIP>

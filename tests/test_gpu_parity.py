@@ -217,6 +217,10 @@ RGEN = [
     (1, 384, 257, 300, 64, "random", 1, False, 67),    # every length; split k-ranges
     (3, 140, 129, 64, 512, "uniform", 1, False, 69),   # 16 groups, one pair per batch entry
     (1, 600, 513, 45, 33, "random", 0, False, 71),     # one cycle past the first group
+    # N <= 64: blocks of 256 rows x 64 columns, two per CU
+    (2, 300, 64, 64, 256, "uniform", 0, True, 73),     # the compensator's shape class
+    (3, 577, 17, 200, 130, "random", 1, False, 75),    # attention-like, ragged N
+    (1, 129, 1, 5, 96, "mult32", 0, False, 77),        # one column, K < 32, rows ending at bounds
 ]
 
 
