@@ -167,11 +167,13 @@ def main():
         # one bit-pair product = one fp4 multiply-add = 2 flops on the matrix cores
         roofline = {"bound": "mfma", "achieved": 2 * achieved / 1e12, "peak": PEAK_FP4_FLOPS / 1e12,
                     "unit": "TFLOP/s", "frac": 2 * achieved / PEAK_FP4_FLOPS, "traffic": traffic,
-                    # 256 x 256 tiles when both M and N exceed one 128-row tile (fragments
-                    # built from int8 chunks with comparator streams, fp4 planes with C-BSG);
-                    # N <= 128 with comparator streams: fragments built inside the GEMM
-                    "kernel": "%s<%s>" % (("k_rgemm" if rng == scg.SC_RNG_LFSR32 else "k_qgemm")
-                                          if g_dom.M > 128 and g_dom.N > 128 else
+                    # M > 128: 256-row blocks (fragments built from int8 chunks with
+                    # comparator streams, 256 or, for N <= 64, 64 columns wide; fp4 planes
+                    # with C-BSG when N > 128); other N <= 128 with comparator streams:
+                    # fragments built from the int8 rows in the GEMM
+                    "kernel": "%s<%s>" % ("k_rgemm" if rng == scg.SC_RNG_LFSR32 and g_dom.M > 128 and
+                                          (g_dom.N > 128 or g_dom.N <= 64) else
+                                          "k_qgemm" if g_dom.M > 128 and g_dom.N > 128 else
                                           "k_fgemm" if g_dom.N <= 128 and rng == scg.SC_RNG_LFSR32 else "k_mgemm",
                                           "bipolar" if g_dom.polarity == 0 else "unipolar"),
                     "kernel_ms": gemm_ms, "frac_of_valu_bitop_peak": achieved / PEAK_BITOPS}

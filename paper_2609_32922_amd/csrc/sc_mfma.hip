@@ -18,17 +18,18 @@
 //                 128-row tile x 64 cycles x 64 elements; element parameters and an
 //                 8-cycle lookup table in LDS, 16-byte stores, 1 KB per wave; with
 //                 comparator streams (M <= 128) both operands in one launch (k_mplanes2)
-//   k_fgemm       N <= 128 with comparator streams: 128x128 tile, the fp4 fragments of
-//                 both operands built in LDS from the int8 rows (an 8-cycle table per
-//                 octet indexed by the int8 byte), so no planes are written or read
+//   k_fgemm       N <= 128 with comparator streams where k_rgemm does not apply (M <= 128,
+//                 or 64 < N <= 128): 128x128 tile, the fp4 fragments of both operands built
+//                 in LDS from the int8 rows (an 8-cycle table per octet indexed by the int8
+//                 byte), so no planes are written or read
 //   k_rchunks     int8 operands (A in the scheduler's row order) laid out in 32-element
 //                 chunks per 256-row pair, the input of k_rgemm
-//   k_rgemm       N > 128 and M > 128 with comparator streams: the tiles and division of
-//                 k_qgemm, but every fp4 fragment is one LDS table read (a table per
-//                 32-cycle group indexed by the int8 byte), so no planes exist and the
+//   k_rgemm       M > 128 and N > 128 (or N <= 64) with comparator streams: the tiles and
+//                 division of k_qgemm, but every fp4 fragment is one LDS table read (a table
+//                 per 32-cycle group indexed by the int8 byte), so no planes exist and the
 //                 loop has no stage buffers; rows ending inside a group read tables masked
 //                 to their length (a second variant masks every fragment when a row pair
-//                 holds too many such lengths)
+//                 holds too many such lengths); for N <= 64 blocks of 256 x 64, two per CU
 //   k_qgemm       N > 128 and M > 128 with C-BSG streams: 256x256 output tile per
 //                 256-thread block, one block per CU, 128x128 per wave as 4x4 32x32 MFMA
 //                 blocks, three LDS buffers of 4 slots (96 KB), memory instructions
