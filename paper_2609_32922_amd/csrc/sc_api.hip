@@ -72,6 +72,8 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     off = align256(off + (size_t)l.LBS * 4);
     l.off_CA = off;
     if (cbsg) off = align256(off + (size_t)(d.L_max + 1) * CA_COLS * 2);
+    l.off_rtab = off;
+    if (l.rgen) off = align256(off + (size_t)(l.LBS / 32) * 512 * 16);
 
     // one A block per batch entry
     const size_t rowsA = (size_t)l.MT * BM;

@@ -9,6 +9,8 @@
 //              fragments); all cleared by k_draws
 //   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
 //   CA         C-BSG only: CA[L][beta] = #{l < L : rA_l < beta}, uint16 [L_max+1][257]
+//   rtab       int8-chunk GEMM only: for each 32-cycle group G, the fp4 slot row of every
+//              int8 byte for A and for B: uint4 [LBS/32][2][256] (built once per call)
 //   per batch entry b of A (batch entries):
 //     perm[MT*BM]      sorted position -> original row (or -1 for padding)
 //     Ls[MT*BM]        stream length at each sorted position
@@ -133,7 +135,7 @@ struct Layout {
     int rslots;        // rgen: tables masked to a row length per cycle group (0 when narrow)
     int KC;            // 32-element chunks per row, ceil(K/32)
     int64_t words_per_L;   // plane words of one 128-row tile per cycle of its length
-    size_t off_rA, off_rB, off_status, off_CA;
+    size_t off_rA, off_rB, off_status, off_CA, off_rtab;
     size_t off_perm, off_Ls, off_RA, off_tileL, off_tileOff, off_Ap, off_SA;
     size_t stride_batchA;          // bytes per A batch entry block
     size_t off_Bp, off_SB, off_RB;

@@ -1310,6 +1310,27 @@ __device__ __forceinline__ uint32_t r_clamp4(uint32_t x) {
     return x | ((~nz & 0x80808080u) >> 7);
 }
 
+// Entry (byte, operand) of the table of cycle group G: the 32 nibbles of cycles 32G .. 32G+31
+// (cycle 32G + k at bits 4 (k % 8) of dword k / 8), sign folded in (unipolar), zero for the
+// padding byte; r points at the operand's draw of cycle 32G.  The tables of every group are
+// built once per call (k_rchunks) into the workspace, [G][operand][byte].
+template <bool BIP>
+__device__ __forceinline__ u4 r_entry(const uint32_t *r, int byte) {
+    u4 x = u4{0u, 0u, 0u, 0u};
+    if (byte == RPAD) return x;
+    const uint32_t zero_nib = BIP ? NIB_NEG : 0u;
+    const int q = (int)(int8_t)(uint8_t)byte;
+    const uint32_t beta = (uint32_t)(BIP ? beta_bipolar(q) : beta_unipolar(q));
+#pragma unroll
+    for (int dw = 0; dw < 4; ++dw) {
+        uint32_t w = 0;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) w |= (r[8 * dw + c] < beta ? NIB_POS : zero_nib) << (4 * c);
+        x[dw] = (!BIP && q < 0) ? negate_nibbles(w) : w;
+    }
+    return x;
+}
+
 struct RChunkArgs {
     const int8_t *X[2];
     int64_t ld[2], strideX[2];
@@ -1318,11 +1339,24 @@ struct RChunkArgs {
     size_t off_perm;      // side 0 (A) takes its rows in the scheduler's order
     int K, KC;
     int vec[2];           // 16-byte loads are aligned (base and row stride multiples of 16)
+    int groups, bip;      // tables: 32-cycle groups, polarity
+    size_t off_r[2], off_rtab;
 };
 
 // Chunks of both operands: thread = (row r of the tile order, half h) of chunk blockIdx.y,
 // side and batch entry from blockIdx.z; each thread copies one 16-byte half.
 __global__ __launch_bounds__(256) void k_rchunks(RChunkArgs a, uint8_t *ws) {
+    if (blockIdx.z == (unsigned)(a.nb[0] + a.nb[1])) {
+        // the last slice of the grid builds the tables of every cycle group
+        u4 *tab = ws_ptr<u4>(ws, a.off_rtab);
+        const int nblk = gridDim.x * gridDim.y;
+        for (int e = (blockIdx.y * gridDim.x + blockIdx.x) * 256 + threadIdx.x; e < a.groups * 512; e += nblk * 256) {
+            const int G = e >> 9, side = (e >> 8) & 1, byte = e & 255;
+            const uint32_t *r = ws_ptr<uint32_t>(ws, a.off_r[side]) + RCH * G;
+            tab[e] = a.bip ? r_entry<true>(r, byte) : r_entry<false>(r, byte);
+        }
+        return;
+    }
     const int side = blockIdx.z >= (unsigned)a.nb[0];
     const int b = side ? blockIdx.z - a.nb[0] : blockIdx.z;
     const int t = blockIdx.x * 256 + threadIdx.x;
@@ -1368,7 +1402,7 @@ __global__ __launch_bounds__(256) void k_rchunks(RChunkArgs a, uint8_t *ws) {
 
 hipError_t launch_rchunks(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const int8_t *B,
                           uint8_t *ws, hipStream_t st) {
-    if (lay.KC == 0) return hipSuccess;
+    if (lay.KC == 0) return hipSuccess;       // no chunk and no table is read
     RChunkArgs a{};
     a.X[0] = A;
     a.X[1] = B;
@@ -1391,9 +1425,14 @@ hipError_t launch_rchunks(const sc_gemm_desc &d, const Layout &lay, const int8_t
     a.KC = lay.KC;
     a.vec[0] = (reinterpret_cast<uintptr_t>(A) % 16 == 0) && d.lda % 16 == 0 && d.strideA % 16 == 0;
     a.vec[1] = (reinterpret_cast<uintptr_t>(B) % 16 == 0) && d.ldb % 16 == 0 && d.strideB % 16 == 0;
+    a.groups = lay.LBS / RCH;
+    a.bip = d.polarity == SC_BIPOLAR_XNOR;
+    a.off_r[0] = lay.off_rA;
+    a.off_r[1] = lay.off_rB;
+    a.off_rtab = lay.off_rtab;
     const int rows = a.rows_pad[0] > a.rows_pad[1] ? a.rows_pad[0] : a.rows_pad[1];
     hipLaunchKernelGGL(k_rchunks, dim3((unsigned)((2 * rows + 255) / 256), (unsigned)lay.KC,
-                                       (unsigned)(d.batch + lay.nbB)),
+                                       (unsigned)(d.batch + lay.nbB + 1)),
                        dim3(256), 0, st, a, ws);
     return hipGetLastError();
 }
@@ -1410,44 +1449,40 @@ __device__ __forceinline__ u4 r_len_mask(int L, int G) {
     return m;
 }
 
-// Table of cycle group G: entry (byte, operand) holds the 32 nibbles of cycles 32G .. 32G+31
-// (cycle 32G + k at bits 4 (k % 8) of dword k / 8), sign folded in (unipolar), zero for the
-// padding byte.  Entry copies are laid out [byte][operand][copy], so a read's byte
-// address is byte * 256 + operand * 128 + copy * 16.  A second region (from byte 65536)
-// holds, for the k-th length set in `rems` (bit r: a row of the pair ends r cycles into the
-// group), A's entries masked to that length: [byte][k][copy], address 65536 + byte * 256 +
-// (k * RREP1 + copy) * 16.
-template <bool BIP, int NT>
-__device__ __forceinline__ void r_build_lut(u4 *lut, const uint32_t *rA, const uint32_t *rB, int G, int tid,
-                                            uint32_t rems) {
-    const uint32_t zero_nib = BIP ? NIB_NEG : 0u;
-    for (int byte = tid; byte < 256; byte += NT) {
-    const int q = (int)(int8_t)(uint8_t)byte;
-    const uint32_t beta = (uint32_t)(BIP ? beta_bipolar(q) : beta_unipolar(q));
+// Entries of one group's table held by a thread: of the group's 512 (A's 256 bytes, then B's),
+// entry k NT + tid, i.e. bytes tid, tid + NT, .. of A, then the same bytes of B.
+template <int NT>
+__device__ __forceinline__ void r_load_ent(u4 (&ent)[512 / NT], const u4 *tab, int tid) {
 #pragma unroll
-    for (int side = 0; side < 2; ++side) {
-        const uint32_t *r = (side ? rB : rA) + RCH * G;
-        u4 x = u4{0u, 0u, 0u, 0u};
-        if (byte != RPAD) {
+    for (int k = 0; k < 512 / NT; ++k) ent[k] = tab[k * NT + tid];
+}
+
+// The LDS table of one group from the thread's entries (r_load_ent): copies laid out
+// [byte][operand][copy], so a read's byte address is byte * 256 + operand * 128 + copy * 16.
+// A second region (from byte 65536) holds, for the k-th length set in `rems` (bit r: a row of
+// the pair ends r cycles into the group), A's entries masked to that length: [byte][k][copy],
+// address 65536 + byte * 256 + (k * RREP1 + copy) * 16.  Each store instruction rotates the
+// copy by the lane, so that a wave's 64 lanes spread over 8 (masked: 4) 16-byte columns of the
+// 256-byte rows instead of all falling into one.
+template <int NT>
+__device__ __forceinline__ void r_fill_lut(u4 *lut, const u4 (&ent)[512 / NT], int tid, uint32_t rems) {
+    constexpr int BPT = 256 / NT;     // bytes per thread
+    const int lane = tid & 63;
 #pragma unroll
-            for (int dw = 0; dw < 4; ++dw) {
-                uint32_t w = 0;
+    for (int i = 0; i < BPT; ++i) {
+        u4 *row = lut + (i * NT + tid) * 16;
 #pragma unroll
-                for (int c = 0; c < 8; ++c) w |= (r[8 * dw + c] < beta ? NIB_POS : zero_nib) << (4 * c);
-                x[dw] = (!BIP && q < 0) ? negate_nibbles(w) : w;
-            }
+        for (int j = 0; j < RREP; ++j) {
+            const int c = (j + lane) & (RREP - 1);
+            row[c] = ent[i];
+            row[RREP + c] = ent[BPT + i];
         }
+        int k = 0;
+        for (uint32_t m = rems; m != 0u; m &= m - 1u, ++k) {
+            const u4 xm = ent[i] & r_len_mask(__builtin_ctz(m), 0);
 #pragma unroll
-        for (int k = 0; k < RREP; ++k) lut[byte * 16 + side * RREP + k] = x;
-        if (side == 0) {
-            int k = 0;
-            for (uint32_t m = rems; m != 0u; m &= m - 1u, ++k) {
-                const u4 xm = x & r_len_mask(__builtin_ctz(m), 0);
-#pragma unroll
-                for (int c = 0; c < RREP1; ++c) lut[256 * 16 + byte * 16 + k * RREP1 + c] = xm;
-            }
+            for (int j = 0; j < RREP1; ++j) row[256 * 16 + k * RREP1 + ((j + lane) & (RREP1 - 1))] = xm;
         }
-    }
     }
 }
 
@@ -1671,7 +1706,13 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     q.loB = lrep + 16u * RREP;
     q.lut = reinterpret_cast<const char *>(lut);
     q.KC = g.KC > 0 ? g.KC : 1;
-    const uint32_t *rA = ws_ptr<uint32_t>(ws, lay.off_rA), *rB = ws_ptr<uint32_t>(ws, lay.off_rB);
+    // this thread's entries of the group tables, the next group's loaded while the current
+    // group runs
+    const u4 *rtab = ws_ptr<u4>(ws, lay.off_rtab);
+    u4 ent[512 / NT];
+    if (x0 < x1) {
+        r_load_ent<NT>(ent, rtab + (size_t)(x0 / g.KC) * 512, tid);
+    }
 
     v16f acc[4][NB];
 #pragma unroll
@@ -1689,7 +1730,10 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
         const uint32_t rm = TABLES ? rems[G] : 0u;
         // every read of the previous group's table is done before it is replaced
         __syncthreads();
-        r_build_lut<BIP, NT>(lut, rA, rB, G, tid, rm);
+        r_fill_lut<NT>(lut, ent, tid, rm);
+        if (xe < x1) {
+            r_load_ent<NT>(ent, rtab + (size_t)(G + 1) * 512, tid);
+        }
         __syncthreads();
         // the lane's A rows: ended, ending inside this group (the masked table of the
         // length's rank among the group's lengths; with MASK a mask instead) or running on
