@@ -7,7 +7,8 @@
 //   k_cbsg_table C-BSG only: CA[L][beta] = ones of A's stream in its first L cycles
 //   k_schedule   per-row length scheduler: validates L_i, counting-sorts rows by L
 //                (descending) so that a 128-row tile runs for the longest length it
-//                holds (Sec. 4.2: "row i stops at l_i"; Sec. 4.1 cost ~ sum of l_i)
+//                holds (Sec. 4.2: row i stops after its own l_i cycles; Sec. 4.1: the
+//                cost grows with the sum of the l_i)
 //   k_marginals  bipolar only: RA_i = sum_d sum_{l<L_i} zA and RB_j(L) for all L
 //   k_planes     comparator stream generation into packed bit planes (one word =
 //                32 inner-dimension elements at one cycle); 64 lanes compare one
@@ -251,14 +252,35 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 
     for (int v = tid; v <= L_max; v += 1024) hist[v] = 0;
     __syncthreads();
-    for (int i0 = 0; i0 < M; i0 += 1024) {
-        const int i = i0 + tid;
-        int l = i < M ? Lb[i] : 0;
-        if (l < 0 || l > L_max) {
-            atomicOr(status, STATUS_BAD_LENGTH);
-            l = 0;
+    // Up to SREG * 1024 rows the lengths are loaded once, all loads in flight together, and
+    // kept in registers for the scatter; longer batch entries loop (and load them twice).
+    constexpr int SREG = 8;
+    const bool cached = M <= SREG * 1024;
+    int lv[SREG];
+    if (cached) {
+#pragma unroll
+        for (int k = 0; k < SREG; ++k) {
+            const int i = k * 1024 + tid;
+            lv[k] = i < M ? Lb[i] : 0;
         }
-        wave_bucket_add(hist, l, i < M);
+#pragma unroll
+        for (int k = 0; k < SREG; ++k) {
+            if (lv[k] < 0 || lv[k] > L_max) {
+                atomicOr(status, STATUS_BAD_LENGTH);
+                lv[k] = 0;
+            }
+            if (k * 1024 < M) wave_bucket_add(hist, lv[k], k * 1024 + tid < M);
+        }
+    } else {
+        for (int i0 = 0; i0 < M; i0 += 1024) {
+            const int i = i0 + tid;
+            int l = i < M ? Lb[i] : 0;
+            if (l < 0 || l > L_max) {
+                atomicOr(status, STATUS_BAD_LENGTH);
+                l = 0;
+            }
+            wave_bucket_add(hist, l, i < M);
+        }
     }
     __syncthreads();
     // start position of each length bucket, longest lengths first
@@ -272,15 +294,29 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         carry += tot;
         __syncthreads();
     }
-    for (int i0 = 0; i0 < M; i0 += 1024) {
-        const int i = i0 + tid;
-        int l = i < M ? Lb[i] : 0;
-        if (l < 0 || l > L_max) l = 0;
-        const int pos = wave_bucket_add(hist, l, i < M);
-        if (i < M) {
-            perm[pos] = i;
-            Ls[pos] = l;
-            RA[pos] = 0;
+    if (cached) {
+#pragma unroll
+        for (int k = 0; k < SREG; ++k) {
+            const int i = k * 1024 + tid;
+            if (k * 1024 >= M) break;
+            const int pos = wave_bucket_add(hist, lv[k], i < M);
+            if (i < M) {
+                perm[pos] = i;
+                Ls[pos] = lv[k];
+                RA[pos] = 0;
+            }
+        }
+    } else {
+        for (int i0 = 0; i0 < M; i0 += 1024) {
+            const int i = i0 + tid;
+            int l = i < M ? Lb[i] : 0;
+            if (l < 0 || l > L_max) l = 0;
+            const int pos = wave_bucket_add(hist, l, i < M);
+            if (i < M) {
+                perm[pos] = i;
+                Ls[pos] = l;
+                RA[pos] = 0;
+            }
         }
     }
     for (int p = M + tid; p < lay.MT * BM; p += 1024) {
@@ -288,8 +324,20 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         Ls[p] = 0;
         RA[p] = 0;
     }
-    __threadfence_block();
     __syncthreads();
+    // After the scatter hist[l] is the end of length l's run of sorted positions (runs in
+    // order of decreasing length, ends non-increasing in l): the length at sorted position
+    // p < M is the largest l whose run ends after p.
+    auto length_at = [&](int p) {
+        if (p >= M) return 0;
+        int lo = 0, hi = L_max;   // hist[lo] > p holds (hist[0] = M)
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (hist[mid] > p) lo = mid;
+            else hi = mid - 1;
+        }
+        return lo;
+    };
     // tile lengths (first sorted row of a tile holds its longest length; a pair of tiles
     // that one 256-row block takes runs at the pair's longest length) and offsets
     carry = 0;
@@ -298,7 +346,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         int tl = 0;
         if (t < lay.MT) {
             const int t0 = lay.mbm == 2 * BM ? (t & ~1) : t;
-            tl = (int)round_up(Ls[(size_t)t0 * BM], lay.tstep);
+            tl = (int)round_up(length_at(t0 * BM), lay.tstep);
             tileL[t] = tl;
         }
         int64_t tot;
@@ -307,7 +355,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         carry += tot;
     }
     // the first tile pair holds the batch entry's longest rows
-    if (tid == 0 && lay.mbm == 2 * BM) atomicMax(status + 1, (uint32_t)tileL[0]);
+    if (tid == 0 && lay.mbm == 2 * BM) atomicMax(status + 1, (uint32_t)round_up(length_at(0), lay.tstep));
     // The int8-chunk GEMM keeps, per cycle group, a table of A masked to each row length
     // that ends inside the group: RSLOTS of them.  Rows are sorted, so the distinct lengths
     // of a pair are the first rows of runs of equal length; a pair with more such lengths

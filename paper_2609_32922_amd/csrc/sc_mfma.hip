@@ -341,25 +341,21 @@ struct MGemmArgs {
     int32_t *counts;
 };
 
-// decode of four adjacent columns j0.. of sorted row position p from the fp4 product sums
+// decode and store four adjacent columns j0.. (ncol of them in range) of original row i of
+// batch entry b from the fp4 product sums: Li its length, scale = sA_i * 127^2, sBj the
+// columns' scales
 template <bool BIP>
-__device__ __forceinline__ void mdecode4(const int32_t (&P)[4], int p, int j0, int ncol, int b,
-                                         const MGemmArgs &g, const Layout &lay, uint8_t *ws) {
-    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
-    const int i = ws_ptr<int32_t>(wsa, lay.off_perm)[p];
-    if (i < 0) return;
-    const int Li = ws_ptr<int32_t>(wsa, lay.off_Ls)[p];
-    const float scale = g.sA[(size_t)b * g.strideSA + i] * 16129.0f;
-    const float *sBb = g.sB + (size_t)b * g.strideSB;
+__device__ __forceinline__ void mdecode4_store(const int32_t (&P)[4], int i, int Li, float scale,
+                                               const float (&sBj)[4], int j0, int ncol, int b,
+                                               const MGemmArgs &g) {
     const int KL = g.K * Li;
     float o[4];
     int32_t cnt[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-        const int j = c < ncol ? j0 + c : j0;
         // bipolar: P = 2X - K L; unipolar: P = S
         cnt[c] = BIP ? (KL + P[c]) / 2 : P[c];
-        o[c] = Li > 0 ? (float)P[c] / (float)Li * (scale * sBb[j]) : 0.0f;
+        o[c] = Li > 0 ? (float)P[c] / (float)Li * (scale * sBj[c]) : 0.0f;
         if (Li == 0) cnt[c] = 0;
     }
     float *op = g.out + (size_t)b * g.strideO + (size_t)i * g.ldo + j0;
@@ -376,6 +372,22 @@ __device__ __forceinline__ void mdecode4(const int32_t (&P)[4], int p, int j0, i
             for (int c = 0; c < ncol; ++c) cp[c] = cnt[c];
         }
     }
+}
+
+// the same for sorted row position p, its row, length and scales read from global memory
+template <bool BIP>
+__device__ __forceinline__ void mdecode4(const int32_t (&P)[4], int p, int j0, int ncol, int b,
+                                         const MGemmArgs &g, const Layout &lay, uint8_t *ws) {
+    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
+    const int i = ws_ptr<int32_t>(wsa, lay.off_perm)[p];
+    if (i < 0) return;
+    const int Li = ws_ptr<int32_t>(wsa, lay.off_Ls)[p];
+    const float scale = g.sA[(size_t)b * g.strideSA + i] * 16129.0f;
+    const float *sBb = g.sB + (size_t)b * g.strideSB;
+    float sBj[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) sBj[c] = sBb[c < ncol ? j0 + c : j0];
+    mdecode4_store<BIP>(P, i, Li, scale, sBj, j0, ncol, b, g);
 }
 
 // Block tile: BM = 128 rows of A x WB columns of B, WB = 256 (two 128-column B plane
@@ -1653,6 +1665,9 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     constexpr bool TABLES = !MASK && !NARROW;         // tables masked to row lengths
     __shared__ u4 lut[(TABLES ? 2 : 1) * 256 * 16];   // 64 or 128 KB; the epilogue's transpose reuses it
     __shared__ uint32_t rems[TABLES ? RGROUPS : 1];   // bit r of rems[G]: a row ends r cycles into group G
+    // what the decode of a whole tile needs (filled after the chunk loop)
+    __shared__ int32_t d_row[256], d_len[256];
+    __shared__ float d_scale[256], d_sB[256];
     if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
     const int NTW = lay.NT / 2;
     int F, SS;
@@ -1676,6 +1691,7 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm) + tp * 256;
     const int32_t *Ls = ws_ptr<int32_t>(wsa, lay.off_Ls) + tp * 256;
     const int ngroups = (int)(round_up(ws_ptr<int32_t>(wsa, lay.off_tileL)[2 * tp], RCH) / RCH);
+
     const int64_t nch = (int64_t)ngroups * g.KC;
     const int64_t x0 = (int64_t)s * nch / S, x1 = (int64_t)(s + 1) * nch / S;
 
@@ -1758,47 +1774,65 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     }
 
     if (split) {
-        int32_t *part = ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256;
+        // a part stores its int32 partial sums (rows of 256 columns) for the split sum: one
+        // lane offset, the element's offset in a scalar register
+        const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
+            ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256, 0, 256 * 256 * 4, 0x00020000);
+        const int voff = ((wr + 4 * grp) * 256 + wc + i32) * 4;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int c = 0; c < NB; ++c)
 #pragma unroll
                 for (int e = 0; e < 16; ++e)
-                    part[(wr + 32 * i + 8 * (e >> 2) + 4 * grp + (e & 3)) * 256 + wc + 32 * c + i32] =
-                        (int32_t)acc[i][c][e];
-    } else {
-        // transpose through LDS, 32 rows at a time, so that each thread decodes four
-        // adjacent columns of one row
-        constexpr int TS = 256 + 4, TR = 32;
-        static_assert(TR * TS * 4 <= 256 * 16 * 16, "the epilogue transpose must fit the table");
-        int32_t *T = reinterpret_cast<int32_t *>(lut);
-        for (int h = 0; h < 256 / TR; ++h) {
-            __syncthreads();
-            // rows 32h .. 32h + 31: MFMA block i = h % 4 of the waves at wr = 128 (h / 4)
-            if (wr == 128 * (h >> 2)) {
+                    __builtin_amdgcn_raw_buffer_store_b32((uint32_t)(int32_t)acc[i][c][e], pr, voff,
+                                                          ((32 * i + 8 * (e >> 2) + (e & 3)) * 256 + 32 * c) * 4, 0);
+        return;
+    }
+    // a whole tile decodes: first what the decode needs per row of the pair (original row or
+    // -1 for padding, length, scale times 127^2) and per column (scale) into LDS, then the
+    // sums are transposed through LDS, 32 rows at a time, so that each thread decodes four
+    // adjacent columns of one row
+    for (int r = tid; r < 256; r += NT) {
+        const int i = perm[r];
+        d_row[r] = i;
+        d_len[r] = i >= 0 ? Ls[r] : 0;
+        d_scale[r] = i >= 0 ? g.sA[(size_t)b * g.strideSA + i] * 16129.0f : 0.0f;
+        const int j = tw * 256 + r;
+        d_sB[r] = j < g.N ? g.sB[(size_t)b * g.strideSB + j] : 0.0f;
+    }
+    constexpr int TS = 256 + 4, TR = 32;
+    static_assert(TR * TS * 4 <= 256 * 16 * 16, "the epilogue transpose must fit the table");
+    int32_t *T = reinterpret_cast<int32_t *>(lut);
+    for (int h = 0; h < 256 / TR; ++h) {
+        __syncthreads();
+        // rows 32h .. 32h + 31: MFMA block i = h % 4 of the waves at wr = 128 (h / 4)
+        if (wr == 128 * (h >> 2)) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    if (i != (h & 3)) continue;
+            for (int i = 0; i < 4; ++i) {
+                if (i != (h & 3)) continue;
 #pragma unroll
-                    for (int c = 0; c < NB; ++c)
+                for (int c = 0; c < NB; ++c)
 #pragma unroll
-                        for (int e = 0; e < 16; ++e)
-                            T[(8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] = (int32_t)acc[i][c][e];
-                }
+                    for (int e = 0; e < 16; ++e)
+                        T[(8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] = (int32_t)acc[i][c][e];
             }
-            __syncthreads();
-            constexpr int NQ = NARROW ? 16 : 64;      // column quads of the block
+        }
+        __syncthreads();
+        constexpr int NQ = NARROW ? 16 : 64;      // column quads of the block
 #pragma unroll
-            for (int k = 0; k < TR * NQ / NT; ++k) {
-                const int idx = tid + NT * k;         // 32 rows x NQ column quads
-                const int rl = idx / NQ, cq = idx % NQ;
-                const int j0 = tw * 256 + 4 * cq;
-                if (j0 >= g.N) continue;
-                const int4 qv = *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]);
-                const int32_t P[4] = {qv.x, qv.y, qv.z, qv.w};
-                mdecode4<BIP>(P, tp * 256 + TR * h + rl, j0, min(4, g.N - j0), b, g, lay, ws);
-            }
+        for (int k = 0; k < TR * NQ / NT; ++k) {
+            const int idx = tid + NT * k;         // 32 rows x NQ column quads
+            const int rl = idx / NQ, cq = idx % NQ, r = TR * h + rl;
+            const int j0 = tw * 256 + 4 * cq;
+            if (j0 >= g.N || d_row[r] < 0) continue;
+            const int4 qv = *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]);
+            const int32_t P[4] = {qv.x, qv.y, qv.z, qv.w};
+            const int ncol = min(4, g.N - j0);
+            float sBj[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) sBj[c] = d_sB[4 * cq + (c < ncol ? c : 0)];
+            mdecode4_store<BIP>(P, d_row[r], d_len[r], d_scale[r], sBj, j0, ncol, b, g);
         }
     }
 }

@@ -321,6 +321,31 @@ def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None, seq=0,
                      rng=seq)
 
 
+# The scheduler keeps up to 8192 lengths per batch entry in registers and loops over longer
+# entries; both paths sort, validate and give the tile lengths.
+SCHED_LONG = [(8192, 64, 1), (8193, 64, 0), (12000, 300, 1)]
+
+
+@pytest.mark.parametrize("case", SCHED_LONG, ids=[str(c) for c in SCHED_LONG])
+def test_schedule_long_batch_entries(dev, oracle_mod, case):
+    import paper_2609_32922_amd as scg
+    M, N, pol = case
+    rng = np.random.default_rng(M + N)
+    g = W.random_gemm(rng, 2, M, N, 40, 96, pol, 61)
+    _note("long batch entries %s" % (case,))
+    out, cnt = _run(g, dev)
+    for b in range(2):
+        rows = np.union1d(_sample(M, rng, 60), [r for r in (8190, 8191, 8192, 8193) if r < M])
+        _compare(g, b, rows, np.arange(N), out, cnt, oracle_mod, "long M %d b%d" % (M, b))
+    # an out-of-range length past the first 8192 rows is flagged and its row counts nothing
+    g.L[1, M - 1] = 97
+    with pytest.raises(scg.ScError) as ei:
+        _run(g, dev, check_status=True)
+    assert ei.value.code == scg.SC_ERR_DEVICE_STATUS
+    out, cnt = _run(g, dev, check_status=False)
+    assert np.all(cnt[1, M - 1] == 0)
+
+
 @pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
 def test_workload_vitb16_fc1_L128(dev, oracle_mod, engine):
     _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod, engine=engine)
