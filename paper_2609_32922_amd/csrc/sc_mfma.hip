@@ -390,6 +390,57 @@ __device__ __forceinline__ void mdecode4(const int32_t (&P)[4], int p, int j0, i
     mdecode4_store<BIP>(P, i, Li, scale, sBj, j0, ncol, b, g);
 }
 
+// What the decode of a whole 256 x 256 tile needs, staged in LDS once per tile: per row of
+// the pair its original row (-1: padding), length and scale times 127^2; per column its scale.
+struct DecodeLds {
+    int32_t row[256], len[256];
+    float scale[256], sB[256];
+};
+
+template <int NT>
+__device__ __forceinline__ void d_stage(DecodeLds &d, const int32_t *perm, const int32_t *Ls, int b, int tw,
+                                        const MGemmArgs &g, int tid) {
+    for (int r = tid; r < 256; r += NT) {
+        const int i = perm[r];
+        d.row[r] = i;
+        d.len[r] = i >= 0 ? Ls[r] : 0;
+        d.scale[r] = i >= 0 ? g.sA[(size_t)b * g.strideSA + i] * 16129.0f : 0.0f;
+        const int j = tw * 256 + r;
+        d.sB[r] = j < g.N ? g.sB[(size_t)b * g.strideSB + j] : 0.0f;
+    }
+}
+
+// decode of row r of the pair, column quad cq of the tile, from the staged data
+template <bool BIP>
+__device__ __forceinline__ void d_decode4(const DecodeLds &d, const int4 &qv, int r, int cq, int tw, int b,
+                                          const MGemmArgs &g) {
+    const int j0 = tw * 256 + 4 * cq;
+    if (j0 >= g.N || d.row[r] < 0) return;
+    const int32_t P[4] = {qv.x, qv.y, qv.z, qv.w};
+    const int ncol = min(4, g.N - j0);
+    float sBj[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) sBj[c] = d.sB[4 * cq + (c < ncol ? c : 0)];
+    mdecode4_store<BIP>(P, d.row[r], d.len[r], d.scale[r], sBj, j0, ncol, b, g);
+}
+
+// A part's int32 partial sums [256 rows][256 columns] from a wave's 4 x NB blocks of 32 x 32
+// accumulators at (wr, wc): one lane offset, each element's offset in a scalar register.
+template <int NB>
+__device__ __forceinline__ void store_part(const v16f (&acc)[4][NB], int32_t *part, int wr, int wc, int grp,
+                                           int i32) {
+    const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(part, 0, 256 * 256 * 4, 0x00020000);
+    const int voff = ((wr + 4 * grp) * 256 + wc + i32) * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int c = 0; c < NB; ++c)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                __builtin_amdgcn_raw_buffer_store_b32((uint32_t)(int32_t)acc[i][c][e], pr, voff,
+                                                      ((32 * i + 8 * (e >> 2) + (e & 3)) * 256 + 32 * c) * 4, 0);
+}
+
 // Block tile: BM = 128 rows of A x WB columns of B, WB = 256 (two 128-column B plane
 // tiles) or 128 (one; taken when N <= 128, where a wider tile would mostly multiply
 // padding).
@@ -1122,6 +1173,7 @@ template <bool BIP>
 __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
     static_assert(QKS % 2 == 0, "the fragment sets alternate within a stage");
     __shared__ u4 smem[QNBUF * QBUF];
+    __shared__ DecodeLds dl;                          // filled after the k loop
     const int NTW = lay.NT / 2;
     int F, SS;
     q_division(g, lay, ws, F, SS);
@@ -1192,18 +1244,12 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
 
     if (split) {
         // partial sums of this unit as int32 [256 rows][256 columns]
-        int32_t *part = ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-#pragma unroll
-                for (int e = 0; e < 16; ++e)
-                    part[(wr + 32 * i + 8 * (e >> 2) + 4 * grp + (e & 3)) * 256 + wc + 32 * c + i32] =
-                        (int32_t)acc[i][c][e];
+        store_part<4>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256, wr, wc, grp, i32);
     } else {
-        // transpose through LDS, 64 rows at a time, so that each thread decodes four
-        // adjacent columns of one row
+        // the rows' and columns' data staged in LDS, the sums transposed through LDS, 64 rows
+        // at a time, so that each thread decodes four adjacent columns of one row
+        d_stage<256>(dl, ws_ptr<int32_t>(wsa, lay.off_perm) + tp * 256, ws_ptr<int32_t>(wsa, lay.off_Ls) + tp * 256,
+                     b, tw, g, tid);
         constexpr int TS = 256 + 4, TR = 64;
         static_assert(TR * TS * 4 <= QNBUF * QBUF * 16, "the epilogue transpose must fit the LDS buffers");
         int32_t *T = reinterpret_cast<int32_t *>(smem);
@@ -1226,11 +1272,7 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
             for (int k = 0; k < TR * 64 / 256; ++k) {
                 const int idx = tid + 256 * k;        // 64 rows x 64 column quads
                 const int rl = idx >> 6, cq = idx & 63;
-                const int j0 = tw * 256 + 4 * cq;
-                if (j0 >= g.N) continue;
-                const int4 q = *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]);
-                const int32_t P[4] = {q.x, q.y, q.z, q.w};
-                mdecode4<BIP>(P, tp * 256 + TR * h + rl, j0, min(4, g.N - j0), b, g, lay, ws);
+                d_decode4<BIP>(dl, *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]), TR * h + rl, cq, tw, b, g);
             }
         }
     }
@@ -1665,9 +1707,7 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     constexpr bool TABLES = !MASK && !NARROW;         // tables masked to row lengths
     __shared__ u4 lut[(TABLES ? 2 : 1) * 256 * 16];   // 64 or 128 KB; the epilogue's transpose reuses it
     __shared__ uint32_t rems[TABLES ? RGROUPS : 1];   // bit r of rems[G]: a row ends r cycles into group G
-    // what the decode of a whole tile needs (filled after the chunk loop)
-    __shared__ int32_t d_row[256], d_len[256];
-    __shared__ float d_scale[256], d_sB[256];
+    __shared__ DecodeLds dl;                          // filled after the chunk loop
     if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
     const int NTW = lay.NT / 2;
     int F, SS;
@@ -1774,33 +1814,13 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     }
 
     if (split) {
-        // a part stores its int32 partial sums (rows of 256 columns) for the split sum: one
-        // lane offset, the element's offset in a scalar register
-        const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
-            ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256, 0, 256 * 256 * 4, 0x00020000);
-        const int voff = ((wr + 4 * grp) * 256 + wc + i32) * 4;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int c = 0; c < NB; ++c)
-#pragma unroll
-                for (int e = 0; e < 16; ++e)
-                    __builtin_amdgcn_raw_buffer_store_b32((uint32_t)(int32_t)acc[i][c][e], pr, voff,
-                                                          ((32 * i + 8 * (e >> 2) + (e & 3)) * 256 + 32 * c) * 4, 0);
+        store_part<NB>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256, wr, wc, grp, i32);
         return;
     }
-    // a whole tile decodes: first what the decode needs per row of the pair (original row or
-    // -1 for padding, length, scale times 127^2) and per column (scale) into LDS, then the
-    // sums are transposed through LDS, 32 rows at a time, so that each thread decodes four
-    // adjacent columns of one row
-    for (int r = tid; r < 256; r += NT) {
-        const int i = perm[r];
-        d_row[r] = i;
-        d_len[r] = i >= 0 ? Ls[r] : 0;
-        d_scale[r] = i >= 0 ? g.sA[(size_t)b * g.strideSA + i] * 16129.0f : 0.0f;
-        const int j = tw * 256 + r;
-        d_sB[r] = j < g.N ? g.sB[(size_t)b * g.strideSB + j] : 0.0f;
-    }
+    // a whole tile decodes: the rows' and columns' data staged in LDS, the sums transposed
+    // through LDS, 32 rows at a time, so that each thread decodes four adjacent columns of
+    // one row
+    d_stage<NT>(dl, perm, Ls, b, tw, g, tid);
     constexpr int TS = 256 + 4, TR = 32;
     static_assert(TR * TS * 4 <= 256 * 16 * 16, "the epilogue transpose must fit the table");
     int32_t *T = reinterpret_cast<int32_t *>(lut);
@@ -1823,16 +1843,8 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
 #pragma unroll
         for (int k = 0; k < TR * NQ / NT; ++k) {
             const int idx = tid + NT * k;         // 32 rows x NQ column quads
-            const int rl = idx / NQ, cq = idx % NQ, r = TR * h + rl;
-            const int j0 = tw * 256 + 4 * cq;
-            if (j0 >= g.N || d_row[r] < 0) continue;
-            const int4 qv = *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]);
-            const int32_t P[4] = {qv.x, qv.y, qv.z, qv.w};
-            const int ncol = min(4, g.N - j0);
-            float sBj[4];
-#pragma unroll
-            for (int c = 0; c < 4; ++c) sBj[c] = d_sB[4 * cq + (c < ncol ? c : 0)];
-            mdecode4_store<BIP>(P, d_row[r], d_len[r], d_scale[r], sBj, j0, ncol, b, g);
+            const int rl = idx / NQ, cq = idx % NQ;
+            d_decode4<BIP>(dl, *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]), TR * h + rl, cq, tw, b, g);
         }
     }
 }
