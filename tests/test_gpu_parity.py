@@ -188,6 +188,24 @@ def test_longest_streams(dev, oracle_mod, polarity, engine):
     _compare(g, 0, np.arange(300), np.arange(270), out, cnt, oracle_mod, "Lmax%d pol%d" % (g.L_max, polarity))
 
 
+@pytest.mark.parametrize("polarity", [0, 1])
+def test_split_partials_extreme(dev, oracle_mod, polarity):
+    # ViT-B fc1's shape (its last 44 tiles are split along k) with constant operands, so that
+    # the parts' partial sums reach their largest magnitudes (every product +1 or -1), of both
+    # signs across columns.  Equal rows of equal length give equal counts, which checks every
+    # row; sampled rows, most in the split tiles, go against the oracle.
+    M, N, K, L = 6304, 3072, 768, 128
+    rng = np.random.default_rng(301 + polarity)
+    g = W.random_gemm(rng, 1, M, N, K, L, polarity, 301 + polarity, uniform_L=L)
+    g.A[:] = 127
+    g.B[:] = np.where(np.arange(N)[:, None] % 2 == 0, 127, -127).astype(np.int8)
+    _note("split partials extreme polarity %d" % polarity)
+    out, cnt = _run(g, dev)
+    assert np.array_equal(cnt[0], np.broadcast_to(cnt[0][:1], cnt[0].shape))
+    rows = np.union1d(_sample(M, rng, 4), [0, 5375, 5376, 5600, 5900, 6200, 6303])
+    _compare(g, 0, rows, np.arange(N), out, cnt, oracle_mod, "extreme pol%d" % polarity)
+
+
 @pytest.mark.parametrize("name", ["vitb16_fc1_L128", "vitb16_fc1_mp64", "ditxl2_proj_mlp_group96"])
 def test_engines_agree_full_size(dev, name):
     # Every output of the full-size layers: the MFMA engine (256 x 256 tiles, whole tiles
