@@ -1429,16 +1429,20 @@ __global__ __launch_bounds__(256) void k_rchunks(RChunkArgs a, uint8_t *ws) {
             if (a.vec[side] && d0 + 16 <= a.K) {
                 v = *reinterpret_cast<const u4 *>(xrow + d0);
             } else {
+                // any byte alignment: the five aligned dwords that cover the 16 bytes, each
+                // loaded only when it holds a byte of the row before K (an aligned dword never
+                // crosses a page, so it is readable when one of its bytes is), then shifted
+                // into place; bytes at or past K are replaced below
+                const uintptr_t p = reinterpret_cast<uintptr_t>(xrow + d0);
+                const uintptr_t end = reinterpret_cast<uintptr_t>(xrow + a.K);
+                const uint32_t *w = reinterpret_cast<const uint32_t *>(p & ~(uintptr_t)3);
+                uint32_t wv[5];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    uint32_t w = 0;
+                for (int k = 0; k < 5; ++k)
+                    wv[k] = reinterpret_cast<uintptr_t>(w + k) < end ? w[k] : 0x80808080u;
+                const uint32_t sh = (uint32_t)(p & 3);
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int d = d0 + 4 * k + j;
-                        w |= (uint32_t)(d < a.K ? (uint8_t)xrow[d] : (uint8_t)RPAD) << (8 * j);
-                    }
-                    v[k] = w;
-                }
+                for (int k = 0; k < 4; ++k) v[k] = __builtin_amdgcn_alignbyte(wv[k + 1], wv[k], sh);
             }
 #pragma unroll
             for (int k = 0; k < 4; ++k) v[k] = r_clamp4(v[k]);

@@ -430,11 +430,12 @@ def test_strided_interleaved_heads(dev, oracle_mod):
         assert np.max(np.abs(oo[nz] - o_ref[nz]) / np.abs(o_ref[nz])) <= 1e-6
 
 
+@pytest.mark.parametrize("shift", [(0, 0), (1, 3)], ids=["aligned", "odd_bases"])
 @pytest.mark.parametrize("polarity", [0, 1])
-def test_rgen_strided(dev, oracle_mod, polarity):
+def test_rgen_strided(dev, oracle_mod, polarity, shift):
     """The int8-chunk GEMM on strided operands: A rows padded to a multiple of 16 bytes
-    (16-byte chunk loads), B rows at an odd stride (bytewise), a wider output row stride,
-    two batch entries with their own strides."""
+    (16-byte chunk loads unless A's base is odd), B rows at an odd stride (loads at any byte
+    alignment), a wider output row stride, two batch entries with their own strides."""
     import torch
     import paper_2609_32922_amd as scg
     rng = np.random.default_rng(71 + polarity)
@@ -460,13 +461,14 @@ def test_rgen_strided(dev, oracle_mod, polarity):
     ws = scg.Workspace(scg.sc_gemm_workspace_size(d), dev)
     _note("int8-chunk GEMM strided polarity %d" % polarity)
     sh = int(torch.cuda.current_stream().cuda_stream)
-    rc = scg.sc_gemm(d, tA.data_ptr(), tsa.data_ptr(), tB.data_ptr(), tsb.data_ptr(), tL.data_ptr(),
+    oa, ob = shift                              # byte offsets of A's and B's bases
+    rc = scg.sc_gemm(d, tA.data_ptr() + oa, tsa.data_ptr(), tB.data_ptr() + ob, tsb.data_ptr(), tL.data_ptr(),
                      out.data_ptr(), cnt.data_ptr(), ws.ptr, ws.nbytes, sh)
     assert rc == 0 and scg.sc_gemm_status(ws.ptr, sh) == 0
     c, o = cnt.cpu().numpy(), out.cpu().numpy()
     for b in range(batch):
-        A = np.stack([Abuf[b * sA_ + i * lda: b * sA_ + i * lda + K] for i in range(M)])
-        B = np.stack([Bbuf[b * sB_ + j * ldb: b * sB_ + j * ldb + K] for j in range(N)])
+        A = np.stack([Abuf[oa + b * sA_ + i * lda: oa + b * sA_ + i * lda + K] for i in range(M)])
+        B = np.stack([Bbuf[ob + b * sB_ + j * ldb: ob + b * sB_ + j * ldb + K] for j in range(N)])
         c_ref, o_ref = oracle_mod.sc_gemm(A, B, sa[b], sb[b], L[b], L_max, polarity, 171)
         cg = np.stack([c[b * sO_ + i * ldo: b * sO_ + i * ldo + N] for i in range(M)])
         og = np.stack([o[b * sO_ + i * ldo: b * sO_ + i * ldo + N] for i in range(M)]).astype(np.float64)
