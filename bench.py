@@ -92,8 +92,8 @@ def main():
         copy_probe(args.copy_probe)
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build runs the SC GEMM on a single "
-              "MI355X (rows shard across GPUs with no collective; see DESIGN.md)",
+        print("bench.py measures one GPU only (--gpus 1): the SC GEMM runs on a single MI355X; "
+              "across GPUs the rows of A would shard with no collective",
               file=sys.stderr)
         sys.exit(2)
     import torch

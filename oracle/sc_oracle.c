@@ -25,7 +25,7 @@
  *     indexed by boundary and cycle only).
  *   - Sec. A.1: LFSRs are the plain PRNG option for the comparator sequence.
  *
- * Readings taken where the paper is silent (each one is listed in the design doc):
+ * Readings taken where the paper is silent:
  *   R-LFSR   32-bit Galois LFSR, right shift, feedback mask 0x80200003, i.e. the
  *            polynomial x^32+x^22+x^2+x+1 (primitive, so the period is 2^32-1).  One draw is 8
  *            steps; the 8 output bits form a byte, first output bit most significant.
