@@ -310,16 +310,22 @@ int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const in
     uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
 
     uint32_t *rA = reinterpret_cast<uint32_t *>(ws + lay.off_rA);
-    hipError_t e = launch_draws(d.seed, d.rng, lay.LBS, rA,
-                                reinterpret_cast<uint32_t *>(ws + lay.off_rB), nullptr, -1,
-                                reinterpret_cast<uint32_t *>(ws + lay.off_status), st);
-    if (e != hipSuccess) return SC_ERR_HIP;
-    if (d.batch == 0 || d.M == 0 || d.N == 0) return SC_OK;
+    // one batch entry with LFSR sequences: the scheduler's single block also clears the
+    // status and makes the sequences (one launch fewer); otherwise k_draws does, first
+    const bool empty = d.batch == 0 || d.M == 0 || d.N == 0;
+    const bool fuse = !empty && d.batch == 1 && d.rng == SC_RNG_LFSR32;
+    hipError_t e = hipSuccess;
+    if (!fuse) {
+        e = launch_draws(d.seed, d.rng, lay.LBS, rA, reinterpret_cast<uint32_t *>(ws + lay.off_rB), nullptr, -1,
+                         reinterpret_cast<uint32_t *>(ws + lay.off_status), st);
+        if (e != hipSuccess) return SC_ERR_HIP;
+    }
+    if (empty) return SC_OK;
 
     if (d.rng == SC_RNG_SOBOL8_CBSG &&
         launch_cbsg_table(rA, d.L_max, reinterpret_cast<uint16_t *>(ws + lay.off_CA), st) != hipSuccess)
         return SC_ERR_HIP;
-    if ((e = launch_schedule(d, lay, L_per_row, ws, st)) != hipSuccess) return SC_ERR_HIP;
+    if ((e = launch_schedule(d, lay, L_per_row, ws, fuse, st)) != hipSuccess) return SC_ERR_HIP;
     const bool mfma = lay.engine == SC_ENGINE_MFMA;
     if (!mfma && lay.mode == MODE_AND && (e = launch_marginals(d, lay, A, B, ws, st)) != hipSuccess)
         return SC_ERR_HIP;

@@ -156,8 +156,9 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay);
 hipError_t launch_draws(uint64_t seed, int rng, int n, uint32_t *rA, uint32_t *rB,
                         uint8_t *bytes_out, int op_only, uint32_t *status, hipStream_t st);
 hipError_t launch_cbsg_table(const uint32_t *rA, int L_max, uint16_t *CA, hipStream_t st);
+// draws: also clear the status words and make the comparator sequences (one batch entry only)
 hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L,
-                           uint8_t *ws, hipStream_t st);
+                           uint8_t *ws, bool draws, hipStream_t st);
 hipError_t launch_marginals(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,
                             const int8_t *B, uint8_t *ws, hipStream_t st);
 hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,

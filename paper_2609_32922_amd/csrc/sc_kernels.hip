@@ -95,17 +95,8 @@ constexpr SobolDirs make_sobol_dirs() {
 }
 __constant__ SobolDirs kSobol = make_sobol_dirs();
 
-__global__ __launch_bounds__(256) void k_draws(uint64_t seed, int rng, int n, uint32_t *rA,
-                                               uint32_t *rB, uint8_t *bytes_out, int op_only,
-                                               uint32_t *status) {
-    const int l = blockIdx.x * blockDim.x + threadIdx.x;
-    const int op = op_only >= 0 ? op_only : (int)blockIdx.y;
-    if (status != nullptr && l == 0 && blockIdx.y == 0) {
-        status[0] = 0u;
-        status[1] = 0u;   // longest tile pair of the call
-        status[2] = 0u;   // some row pair holds more lengths inside a cycle group than tables
-    }
-    if (l >= n) return;
+// Draw l of operand op (0: A, 1: B) of the comparator sequence.
+__device__ __forceinline__ uint32_t draw_value(uint64_t seed, int rng, int op, int l) {
     const uint64_t h = splitmix64(2ull * seed + (uint64_t)op);
     uint32_t v = 0;
     if (rng == SC_RNG_SOBOL8_CBSG) {
@@ -124,6 +115,21 @@ __global__ __launch_bounds__(256) void k_draws(uint64_t seed, int rng, int n, ui
             s = (s >> 1) ^ ((s & 1u) ? kFeedback : 0u);
         }
     }
+    return v;
+}
+
+__global__ __launch_bounds__(256) void k_draws(uint64_t seed, int rng, int n, uint32_t *rA,
+                                               uint32_t *rB, uint8_t *bytes_out, int op_only,
+                                               uint32_t *status) {
+    const int l = blockIdx.x * blockDim.x + threadIdx.x;
+    const int op = op_only >= 0 ? op_only : (int)blockIdx.y;
+    if (status != nullptr && l == 0 && blockIdx.y == 0) {
+        status[0] = 0u;
+        status[1] = 0u;   // longest tile pair of the call
+        status[2] = 0u;   // some row pair holds more lengths inside a cycle group than tables
+    }
+    if (l >= n) return;
+    const uint32_t v = draw_value(seed, rng, op, l);
     if (bytes_out != nullptr)
         bytes_out[l] = (uint8_t)v;
     else
@@ -238,7 +244,8 @@ __device__ int wave_bucket_add(int *hist, int l, bool active) {
 }
 
 __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L, int64_t strideL,
-                                                   int M, int L_max, Layout lay, uint8_t *ws) {
+                                                   int M, int L_max, Layout lay, uint8_t *ws, uint64_t seed,
+                                                   int rng, int ndraws) {
     __shared__ int hist[SC_L_MAX_LIMIT + 1];
     const int b = blockIdx.x, tid = threadIdx.x;
     uint8_t *wsb = ws + (size_t)b * lay.stride_batchA;
@@ -250,6 +257,20 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     uint32_t *status = ws_ptr<uint32_t>(ws, lay.off_status);
     const int32_t *Lb = L + (size_t)b * strideL;
 
+    if (ndraws > 0) {
+        // one batch entry: this block also clears the status words and makes the comparator
+        // sequences (the work of k_draws), before any of its own status updates
+        if (tid == 0) {
+            status[0] = 0u;
+            status[1] = 0u;
+            status[2] = 0u;
+        }
+        uint32_t *rA = ws_ptr<uint32_t>(ws, lay.off_rA), *rB = ws_ptr<uint32_t>(ws, lay.off_rB);
+        for (int l = tid; l < ndraws; l += 1024) {
+            rA[l] = draw_value(seed, rng, 0, l);
+            rB[l] = draw_value(seed, rng, 1, l);
+        }
+    }
     for (int v = tid; v <= L_max; v += 1024) hist[v] = 0;
     __syncthreads();
     // Up to SREG * 1024 rows the lengths are loaded once, all loads in flight together, and
@@ -396,9 +417,10 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 }
 
 hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L, uint8_t *ws,
-                           hipStream_t st) {
+                           bool draws, hipStream_t st) {
+    if (draws && d.batch != 1) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_schedule, dim3((unsigned)d.batch), dim3(1024), 0, st, L, d.strideL, d.M,
-                       d.L_max, lay, ws);
+                       d.L_max, lay, ws, d.seed, d.rng, draws ? lay.LBS : 0);
     return hipGetLastError();
 }
 
