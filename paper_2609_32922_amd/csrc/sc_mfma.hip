@@ -1397,8 +1397,46 @@ struct RChunkArgs {
     size_t off_r[2], off_rtab;
 };
 
-// Chunks of both operands: thread = (row r of the tile order, half h) of chunk blockIdx.y,
-// side and batch entry from blockIdx.z; each thread copies one 16-byte half.
+// One 16-byte half of a chunk: bytes d0 .. d0 + 15 of row xrow (K bytes; null: a padding
+// row), clamped to [-127, 127], 0x80 past K.
+__device__ __forceinline__ u4 r_half(const int8_t *xrow, int d0, int K, bool vec) {
+    u4 v = u4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
+    if (xrow == nullptr || d0 >= K) return v;
+    if (vec && d0 + 16 <= K) {
+        v = *reinterpret_cast<const u4 *>(xrow + d0);
+    } else {
+        // any byte alignment: the five aligned dwords that cover the 16 bytes, each loaded
+        // only when it holds a byte of the row before K (an aligned dword never crosses a
+        // page, so it is readable when one of its bytes is), then shifted into place; bytes
+        // at or past K are replaced below
+        const uintptr_t p = reinterpret_cast<uintptr_t>(xrow + d0);
+        const uintptr_t end = reinterpret_cast<uintptr_t>(xrow + K);
+        const uint32_t *w = reinterpret_cast<const uint32_t *>(p & ~(uintptr_t)3);
+        uint32_t wv[5];
+#pragma unroll
+        for (int k = 0; k < 5; ++k) wv[k] = reinterpret_cast<uintptr_t>(w + k) < end ? w[k] : 0x80808080u;
+        const uint32_t sh = (uint32_t)(p & 3);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = __builtin_amdgcn_alignbyte(wv[k + 1], wv[k], sh);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = r_clamp4(v[k]);
+    if (d0 + 16 > K) {          // the elements past K keep the padding byte
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (d0 + 4 * k + j >= K) v[k] = (v[k] & ~(0xFFu << (8 * j))) | ((uint32_t)RPAD << (8 * j));
+    }
+    return v;
+}
+
+// Chunks of both operands, through LDS: a block takes 64 rows (of the tile order) x 8 chunks
+// (256 bytes of each row).  It reads them row by row, 16 lanes per row (coalesced along the
+// row), into LDS as [chunk][row][half], then writes each chunk's 64 rows x 32 bytes, which are
+// contiguous in the chunk layout.  Side and batch entry from blockIdx.z.
+constexpr int RC_ROWS = 64, RC_CH = 8;
+constexpr int RC_CSTRIDE = RC_ROWS * 2 + 1;      // u4 per chunk in LDS (+1: banks shift by chunk)
 __global__ __launch_bounds__(256) void k_rchunks(RChunkArgs a, uint8_t *ws) {
     if (blockIdx.z == (unsigned)(a.nb[0] + a.nb[1])) {
         // the last slice of the grid builds the tables of every cycle group
@@ -1411,50 +1449,28 @@ __global__ __launch_bounds__(256) void k_rchunks(RChunkArgs a, uint8_t *ws) {
         }
         return;
     }
+    __shared__ u4 sm[RC_CH * RC_CSTRIDE];
     const int side = blockIdx.z >= (unsigned)a.nb[0];
     const int b = side ? blockIdx.z - a.nb[0] : blockIdx.z;
-    const int t = blockIdx.x * 256 + threadIdx.x;
-    const int r = t >> 1, h = t & 1;
-    if (r >= a.rows_pad[side]) return;
+    const int r0 = blockIdx.x * RC_ROWS, c0 = blockIdx.y * RC_CH;
+    if (r0 >= a.rows_pad[side]) return;                 // (uniform over the block)
+    const int nc = min(RC_CH, a.KC - c0);
     uint8_t *wsb = ws + (size_t)b * a.stride_batch[side];
-    const int src = side == 0 ? ws_ptr<int32_t>(wsb, a.off_perm)[r] : (r < a.rows[side] ? r : -1);
-    const int8_t *xrow = src >= 0 ? a.X[side] + (size_t)b * a.strideX[side] + (size_t)src * a.ld[side] : nullptr;
-    u4 *out = reinterpret_cast<u4 *>(ws_ptr<uint8_t>(wsb, a.off_out[side])) + (size_t)(r >> 8) * a.KC * 512 +
-              (r & 255) * 2 + h;
-    {
-        const int c = blockIdx.y;
-        const int d0 = c * RCH + 16 * h;
-        u4 v = u4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
-        if (xrow != nullptr && d0 < a.K) {
-            if (a.vec[side] && d0 + 16 <= a.K) {
-                v = *reinterpret_cast<const u4 *>(xrow + d0);
-            } else {
-                // any byte alignment: the five aligned dwords that cover the 16 bytes, each
-                // loaded only when it holds a byte of the row before K (an aligned dword never
-                // crosses a page, so it is readable when one of its bytes is), then shifted
-                // into place; bytes at or past K are replaced below
-                const uintptr_t p = reinterpret_cast<uintptr_t>(xrow + d0);
-                const uintptr_t end = reinterpret_cast<uintptr_t>(xrow + a.K);
-                const uint32_t *w = reinterpret_cast<const uint32_t *>(p & ~(uintptr_t)3);
-                uint32_t wv[5];
-#pragma unroll
-                for (int k = 0; k < 5; ++k)
-                    wv[k] = reinterpret_cast<uintptr_t>(w + k) < end ? w[k] : 0x80808080u;
-                const uint32_t sh = (uint32_t)(p & 3);
-#pragma unroll
-                for (int k = 0; k < 4; ++k) v[k] = __builtin_amdgcn_alignbyte(wv[k + 1], wv[k], sh);
-            }
-#pragma unroll
-            for (int k = 0; k < 4; ++k) v[k] = r_clamp4(v[k]);
-            if (d0 + 16 > a.K) {          // the elements past K keep the padding byte
-#pragma unroll
-                for (int k = 0; k < 4; ++k)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        if (d0 + 4 * k + j >= a.K) v[k] = (v[k] & ~(0xFFu << (8 * j))) | ((uint32_t)RPAD << (8 * j));
-            }
-        }
-        out[(size_t)c * 512] = v;
+    const int tid = threadIdx.x, hl = tid & 15;         // hl = 2 * chunk + half
+    const bool vec = a.vec[side] != 0;
+    for (int pass = 0; pass < RC_ROWS / 16; ++pass) {
+        const int rl = pass * 16 + (tid >> 4), r = r0 + rl;
+        if ((hl >> 1) >= nc) continue;
+        const int src = side == 0 ? ws_ptr<int32_t>(wsb, a.off_perm)[r] : (r < a.rows[side] ? r : -1);
+        const int8_t *xrow = src >= 0 ? a.X[side] + (size_t)b * a.strideX[side] + (size_t)src * a.ld[side] : nullptr;
+        sm[(hl >> 1) * RC_CSTRIDE + rl * 2 + (hl & 1)] = r_half(xrow, (c0 + (hl >> 1)) * RCH + 16 * (hl & 1), a.K, vec);
+    }
+    __syncthreads();
+    u4 *out = reinterpret_cast<u4 *>(ws_ptr<uint8_t>(wsb, a.off_out[side])) + (size_t)(r0 >> 8) * a.KC * 512 +
+              (r0 & 255) * 2;
+    for (int k = tid; k < nc * RC_ROWS * 2; k += 256) {
+        const int c = k / (RC_ROWS * 2), e = k % (RC_ROWS * 2);
+        out[(size_t)(c0 + c) * 512 + e] = sm[c * RC_CSTRIDE + e];
     }
 }
 
@@ -1489,7 +1505,7 @@ hipError_t launch_rchunks(const sc_gemm_desc &d, const Layout &lay, const int8_t
     a.off_r[1] = lay.off_rB;
     a.off_rtab = lay.off_rtab;
     const int rows = a.rows_pad[0] > a.rows_pad[1] ? a.rows_pad[0] : a.rows_pad[1];
-    hipLaunchKernelGGL(k_rchunks, dim3((unsigned)((2 * rows + 255) / 256), (unsigned)lay.KC,
+    hipLaunchKernelGGL(k_rchunks, dim3((unsigned)((rows + RC_ROWS - 1) / RC_ROWS), (unsigned)((lay.KC + RC_CH - 1) / RC_CH),
                                        (unsigned)(d.batch + lay.nbB + 1)),
                        dim3(256), 0, st, a, ws);
     return hipGetLastError();
