@@ -1278,51 +1278,70 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
     }
 }
 
-// sums the partial counts of every part of the split tiles F.. and decodes (eight blocks
-// per tile, 32 rows each; thread = row x four adjacent columns)
-template <bool BIP>
+// sums the partial counts of every part of the split tiles F.. and decodes (256 / QR_ROWS
+// blocks per tile of QR_ROWS rows each; thread = row x four adjacent columns).  8-row blocks
+// when few tiles are split, so that enough waves keep loads in flight; 32-row blocks when many
+// are (less per-block overhead).
+template <bool BIP, int QR_ROWS>
 __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, uint8_t *ws) {
-    constexpr int NK = 32 * 64 / 256;
+    constexpr int NK = QR_ROWS * 64 / 256;    // column quads per thread
+    constexpr int BPT = 256 / QR_ROWS;        // blocks per tile
     const int NTW = lay.NT / 2;
     int F, SS;
     q_division(g, lay, ws, F, SS);
-    const int tile = F + (blockIdx.x >> 3), part8 = blockIdx.x & 7;
+    const int tile = F + (int)(blockIdx.x / BPT), part = (int)(blockIdx.x % BPT);
     if (tile >= g.batch * (lay.MT / 2) * NTW) return;
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
     const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part) +
                                                       (size_t)(tile - F) * SS * 256 * 256) +
-                       (size_t)part8 * 32 * 64 + threadIdx.x;
+                       (size_t)part * QR_ROWS * 64 + threadIdx.x;
+    // a thread keeps NK column quads; quads past N hold nothing to sum (nor, in the 64-column
+    // blocks, anything written).  Every part's loads are issued before any sum.
+    const bool colok = tw * 256 + 4 * (int)(threadIdx.x & 63) < g.N;
+    const int ns = colok ? SS : 0;
+    // (8-row blocks: every part's loads in flight at once; 32-row blocks: one part at a time)
+    constexpr int SB = NK <= 2 ? MAX_SPLIT : 1;
     int4 sum[NK];
 #pragma unroll
     for (int k = 0; k < NK; ++k) sum[k] = make_int4(0, 0, 0, 0);
-    // a thread keeps one column quad; quads past N hold nothing to sum (nor, in the 64-column
-    // blocks, anything written)
-    const bool colok = tw * 256 + 4 * (int)(threadIdx.x & 63) < g.N;
-    for (int s = 0; s < (colok ? SS : 0); ++s) {
-        const int4 *src = base + (size_t)s * 256 * 64;
-        int4 q[NK];
+    for (int s0 = 0; s0 < ns; s0 += SB) {
+        int4 q[SB][NK];
 #pragma unroll
-        for (int k = 0; k < NK; ++k) q[k] = src[256 * k];
+        for (int s = 0; s < SB; ++s)
 #pragma unroll
-        for (int k = 0; k < NK; ++k) {
-            sum[k].x += q[k].x;
-            sum[k].y += q[k].y;
-            sum[k].z += q[k].z;
-            sum[k].w += q[k].w;
-        }
+            for (int k = 0; k < NK; ++k)
+                q[s][k] = s0 + s < ns ? base[(size_t)(s0 + s) * 256 * 64 + 256 * k] : make_int4(0, 0, 0, 0);
+#pragma unroll
+        for (int s = 0; s < SB; ++s)
+#pragma unroll
+            for (int k = 0; k < NK; ++k) {
+                sum[k].x += q[s][k].x;
+                sum[k].y += q[s][k].y;
+                sum[k].z += q[s][k].z;
+                sum[k].w += q[s][k].w;
+            }
     }
     const int32_t *perm = ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_perm);
 #pragma unroll
     for (int k = 0; k < NK; ++k) {
         const int idx = threadIdx.x + 256 * k;
-        const int rl = part8 * 32 + (idx >> 6), cq = idx & 63;
+        const int rl = part * QR_ROWS + (idx >> 6), cq = idx & 63;
         const int j0 = tw * 256 + 4 * cq;
         if (j0 >= g.N || perm[tp * 256 + rl] < 0) continue;
         const int32_t P[4] = {sum[k].x, sum[k].y, sum[k].z, sum[k].w};
         mdecode4<BIP>(P, tp * 256 + rl, j0, min(4, g.N - j0), b, g, lay, ws);
     }
+}
+
+template <bool BIP>
+static hipError_t launch_qreduce(const MGemmArgs &g, const Layout &lay, uint8_t *ws, unsigned tail, hipStream_t st) {
+    if (tail * 8u < 1024u)
+        hipLaunchKernelGGL((k_qgemm_reduce<BIP, 8>), dim3(tail * 32u), dim3(256), 0, st, g, lay, ws);
+    else
+        hipLaunchKernelGGL((k_qgemm_reduce<BIP, 32>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
+    return hipGetLastError();
 }
 
 template <bool BIP>
@@ -1333,8 +1352,7 @@ static hipError_t launch_qgemm(const MGemmArgs &g, const Layout &lay, uint8_t *w
                        lay, ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || tail == 0) return e;
-    hipLaunchKernelGGL((k_qgemm_reduce<BIP>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
-    return hipGetLastError();
+    return launch_qreduce<BIP>(g, lay, ws, tail, st);
 }
 
 // ----------------------------------------------------------------------------
@@ -1880,8 +1898,7 @@ static hipError_t launch_rgemm_w(const MGemmArgs &g, const Layout &lay, uint8_t 
     hipLaunchKernelGGL((k_rgemm<BIP, true, NARROW>), grid, block, 0, st, g, lay, ws);
     e = hipGetLastError();
     if (e != hipSuccess || tail == 0) return e;
-    hipLaunchKernelGGL((k_qgemm_reduce<BIP>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
-    return hipGetLastError();
+    return launch_qreduce<BIP>(g, lay, ws, tail, st);
 }
 
 template <bool BIP>
