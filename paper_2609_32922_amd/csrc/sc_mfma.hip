@@ -23,20 +23,25 @@
 //                 in LDS from the int8 rows (an 8-cycle table per octet indexed by the int8
 //                 byte), so no planes are written or read
 //   k_rchunks     int8 operands (A in the scheduler's row order) laid out in 32-element
-//                 chunks per 256-row pair, the input of k_rgemm
+//                 chunks per 256-row pair through LDS (rows read along, chunks written
+//                 contiguous), the input of k_rgemm; its last grid slice builds the table
+//                 entries of every 32-cycle group once per call
 //   k_rgemm       M > 128 and N > 128 (or N <= 64) with comparator streams: the tiles and
 //                 division of k_qgemm, but every fp4 fragment is one LDS table read (a table
 //                 per 32-cycle group indexed by the int8 byte), so no planes exist and the
 //                 loop has no stage buffers; rows ending inside a group read tables masked
 //                 to their length (a second variant masks every fragment when a row pair
-//                 holds too many such lengths); for N <= 64 blocks of 256 x 64, two per CU
+//                 holds too many such lengths); for N <= 64 blocks of 256 x 64, two per CU.
+//                 A block copies each group's table entries into LDS (prefetched during
+//                 the previous group); a whole tile decodes from row and column data
+//                 staged in LDS, a part stores int32 partial sums
 //   k_qgemm       N > 128 and M > 128 with C-BSG streams: 256x256 output tile per
 //                 256-thread block, one block per CU, 128x128 per wave as 4x4 32x32 MFMA
 //                 blocks, three LDS buffers of 4 slots (96 KB), memory instructions
 //                 interleaved one per MFMA.  Whole tiles in full rounds, the tiles of a last
 //                 partial round (or every tile, when row lengths vary) split along k.
 //   k_qgemm_reduce sums the partial counts of the split tiles of k_qgemm or k_rgemm and
-//                 decodes
+//                 decodes (8-row blocks when few tiles are split, 32-row blocks otherwise)
 //   k_mgemm       the rest (M <= 128, or N <= 128 with C-BSG streams): 128x256 output
 //                 tile per 256-thread block (128x128 and 64x64 when N <= 128), 64x128 per
 //                 wave as 2x4 32x32 MFMA blocks, 4 slots (2 MFMA k-steps of 64) per LDS
