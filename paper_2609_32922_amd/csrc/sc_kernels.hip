@@ -3,7 +3,8 @@
 // Pipeline of one sc_gemm call (all on the caller's stream):
 //   k_draws      comparator sequences r^A, r^B (Sec. 3.1 "Bitstream generation",
 //                LFSR or scrambled Sobol-8 of Sec. A.1) -- one lane per cycle, the LFSR
-//                through jump-ahead
+//                through jump-ahead; it also clears the status words.  With one batch
+//                entry and LFSR sequences k_schedule does both instead (one launch fewer)
 //   k_cbsg_table C-BSG only: CA[L][beta] = ones of A's stream in its first L cycles
 //   k_schedule   per-row length scheduler: validates L_i, counting-sorts rows by L
 //                (descending) so that a 128-row tile runs for the longest length it
