@@ -144,6 +144,30 @@ def sc_gemm(A: np.ndarray, B: np.ndarray, sA: np.ndarray, sB: np.ndarray,
     return counts, out
 
 
+def decode(counts: np.ndarray, sA: np.ndarray, sB: np.ndarray, L: np.ndarray, K: int,
+           polarity: int) -> np.ndarray:
+    """Eq. (1) (Sec. 3.1, "SC matrix multiplication") applied to a count matrix, float64.
+
+    counts [M, N] int: X_ij (bipolar XNOR counts) or S_ij (unipolar signed AND counts).
+    Bipolar  out_ij = sA_i sB_j 127^2 (2 X_ij / L_i - K); unipolar out_ij = sA_i sB_j 127^2
+    S_ij / L_i; a row with L_i = 0 decodes to 0.  The same formula, in the same order of
+    operations, as the decode inside ``sc_gemm``, written out element-wise in numpy so it
+    can be applied to any count matrix.
+    """
+    c = np.asarray(counts, dtype=np.float64)
+    M, N = c.shape
+    a = np.asarray(sA, dtype=np.float32).astype(np.float64).reshape(M, 1)
+    b = np.asarray(sB, dtype=np.float32).astype(np.float64).reshape(1, N)
+    Li = np.asarray(L, dtype=np.int64).reshape(M, 1)
+    scale = a * b * float(127 * 127)
+    Ld = np.where(Li > 0, Li, 1).astype(np.float64)
+    if polarity == 0:
+        out = scale * (2.0 * c / Ld - float(K))
+    else:
+        out = scale * c / Ld
+    return np.where(Li > 0, out, 0.0)
+
+
 def sobol_shift(seed: int, op: int) -> int:
     return int(_load().oracle_sobol_shift(ctypes.c_uint64(seed), op))
 

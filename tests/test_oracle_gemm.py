@@ -47,6 +47,48 @@ def test_matches_pure_python_bruteforce(oracle_mod, polarity):
                     assert abs(Fraction(o[i, j]) - exact) <= abs(exact) * Fraction(1, 10**14)
 
 
+@pytest.mark.parametrize("polarity", [BIP, UNI])
+def test_decode_matches_exact_rational_decode(oracle_mod, polarity):
+    # oracle.decode applied to the brute force's counts against the brute force's exact
+    # rational Eq. (1), and equal to the decode inside the oracle's GEMM
+    rng = np.random.default_rng(140 + polarity)
+    for case in range(30):
+        M, N, K = (int(x) for x in rng.integers(1, 4, 3))
+        L_max = int(rng.choice([0, 1, 5, 32, 33, 64]))
+        A, B, sA, sB, L = _rand_case(rng, M, N, K, L_max)
+        seed = int(rng.integers(0, 2**40))
+        cb, ob = bf.sc_gemm(A.tolist(), B.tolist(), sA.tolist(), sB.tolist(), L.tolist(),
+                            polarity, seed)
+        o = oracle_mod.decode(np.array(cb, np.int32).reshape(M, N), sA, sB, L, K, polarity)
+        for i in range(M):
+            for j in range(N):
+                exact = ob[i][j]
+                if exact == 0:
+                    assert o[i, j] == 0.0
+                else:
+                    assert abs(Fraction(o[i, j]) - exact) <= abs(exact) * Fraction(1, 10**14)
+        c, og = oracle_mod.sc_gemm(A, B, sA, sB, L, L_max, polarity, seed)
+        assert np.array_equal(o, og)
+
+
+def test_decode_closed_forms(oracle_mod):
+    # counts at their extremes decode to +-(scale product) K; the midpoint count to 0;
+    # one count step moves the bipolar decode by 2/L and the unipolar one by 1/L of the scale
+    sA = np.array([0.5, 0.25, 1.0], np.float32)
+    sB = np.array([2.0, 4.0], np.float32)
+    L = np.array([64, 32, 0], np.int32)
+    K = 10
+    X = np.array([[640, 0], [160, 161], [5, 5]], np.int32)
+    o = oracle_mod.decode(X, sA, sB, L, K, BIP)
+    assert o[0, 0] == 0.5 * 2.0 * 16129 * K and o[0, 1] == -0.5 * 4.0 * 16129 * K
+    assert o[1, 0] == 0.0 and o[1, 1] == 0.25 * 4.0 * 16129 * (2.0 / 32)
+    assert np.all(o[2] == 0.0)
+    S = np.array([[64, -64], [1, -1], [3, 3]], np.int32)
+    u = oracle_mod.decode(S, sA, sB, L, K, UNI)
+    assert u[0, 0] == 0.5 * 2.0 * 16129 and u[0, 1] == -0.5 * 4.0 * 16129
+    assert u[1, 0] == 0.25 * 2.0 * 16129 / 32 and np.all(u[2] == 0.0)
+
+
 def test_count_range_and_zero_length(oracle_mod):
     rng = np.random.default_rng(1)
     A, B, sA, sB, L = _rand_case(rng, 9, 7, 37, 70)
