@@ -1,17 +1,17 @@
-"""Benchmark of the MI355X SC GEMM: one step = one full sc_gemm call (comparator
-sequences, row-length scheduler, marginals, stream generation into bit planes,
-packed AND+popcount GEMM and decode) over one batch of synthetic input already
-resident in HBM.
+"""Benchmark of the MI355X SC GEMM: one step = one full sc_gemm call per GEMM of the
+workload (comparator sequences, row-length scheduler, operand layout and per-cycle-group
+stream tables, the counting GEMM on the matrix cores and the decode) over one batch of
+synthetic input already resident in HBM.
 
 Prints ONE JSON line.  ``value`` is whole-call throughput in stream-bit-ops/s
-(N * K * sum_i L_i per step / seconds per step).  ``roofline`` is for the dominant
-kernel (the packed GEMM and, when its tiles are split, the pass that sums the splits),
-timed with HIP events recorded by the library around those launches on the call's
-stream, against the integer-VALU peak for 2 instructions per 32 bit pairs at the
-vector rate of 128 32-bit lane operations per CU per clock (two VALU issues per
-SIMD per quad-cycle, the rate behind the 157.3 TFLOP/s fp32 vector figure):
-256 CUs x 128 lanes x 2.4 GHz x 32 / 2 = 1.258e15 bit-ops/s.
-``cpu_baseline`` times the CPU oracle on a bounded row sample of the same workload.
+(N * K * sum_i L_i per step / seconds per step).  ``roofline`` is for the dominant kernel
+(the counting GEMM of the largest GEMM and, when its tiles are split, the pass that sums
+the splits), timed with HIP events that the library records around exactly those launches
+on the call's stream: one stream-bit-op is one fp4 product on the matrix cores (2 flops),
+against the dense fp4 MFMA peak.  ``valu_bitop_peak`` is the measured rate of the same
+work done as packed words on the vector ALUs (AND + accumulating popcount, 2 instructions
+per 32 bit pairs: libscpeak), with the clock under that load; ``value`` is also given as a
+multiple of it.  ``cpu_baseline`` times the CPU oracle on a bounded row sample.
 """
 import argparse
 import json
@@ -25,9 +25,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "SC stream-bit-ops/sec (M·N·K·L) and % of gfx950 bitop+popcount peak"
-PEAK_BITOPS = 256 * 128 * 2.4e9 * 32 / 2         # 1.2583e15 (dual-issue VALU rate)
-PEAK_SINGLE_ISSUE = 256 * 64 * 2.4e9 * 32 / 2    # 6.2915e14 (one VALU issue per quad-cycle)
-PEAK_FP4_FLOPS = 10.1e15                         # dense fp4 (e2m1) MFMA, MI355X
+PEAK_FP4_FLOPS = 10.1e15                         # dense fp4 (e2m1) MFMA, MI355X (published)
+# the paper's one speed figure for this path (Sec. 4.2): its fused GPU SC matmul against a
+# direct CPU simulation, hardware of both sides not stated
+PAPER_GPU_VS_CPU = 95000.0
 
 
 def parse():
@@ -36,15 +37,14 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="vitb16_fc1_L128")
-    p.add_argument("--engine", choices=("auto", "valu", "mfma"), default="auto",
-                   help="counting engine: packed popcount on the VALUs, or fp4 products on "
-                        "the matrix cores (auto: MFMA while K*L_max <= 2^24)")
     p.add_argument("--rng", choices=("lfsr", "cbsg"), default="lfsr",
                    help="comparator source: 32-bit LFSR, or scrambled Sobol-8 with "
                         "conditional generation of B's stream (C-BSG, L_max <= 256)")
     p.add_argument("--cpu-rows", type=int, default=0,
                    help="rows of A for the oracle sample (0 = size it to ~15 s)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-valu-peak", action="store_true",
+                   help="skip the VALU AND + popcount peak measurement")
     p.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                    help="only run a plain device copy of BYTES bytes (3 times), to calibrate "
                         "the HBM byte counters against a kernel of known traffic")
@@ -102,11 +102,6 @@ def main():
 
     w = W.WORKLOADS[args.workload]()
     rng = scg.SC_RNG_SOBOL8_CBSG if args.rng == "cbsg" else scg.SC_RNG_LFSR32
-    engine = {"auto": scg.SC_ENGINE_AUTO, "valu": scg.SC_ENGINE_VALU,
-              "mfma": scg.SC_ENGINE_MFMA}[args.engine]
-    resolved = {g.name: (engine if engine != scg.SC_ENGINE_AUTO else
-                         (scg.SC_ENGINE_MFMA if g.K * g.L_max <= (1 << 24) else scg.SC_ENGINE_VALU))
-                for g in w.gemms}
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -114,8 +109,7 @@ def main():
     for g in w.gemms:
         t = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (g.A, g.sA, g.B, g.sB, g.L)]
         out = torch.empty((g.batch, g.M, g.N), dtype=torch.float32, device=dev)
-        d = scg.make_desc(t[0], t[2], g.L_max, g.polarity, g.seed, int(round(float(g.L.mean()))),
-                          rng, engine)
+        d = scg.make_desc(t[0], t[2], g.L_max, g.polarity, g.seed, int(round(float(g.L.mean()))), rng)
         ws = scg.Workspace(scg.sc_gemm_workspace_size(d), dev)
         staged.append((g, t, out, ws))
     bitops = w.bitops()
@@ -133,13 +127,14 @@ def main():
             pe = None if pairs is None else (pairs[k][0].cuda_event, pairs[k][1].cuda_event)
             scg.gemm(t[0], t[1], t[2], t[3], t[4], L_max=g.L_max, polarity=g.polarity,
                      seed=g.seed, out=out, workspace=ws, stream=stream, prof_events=pe,
-                     L_hint=int(round(float(g.L.mean()))), rng=rng, engine=engine)
+                     L_hint=int(round(float(g.L.mean()))), rng=rng)
 
     for _ in range(args.warmup):
         step()
-    rc = scg.sc_gemm_status(staged[0][3].ptr, int(stream.cuda_stream))
-    if rc != 0:
-        raise SystemExit("device status error: %s" % scg.strerror(rc))
+    for k in range(len(staged)):
+        rc = scg.sc_gemm_status(staged[k][3].ptr, int(stream.cuda_stream))
+        if rc != 0:
+            raise SystemExit("device status error: %s" % scg.strerror(rc))
     torch.cuda.synchronize()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
@@ -152,42 +147,31 @@ def main():
     ms_per_step = ms_total / nsteps
     value = bitops / (ms_per_step * 1e-3)
 
-    # dominant kernel: the packed GEMM of the largest GEMM in the workload
+    # dominant kernel: the counting GEMM of the largest GEMM in the workload
     kidx = int(np.argmax([g.bitops() for g in w.gemms]))
     gemm_ms = float(np.mean([ev_pairs[s][kidx][0].elapsed_time(ev_pairs[s][kidx][1])
                              for s in range(nsteps)]))
     g_dom = w.gemms[kidx]
     achieved = g_dom.bitops() / (gemm_ms * 1e-3)
-    dom_engine = resolved[g_dom.name]
-    # counter summaries are keyed by workload, comparator source and engine
-    traffic_key = "%s:%s:%s" % (args.workload, args.rng,
-                                "mfma" if dom_engine == scg.SC_ENGINE_MFMA else "valu")
-    traffic = measured_traffic(traffic_key)
-    if dom_engine == scg.SC_ENGINE_MFMA:
-        # one bit-pair product = one fp4 multiply-add = 2 flops on the matrix cores
-        roofline = {"bound": "mfma", "achieved": 2 * achieved / 1e12, "peak": PEAK_FP4_FLOPS / 1e12,
-                    "unit": "TFLOP/s", "frac": 2 * achieved / PEAK_FP4_FLOPS, "traffic": traffic,
-                    # M > 128: 256-row blocks (fragments built from int8 chunks with
-                    # comparator streams, 256 or, for N <= 64, 64 columns wide; fp4 planes
-                    # with C-BSG when N > 128); other N <= 128 with comparator streams:
-                    # fragments built from the int8 rows in the GEMM
-                    "kernel": "%s<%s>" % ("k_rgemm" if rng == scg.SC_RNG_LFSR32 and g_dom.M > 128 and
-                                          (g_dom.N > 128 or g_dom.N <= 64) else
-                                          "k_qgemm" if g_dom.M > 128 and g_dom.N > 128 else
-                                          "k_fgemm" if g_dom.N <= 128 and rng == scg.SC_RNG_LFSR32 else "k_mgemm",
-                                          "bipolar" if g_dom.polarity == 0 else "unipolar"),
-                    "kernel_ms": gemm_ms, "frac_of_valu_bitop_peak": achieved / PEAK_BITOPS}
-    else:
-        roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_BITOPS / 1e12,
-                    "unit": "Tbitop/s", "frac": achieved / PEAK_BITOPS, "traffic": traffic,
-                    "kernel": ("k_gemm<unipolar>" if g_dom.polarity == 1 else
-                               "k_gemm<bipolar-cbsg>" if rng == scg.SC_RNG_SOBOL8_CBSG else
-                               "k_gemm<bipolar>"),
-                    "kernel_ms": gemm_ms, "frac_of_single_issue_peak": achieved / PEAK_SINGLE_ISSUE}
+    traffic = measured_traffic("%s:%s" % (args.workload, args.rng))
+    # one bit-pair product = one fp4 multiply-add = 2 flops on the matrix cores
+    roofline = {"bound": "mfma", "achieved": 2 * achieved / 1e12, "peak": PEAK_FP4_FLOPS / 1e12,
+                "unit": "TFLOP/s", "frac": 2 * achieved / PEAK_FP4_FLOPS, "traffic": traffic,
+                "kernel": "%s<%s>" % (gemm_kernel_name(g_dom, rng == scg.SC_RNG_LFSR32),
+                                      "bipolar" if g_dom.polarity == 0 else "unipolar"),
+                "kernel_ms": gemm_ms, "kernel_stream_bit_ops_per_s": achieved}
+
+    valu = None
+    if not args.no_valu_peak:
+        valu = valu_peak()
+        valu["value_over_peak"] = value / valu["bitops_per_s"]
+        valu["kernel_over_peak"] = achieved / valu["bitops_per_s"]
 
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, args.cpu_rows, args.rng == "cbsg")
+        cpu["gpu_over_oracle"] = value / cpu["value"]
+        cpu["paper_gpu_over_cpu"] = PAPER_GPU_VS_CPU
 
     g0 = w.gemms[0]
     cfg = {"workload": w.name, "gemms": [{"name": g.name, "batch": g.batch, "M": g.M, "N": g.N,
@@ -195,46 +179,97 @@ def main():
                                           "L_max": g.L_max} for g in w.gemms],
            "polarity": "bipolar_xnor" if g0.polarity == 0 else "unipolar_and_sign_magnitude",
            "rng": "sobol8_cbsg" if args.rng == "cbsg" else "lfsr32", "seed": g0.seed,
-           "engine": {k: ("mfma" if v == scg.SC_ENGINE_MFMA else "valu") for k, v in resolved.items()},
            "bitops_per_step": bitops}
     line = {"metric": METRIC, "value": value, "unit": "stream-bit-ops/s", "n_gpus": 1,
             "steps": nsteps, "warmup": args.warmup, "ms_per_step": ms_per_step,
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-            "dtype": "fp4" if dom_engine == scg.SC_ENGINE_MFMA else "u32",
-            "data": "synthetic", "config": cfg, "roofline": roofline, "cpu_baseline": cpu}
+            "dtype": "fp4", "data": "synthetic", "config": cfg, "roofline": roofline,
+            "valu_bitop_peak": valu, "cpu_baseline": cpu}
     print(json.dumps(line), flush=True)
 
 
+def gemm_kernel_name(g, comparator):
+    """The counting kernel the library takes for this shape (see make_layout): 256-row blocks
+    for M > 128 (fragments from int8 chunks with comparator streams, 256 or, for N <= 64, 64
+    columns wide; fp4 planes with C-BSG when N > 128); fragments from the int8 rows for other
+    N <= 128 with comparator streams; 128-row planes otherwise."""
+    if comparator and g.M > 128 and (g.N > 128 or g.N <= 64):
+        return "k_rgemm"
+    if g.M > 128 and g.N > 128:
+        return "k_qgemm"
+    if comparator and g.N <= 128:
+        return "k_fgemm"
+    return "k_mgemm"
+
+
+def valu_peak():
+    """The measured VALU rate of packed AND + accumulating popcount (libscpeak), best over
+    1, 2, 4 and 8 waves per SIMD, with the shader clock under that load."""
+    from paper_2609_32922_amd import peak
+    best = None
+    for wps in (1, 2, 4, 8):
+        r = peak.sc_peak_valu_bitop(wps, 50000)
+        if best is None or r.bitops_per_s > best.bitops_per_s:
+            best = r
+    return {"bitops_per_s": best.bitops_per_s, "unit": "stream-bit-ops/s",
+            "lane_ops_per_s": best.lane_ops_per_s, "clock_ghz": best.clock_hz / 1e9,
+            "cus": best.cus, "waves_per_simd": best.waves_per_simd,
+            "lane_ops_per_cu_per_clock": best.lane_ops_per_s / (best.cus * best.clock_hz),
+            "kind": "measured: 16 AND -> v_bcnt_u32_b32 chains per lane, registers only"}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, rows, cbsg=False):
-    """The CPU oracle, as it stands, on the first rows of the dominant GEMM."""
+    """The CPU oracle, as it stands, on the first rows of the dominant GEMM: all the host
+    threads this process may use (capped by OMP_NUM_THREADS when it is set, the CPU share
+    of one GPU on a shared host), then one thread on a small slice for the per-core rate."""
     import oracle
     ref = oracle.sc_gemm_cbsg if cbsg else oracle.sc_gemm
-    threads = min(len(os.sched_getaffinity(0)), 16)
+    visible = len(os.sched_getaffinity(0))
+    cap = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    threads = min(visible, cap) if cap > 0 else visible
     g = max(w.gemms, key=lambda x: x.bitops())
     b = 0
     bB = 0 if g.B.shape[0] == 1 else b
 
-    def run(n):
+    def run(n, nthreads):
         t = time.perf_counter()
         ref(g.A[b][:n], g.B[bB], g.sA[b][:n], g.sB[bB], g.L[b][:n], g.L_max,
-            g.polarity, g.seed, nthreads=threads, want_out=True)
+            g.polarity, g.seed, nthreads=nthreads, want_out=True)
         return time.perf_counter() - t
+
+    def ops(n):
+        return int(g.N) * int(g.K) * int(g.L[b][:n].astype(np.int64).sum())
 
     target = 15.0
     if rows <= 0:
         # size the sample so that the timed oracle run takes about 15 s: two probes give
         # the fixed cost (B streams) and the per-row cost
         r1, r2 = 16, 64
-        t1, t2 = run(r1), run(r2)
+        t1, t2 = run(r1, threads), run(r2, threads)
         per_row = max((t2 - t1) / (r2 - r1), 1e-6)
         rows = int(max(r2, min(g.M, (target - max(t1 - r1 * per_row, 0.0)) / per_row)))
-    dt = run(rows)
-    ops = int(g.N) * int(g.K) * int(g.L[b][:rows].astype(np.int64).sum())
-    return {"value": ops / dt, "unit": "stream-bit-ops/s", "cores": threads, "kind": "oracle",
-            "seconds": dt,
+    dt = run(rows, threads)
+    # one thread: the difference of two slices removes the fixed cost of B's streams
+    s1, s2 = 2, 10
+    d1, d2 = run(s1, 1), run(s2, 1)
+    one = (ops(s2) - ops(s1)) / max(d2 - d1, 1e-9)
+    return {"value": ops(rows) / dt, "unit": "stream-bit-ops/s", "cores": threads, "kind": "oracle",
+            "seconds": dt, "cpu_model": cpu_model(), "host_threads_visible": visible,
+            "one_thread_value": one,
             "sample": "%s/%s rows 0..%d of %d, all %d columns, K=%d, %d stream-bit-ops "
-                      "(every stream materialised inside the timed run)"
-                      % (w.name, g.name, rows - 1, g.M, g.N, g.K, ops)}
+                      "(every stream materialised inside the timed run); one-thread rate from "
+                      "rows %d..%d" % (w.name, g.name, rows - 1, g.M, g.N, g.K, ops(rows), s1, s2 - 1)}
 
 
 if __name__ == "__main__":

@@ -71,7 +71,8 @@ extern "C" {
 enum {
     SC_OK = 0,
     SC_ERR_NULL = -1,          /* a required pointer is NULL */
-    SC_ERR_SHAPE = -2,         /* batch, M, N or K negative, or K > SC_K_LIMIT */
+    SC_ERR_SHAPE = -2,         /* batch, M, N or K negative, K > SC_K_LIMIT, or
+                                  K * L_max > SC_KL_LIMIT */
     SC_ERR_LEN = -3,           /* L_max outside [1, SC_L_MAX_LIMIT] ([1, 256] for C-BSG),
                                   or L_hint outside [0, L_max] */
     SC_ERR_POLARITY = -4,      /* polarity not one of SC_BIPOLAR_XNOR / SC_UNIPOLAR_AND_SM */
@@ -80,22 +81,20 @@ enum {
     SC_ERR_HIP = -7,           /* a HIP runtime call or kernel launch failed */
     SC_ERR_DEVICE_STATUS = -8, /* (sc_gemm_status) some L_i was outside [0, L_max] */
     SC_ERR_STRIDE = -9,        /* a row stride is smaller than the row length */
-    SC_ERR_ENGINE = -10        /* unknown engine, reserved != 0, or MFMA with K*L_max > 2^24 */
+    SC_ERR_RESERVED = -10      /* the descriptor's reserved field is not 0 */
 };
 
 enum { SC_BIPOLAR_XNOR = 0, SC_UNIPOLAR_AND_SM = 1 };
 enum { SC_RNG_LFSR32 = 0, SC_RNG_SOBOL8_CBSG = 1 };
 
-/* Counting engine.  Both give identical counts and outputs.
- *   SC_ENGINE_VALU  packed bit planes, AND/XOR + popcount on the vector ALUs
- *   SC_ENGINE_MFMA  stream bits as fp4 (e2m1) values in {-1, 0, +1}, counted by the
- *                   matrix cores in fp32 (exact: every partial sum is an integer
- *                   below 2^24); needs K * L_max <= 2^24
- *   SC_ENGINE_AUTO  MFMA when K * L_max <= 2^24, else VALU */
-enum { SC_ENGINE_AUTO = 0, SC_ENGINE_VALU = 1, SC_ENGINE_MFMA = 2 };
+/* Counting: every stream bit becomes an fp4 (e2m1) value in {-1, 0, +1} and the matrix
+ * cores sum their products in fp32.  A work unit sums at most 2^24 products per output,
+ * so every partial sum is an exact integer; longer inner ranges are split into up to 8
+ * such units whose int32 partial counts are added exactly.  Hence K * L_max <= 2^27. */
 
-#define SC_L_MAX_LIMIT 4096     /* largest supported stream length */
-#define SC_K_LIMIT (1 << 20)    /* largest inner dimension (counts stay exact in int32) */
+#define SC_L_MAX_LIMIT 4096             /* largest supported stream length */
+#define SC_K_LIMIT (1 << 20)            /* largest inner dimension */
+#define SC_KL_LIMIT (1ll << 27)         /* largest K * L_max */
 
 typedef struct sc_gemm_desc {
     int32_t batch;              /* >= 0 independent problems */
@@ -110,15 +109,16 @@ typedef struct sc_gemm_desc {
     int32_t L_hint;             /* optional expected mean of the L_i (0 = unknown, taken as
                                    L_max); only tunes how GEMM tiles are split over the
                                    compute units, never changes a result; 0..L_max */
-    int32_t engine;             /* SC_ENGINE_AUTO, SC_ENGINE_VALU or SC_ENGINE_MFMA */
     int32_t reserved;           /* must be 0 */
     uint64_t seed;              /* comparator seed; same seed => bit-identical results */
     void *prof_event_begin;     /* optional hipEvent_t recorded just before the main */
     void *prof_event_end;       /*   GEMM kernel and just after it (profiling); NULL = off */
 } sc_gemm_desc;
 
-/* Bytes of device workspace sc_gemm needs for `desc` (host-only, no HIP call).
- * Returns SC_OK and writes *bytes, or a negative SC_ERR_* code for a bad desc. */
+/* Bytes of device workspace sc_gemm needs for `desc` on the current HIP device (the size
+ * depends on the device's compute-unit count, which is queried once per device; with no
+ * device visible an MI355X's 256 is assumed).  Enqueues nothing.  Returns SC_OK and writes
+ * *bytes, or a negative SC_ERR_* code for a bad desc. */
 int sc_gemm_workspace_size(const sc_gemm_desc *desc, size_t *bytes);
 
 /*

@@ -9,17 +9,15 @@ back to the CPU: without the built library every call raises.
 """
 from __future__ import annotations
 
-from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_ERR_ENGINE, SC_L_MAX_LIMIT, SC_OK,  # noqa: F401
-                   SC_ENGINE_AUTO, SC_ENGINE_MFMA, SC_ENGINE_VALU, SC_RNG_LFSR32,
-                   SC_RNG_SOBOL8_CBSG, SC_UNIPOLAR_AND_SM, ScError, ScGemmDesc, load, sc_comparator_sequence,
-                   sc_gemm, sc_gemm_status, sc_gemm_workspace_size, sc_mp_lengths, sc_quantize,
-                   sc_version, strerror)
+from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_ERR_RESERVED, SC_KL_LIMIT,  # noqa: F401
+                   SC_L_MAX_LIMIT, SC_OK, SC_RNG_LFSR32, SC_RNG_SOBOL8_CBSG, SC_UNIPOLAR_AND_SM,
+                   ScError, ScGemmDesc, load, sc_comparator_sequence, sc_gemm, sc_gemm_status,
+                   sc_gemm_workspace_size, sc_mp_lengths, sc_quantize, sc_version, strerror)
 
 __all__ = ["gemm", "make_desc", "comparator_sequence", "quantize", "mp_lengths", "Workspace",
            "ScGemmDesc", "ScError", "sc_gemm", "sc_gemm_workspace_size", "sc_gemm_status",
            "sc_comparator_sequence", "sc_quantize", "sc_mp_lengths", "SC_BIPOLAR_XNOR",
-           "SC_UNIPOLAR_AND_SM", "SC_RNG_LFSR32", "SC_RNG_SOBOL8_CBSG", "SC_ENGINE_AUTO",
-           "SC_ENGINE_VALU", "SC_ENGINE_MFMA"]
+           "SC_UNIPOLAR_AND_SM", "SC_RNG_LFSR32", "SC_RNG_SOBOL8_CBSG"]
 
 
 def _stream_handle(stream):
@@ -29,7 +27,7 @@ def _stream_handle(stream):
 
 
 def make_desc(A, B, L_max: int, polarity: int, seed: int, L_hint: int = 0,
-              rng: int = SC_RNG_LFSR32, engine: int = SC_ENGINE_AUTO) -> ScGemmDesc:
+              rng: int = SC_RNG_LFSR32) -> ScGemmDesc:
     """Descriptor for contiguous A [batch, M, K] and B [batch or 1, N, K] tensors."""
     if A.dim() == 2:
         A = A.unsqueeze(0)
@@ -45,7 +43,6 @@ def make_desc(A, B, L_max: int, polarity: int, seed: int, L_hint: int = 0,
     d.strideA, d.strideB, d.strideO = M * K, (N * K if nb == batch and batch > 1 else 0), M * N
     d.strideSA, d.strideSB, d.strideL = M, (N if nb == batch and batch > 1 else 0), M
     d.L_max, d.polarity, d.rng, d.L_hint, d.seed = int(L_max), int(polarity), int(rng), int(L_hint), int(seed)
-    d.engine = int(engine)
     return d
 
 
@@ -65,42 +62,76 @@ class Workspace:
         return self
 
 
+def _check_output(t, name, dtype, shape, device):
+    """A caller-supplied output must be exactly what the kernels write into."""
+    import torch
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, not %s" % (name, dtype, t.dtype))
+    if not t.is_cuda or t.device != device:
+        raise ValueError("%s must be on %s" % (name, device))
+    if tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous %s tensor of shape %s, got %s" % (
+            name, dtype, tuple(shape), tuple(t.shape)))
+    return t
+
+
 def gemm(A, sA, B, sB, L, *, L_max: int, polarity: int = SC_BIPOLAR_XNOR, seed: int = 0,
          out=None, counts=None, want_counts: bool = False, workspace: Workspace = None,
          stream=None, check_status: bool = False, prof_events=None, L_hint: int = 0,
-         rng: int = SC_RNG_LFSR32, engine: int = SC_ENGINE_AUTO):
+         rng: int = SC_RNG_LFSR32):
     """SC GEMM on torch device tensors.
 
     A int8 [batch, M, K] (or [M, K]), sA float32 [batch, M], B int8 [batch or 1, N, K],
-    sB float32 [batch or 1, N], L int32 [batch, M].  ``rng`` selects the comparator
-    source (LFSR, or Sobol-8 with conditional generation of B, L_max <= 256) and
-    ``engine`` the counting engine (AUTO, VALU popcount or MFMA fp4).
+    sB float32 [batch or 1, N], L int32 [batch, M], all on one device.  ``rng`` selects
+    the comparator source (LFSR, or Sobol-8 with conditional generation of B,
+    L_max <= 256).  ``out`` (float32) and ``counts`` (int32), when given, must be
+    contiguous [batch, M, N] tensors ([M, N] for 2-d A) on A's device.  When ``stream`` is
+    not the current stream, tensors allocated here are marked as used by ``stream``.
     Returns (out, counts or None).
     """
     import torch
     squeeze = A.dim() == 2
     A3 = A.unsqueeze(0) if A.dim() == 2 else A
     B3 = B.unsqueeze(0) if B.dim() == 2 else B
-    d = make_desc(A3, B3, L_max, polarity, seed, L_hint, rng, engine)
+    d = make_desc(A3, B3, L_max, polarity, seed, L_hint, rng)
+    dev = A3.device
     for t, name in ((A3, "A"), (B3, "B"), (sA, "sA"), (sB, "sB"), (L, "L")):
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError("%s must be a contiguous device tensor" % name)
+        if not t.is_cuda or not t.is_contiguous() or t.device != dev:
+            raise ValueError("%s must be a contiguous tensor on %s" % (name, dev))
     if A3.dtype != torch.int8 or B3.dtype != torch.int8 or sA.dtype != torch.float32 \
             or sB.dtype != torch.float32 or L.dtype != torch.int32:
         raise TypeError("dtypes: A, B int8; sA, sB float32; L int32")
     batch, M, N = d.batch, d.M, d.N
     if sA.numel() != batch * M or L.numel() != batch * M or sB.numel() != B3.shape[0] * N:
         raise ValueError("scale or length vector has the wrong size")
+    oshape = (M, N) if squeeze else (batch, M, N)
+    s = stream if stream is not None else torch.cuda.current_stream(dev)
+    foreign = s != torch.cuda.current_stream(dev)
+    made = []
     if out is None:
-        out = torch.empty((batch, M, N), dtype=torch.float32, device=A.device)
+        out = torch.empty(oshape, dtype=torch.float32, device=dev)
+        made.append(out)
+    else:
+        _check_output(out, "out", torch.float32, oshape, dev)
     if counts is None and want_counts:
-        counts = torch.empty((batch, M, N), dtype=torch.int32, device=A.device)
+        counts = torch.empty(oshape, dtype=torch.int32, device=dev)
+        made.append(counts)
+    elif counts is not None:
+        _check_output(counts, "counts", torch.int32, oshape, dev)
     nbytes = sc_gemm_workspace_size(d)
-    ws = (workspace or Workspace(nbytes, A.device)).ensure(nbytes)
+    if workspace is None:
+        ws = Workspace(nbytes, dev)
+        made.append(ws._buf)
+    else:
+        ws = workspace.ensure(nbytes)
+    if foreign:
+        # the caching allocator must not hand these blocks out again before `s` is done
+        for t in made:
+            t.record_stream(s)
     if prof_events is not None:
         d.prof_event_begin = prof_events[0]
         d.prof_event_end = prof_events[1]
-    sh = _stream_handle(stream)
+    sh = int(s.cuda_stream)
     rc = sc_gemm(d, A3.data_ptr(), sA.data_ptr(), B3.data_ptr(), sB.data_ptr(), L.data_ptr(),
                  out.data_ptr(), counts.data_ptr() if counts is not None else 0, ws.ptr, ws.nbytes, sh)
     if rc != SC_OK:
@@ -109,9 +140,6 @@ def gemm(A, sA, B, sB, L, *, L_max: int, polarity: int = SC_BIPOLAR_XNOR, seed: 
         rc = sc_gemm_status(ws.ptr, sh)
         if rc != SC_OK:
             raise ScError(rc, "sc_gemm (device status)")
-    if squeeze:
-        out = out[0]
-        counts = counts[0] if counts is not None else None
     return out, counts
 
 

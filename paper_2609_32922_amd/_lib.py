@@ -22,17 +22,15 @@ SC_ERR_WORKSPACE = -6
 SC_ERR_HIP = -7
 SC_ERR_DEVICE_STATUS = -8
 SC_ERR_STRIDE = -9
-SC_ERR_ENGINE = -10
+SC_ERR_RESERVED = -10
 
 SC_BIPOLAR_XNOR = 0
 SC_UNIPOLAR_AND_SM = 1
 SC_RNG_LFSR32 = 0
 SC_RNG_SOBOL8_CBSG = 1
-SC_ENGINE_AUTO = 0
-SC_ENGINE_VALU = 1
-SC_ENGINE_MFMA = 2
 SC_L_MAX_LIMIT = 4096
 SC_K_LIMIT = 1 << 20
+SC_KL_LIMIT = 1 << 27
 
 
 class ScGemmDesc(ctypes.Structure):
@@ -55,7 +53,6 @@ class ScGemmDesc(ctypes.Structure):
         ("polarity", ctypes.c_int32),
         ("rng", ctypes.c_int32),
         ("L_hint", ctypes.c_int32),
-        ("engine", ctypes.c_int32),
         ("reserved", ctypes.c_int32),
         ("seed", ctypes.c_uint64),
         ("prof_event_begin", ctypes.c_void_p),

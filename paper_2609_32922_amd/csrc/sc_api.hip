@@ -3,6 +3,8 @@
 #include <limits.h>
 #include <math.h>
 
+#include <atomic>
+
 #include "sc_internal.h"
 
 namespace scg {
@@ -20,32 +22,46 @@ bool mul_ok(size_t a, size_t b, size_t *r) {
 
 }  // namespace
 
-// the engine an AUTO descriptor runs on
-static int resolve_engine(const sc_gemm_desc &d) {
-    if (d.engine != SC_ENGINE_AUTO) return d.engine;
-    return (int64_t)d.K * d.L_max <= MFMA_EXACT ? SC_ENGINE_MFMA : SC_ENGINE_VALU;
+// Compute units of the current device (the width over which the GEMM's work is divided),
+// cached per device; DEFAULT_CUS when no device can be queried (e.g. sizing a workspace on
+// a host without a GPU).
+static int device_cus() {
+    static std::atomic<int> cache[64];
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+        (void)hipGetLastError();
+        return DEFAULT_CUS;
+    }
+    if (dev < 64) {
+        const int c = cache[dev].load(std::memory_order_relaxed);
+        if (c > 0) return c;
+    }
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+        (void)hipGetLastError();
+        return DEFAULT_CUS;
+    }
+    if (dev < 64) cache[dev].store(n, std::memory_order_relaxed);
+    return n;
 }
 
-bool make_layout(const sc_gemm_desc &d, Layout *lay) {
+bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
     Layout l{};
-    l.engine = resolve_engine(d);
-    const bool mfma = l.engine == SC_ENGINE_MFMA;
-    l.KB = (d.K + 31) / 32;
+    l.cus = cus > 0 ? cus : DEFAULT_CUS;
     l.KQP = (int)round_up((d.K + 3) / 4, 4);
-    l.tstep = mfma ? MSTEP : LSTEP;
-    l.words_per_L = mfma ? (int64_t)l.KQP * 64 : (int64_t)l.KB * BM;
+    l.words_per_L = (int64_t)l.KQP * 64;
     l.MT = (d.M + BM - 1) / BM;
     l.NT = (d.N + BN - 1) / BN;
     // N <= 64 with comparator streams and M > 128: the int8-chunk GEMM in blocks of
     // 256 rows x 64 columns (the B side still laid out as one 256-row pair)
-    l.narrow = mfma && d.rng == SC_RNG_LFSR32 && d.N <= 64 && d.M > BM;
+    l.narrow = d.rng == SC_RNG_LFSR32 && d.N <= 64 && d.M > BM;
     l.mbn = (l.NT > 1 || l.narrow) ? 2 * BN : BN;
-    if (mfma) l.NT = (int)round_up(l.NT, l.mbn / BN);
+    l.NT = (int)round_up(l.NT, l.mbn / BN);
     // N <= 128 (one B tile): every A plane would be used once, so the GEMM generates the
     // fragments itself (comparator streams; operand offsets must fit 31 bits)
-    l.fused = mfma && l.mbn == BN && d.rng == SC_RNG_LFSR32 &&
-              fused_extent(d.M, d.lda, d.K) < INT_MAX - 4 && fused_extent(d.N, d.ldb, d.K) < INT_MAX - 4;
-    l.mbm = (mfma && l.MT > 1 && l.mbn == 2 * BN) ? 2 * BM : BM;
+    l.fused = l.mbn == BN && d.rng == SC_RNG_LFSR32 && fused_extent(d.M, d.lda, d.K) < INT_MAX - 4 &&
+              fused_extent(d.N, d.ldb, d.K) < INT_MAX - 4;
+    l.mbm = (l.MT > 1 && l.mbn == 2 * BN) ? 2 * BM : BM;
     if (l.mbm == 2 * BM) l.MT = (int)round_up(l.MT, 2);
     // 256 x 256 blocks with comparator streams: fragments from int8 chunks and a table of
     // each 32-cycle group, so the operands are read as bytes instead of fp4 planes
@@ -53,14 +69,9 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     l.rslots = l.narrow ? 0 : RSLOTS;
     l.KC = (d.K + 31) / 32;
     l.LBS = (int)round_up(d.L_max, LCH);
-    l.LP = (int)round_up(d.L_max, LSTEP);
     l.nbB = (d.strideB == 0) ? 1 : d.batch;
     if (l.nbB < 1) l.nbB = 1;
     const bool cbsg = d.rng == SC_RNG_SOBOL8_CBSG;
-    const bool uni = d.polarity == SC_UNIPOLAR_AND_SM;
-    l.mode = uni ? MODE_SIGNED : (cbsg ? MODE_CBSG : MODE_AND);
-    const bool signsA = !mfma && l.mode != MODE_AND, signsB = !mfma && uni;
-    const bool needRB = !mfma && l.mode == MODE_AND;
 
     // the status word is always the first word of the workspace
     size_t off = 0;
@@ -82,21 +93,17 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     a = align256(a + rowsA * 4);
     l.off_Ls = a;
     a = align256(a + rowsA * 4);
-    l.off_RA = a;
-    a = align256(a + rowsA * 4);
     l.off_tileL = a;
     a = align256(a + (size_t)l.MT * 4);
     l.off_tileOff = a;
     a = align256(a + (size_t)l.MT * 8);
     l.off_Ap = a;
-    // largest planes of one batch entry: every tile at L_max rounded up to its step
-    if (!mul_ok((size_t)l.MT * (size_t)l.words_per_L, (size_t)round_up(d.L_max, l.tstep) * 4, &sz))
+    // largest planes of one batch entry: every tile at L_max rounded up to an octet
+    if (!mul_ok((size_t)l.MT * (size_t)l.words_per_L, (size_t)round_up(d.L_max, MSTEP) * 4, &sz))
         return false;
     if (l.fused) sz = 0;
     if (l.rgen && !mul_ok(rowsA, (size_t)l.KC * 32, &sz)) return false;
     a = align256(a + sz);
-    l.off_SA = a;
-    if (signsA) a = align256(a + rowsA * (size_t)l.KB * 4);
     l.stride_batchA = a;
     const size_t baseA = off;
     size_t totA;
@@ -111,25 +118,35 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     if (l.fused) sz = 0;
     if (l.rgen && !mul_ok(rowsB, (size_t)l.KC * 32, &sz)) return false;
     bb = align256(bb + sz);
-    l.off_SB = bb;
-    if (signsB) bb = align256(bb + rowsB * (size_t)l.KB * 4);
-    l.off_RB = bb;
-    if (needRB) bb = align256(bb + (size_t)d.N * (size_t)(d.L_max + 1) * 4);
     l.stride_batchB = bb;
     const size_t baseB = off;
     size_t totB;
     if (!mul_ok(bb, (size_t)l.nbB, &totB)) return false;
     off += totB;
 
+    // Exactness of the counts: a GEMM part sums its products into fp32 accumulators, which
+    // stay exact integers while a part holds at most 2^24 products per output.  Units of the
+    // inner range and products per unit of each GEMM: (32-cycle group, 32-element chunk) =
+    // 1024 (int8-chunk GEMM); stage of 4 slots = 128 (fused GEMM); k-step of 2 slots = 64.
+    // A part takes at most ceil(units / S) units, so S is at least Smin; the parts' int32
+    // partial sums are then added exactly.
+    const int64_t octs = round_up(d.L_max, MSTEP) / MSTEP;
+    const int64_t units = l.rgen ? (int64_t)(l.LBS / 32) * l.KC
+                                 : l.fused ? octs * (l.KQP / MSTAGE) : octs * (l.KQP / 2);
+    const int64_t per_unit = l.rgen ? 32 * 32 : l.fused ? 128 : 64;
+    l.Smin = 1;
+    while (l.Smin <= MAX_SPLIT && (units + l.Smin - 1) / l.Smin * per_unit > MFMA_EXACT) l.Smin *= 2;
+    if (l.Smin > MAX_SPLIT) return false;
+
     // Division of the GEMM tiles into work units.
-    const bool quad = mfma && l.mbm == 2 * BM;
-    const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * (l.MT / (l.mbm / BM)) *
-                          (mfma ? l.NT / (l.mbn / BN) : l.NT);
-    // indivisible steps along K per cycle (chunks of every 32-cycle group with rgen)
-    const int kunits = l.rgen ? l.KC * (l.LBS / 32) : mfma ? l.KQP / 2 : l.KB;
-    const double tile_bytes = (double)l.mbm * (mfma ? l.mbn : BN) * 4.0;
+    const bool quad = l.mbm == 2 * BM;
+    const int64_t tiles = (int64_t)(d.batch > 0 ? d.batch : 0) * (l.MT / (l.mbm / BM)) * (l.NT / (l.mbn / BN));
+    // indivisible steps along the inner range per cycle (chunks of every 32-cycle group with rgen)
+    const int kunits = l.rgen ? l.KC * (l.LBS / 32) : l.KQP / 2;
+    const int smax = kunits > l.Smin ? kunits : l.Smin;
+    const double tile_bytes = (double)l.mbm * l.mbn * 4.0;
     const double Lmean = d.L_hint > 0 ? d.L_hint : d.L_max;
-    l.S = 1;
+    l.S = l.Smin;
     l.F = 0;
     if (quad && tiles > 0) {
         // 256 x 256 tiles, one block per CU, taking whole tiles or parts of tiles
@@ -140,17 +157,17 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
         // together from its L2 (three-way splits measured slower than four-way).  With
         // F = 0 the GEMM kernels may lower s again with the actual longest tile pair
         // (measured: 6304 x 768 x 3072 with L in [16, 256], mean 64, longest 172: the GEMM
-        // takes 0.49 ms split two ways against 0.61 ms three ways).
+        // takes 0.49 ms split two ways against 0.61 ms three ways), never below Smin.
         // (the 64-column blocks of N <= 64 do a quarter of the work and run two per CU)
         l.q_perL = (double)l.mbm * (l.narrow ? 64 : l.mbn) * 4.0 * l.KQP / MFMA_QUAD_RATE;
-        l.q_slots = l.narrow ? 2 * CUS : CUS;
+        l.q_slots = l.narrow ? 2 * l.cus : l.cus;
         l.q_Lmean = Lmean;
         l.q_one = Lmean >= d.L_max;
         const double avgT = l.q_perL * Lmean, maxT = l.q_perL * d.L_max;
         double best = 0.0;
-        for (int s = 1; s <= MAX_SPLIT && s <= (kunits > 0 ? kunits : 1); s *= 2) {
+        for (int s = l.Smin; s <= MAX_SPLIT && s <= smax; s *= 2) {
             const double est = quad_split_time(tiles, s, l.q_perL, Lmean, d.L_max, l.q_one != 0, l.q_slots);
-            if (s == 1 || est < best * 0.97) {
+            if (s == l.Smin || est < best * 0.97) {
                 best = est;
                 l.S = s;
             }
@@ -161,7 +178,7 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
         int s2 = R > 0 ? (int)(l.q_slots / R) : 1;
         s2 = s2 > MAX_SPLIT ? MAX_SPLIT : s2;
         if (s2 > kunits) s2 = kunits;
-        if (tiles >= l.q_slots && R > 0 && s2 > 1) {
+        if (l.Smin == 1 && tiles >= l.q_slots && R > 0 && s2 > 1) {
             const double red = (double)R * (2 * s2) * tile_bytes / PART_BW + 5e-6;
             const double est = fmax((double)(tiles / l.q_slots) * avgT + avgT / s2, maxT) + red;
             if (est < best * 0.97) {
@@ -175,23 +192,20 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
         // 128-row tiles: every tile split s ways.  Estimated time of split s: the busiest
         // slot (a resident block) runs ceil(units/slots) units of average work, plus the
         // excess of the heaviest unit over the average, plus, for s > 1, writing and summing
-        // s partial tiles.  MFMA units are dealt to the eight XCDs round-robin, so s is a
-        // power of two: each XCD then keeps one k-range of its tiles, and its L2 serves that
-        // range to all of them.  Rates are the measured order of magnitude: VALU engine
-        // 2.8e12 bit pairs/s per CU; MFMA engine 4.8e12 products/s per resident block (two
-        // per CU); partial sums at 3e12 B/s.
-        const int slots = mfma ? CUS * MFMA_BLOCKS_PER_CU : CUS;
-        const double rate = mfma ? 4.8e12 : 2.8e12;
-        const double per_L = mfma ? (double)BM * l.mbn * 4.0 * l.KQP : (double)BM * BN * 32.0 * l.KB;
+        // s partial tiles.  Units are dealt to the eight XCDs round-robin, so s is a power of
+        // two: each XCD then keeps one k-range of its tiles, and its L2 serves that range to
+        // all of them.  Rates are the measured order of magnitude: 4.8e12 products/s per
+        // resident block (two per CU); partial sums at 3e12 B/s.
+        const int slots = l.cus * MFMA_BLOCKS_PER_CU;
+        const double rate = 4.8e12;
+        const double per_L = (double)BM * l.mbn * 4.0 * l.KQP;
         double best = 0.0;
-        for (int s = 1; s <= MAX_SPLIT && s <= kunits; s = mfma ? 2 * s : s + 1) {
-            const int64_t units = tiles * s;
+        for (int s = l.Smin; s <= MAX_SPLIT && s <= smax; s *= 2) {
+            const int64_t nunits = tiles * s;
             const double avg_u = per_L * Lmean / s, max_u = per_L * d.L_max / s;
-            const double gemm = ((double)((units + slots - 1) / slots) * avg_u + (max_u - avg_u)) / rate;
-            const double red = s > 1 ? (mfma ? (double)tiles * (2 * s) * tile_bytes / 3e12
-                                             : (double)tiles * (s + 1) * tile_bytes / 3.7e12) + 5e-6
-                                     : 0.0;
-            if (s == 1 || gemm + red < best * (mfma ? 0.97 : 0.99)) {
+            const double gemm = ((double)((nunits + slots - 1) / slots) * avg_u + (max_u - avg_u)) / rate;
+            const double red = s > 1 ? (double)tiles * (2 * s) * tile_bytes / 3e12 + 5e-6 : 0.0;
+            if (s == l.Smin || gemm + red < best * 0.97) {
                 best = gemm + red;
                 l.S = s;
             }
@@ -208,14 +222,10 @@ bool make_layout(const sc_gemm_desc &d, Layout *lay) {
     // make every offset absolute for batch entry 0
     l.off_perm += baseA;
     l.off_Ls += baseA;
-    l.off_RA += baseA;
     l.off_tileL += baseA;
     l.off_tileOff += baseA;
     l.off_Ap += baseA;
-    l.off_SA += baseA;
     l.off_Bp += baseB;
-    l.off_SB += baseB;
-    l.off_RB += baseB;
     l.total = off;
     *lay = l;
     return true;
@@ -225,16 +235,13 @@ static int check_desc(const sc_gemm_desc *d) {
     if (d == nullptr) return SC_ERR_NULL;
     if (d->batch < 0 || d->M < 0 || d->N < 0 || d->K < 0 || d->K > SC_K_LIMIT) return SC_ERR_SHAPE;
     if (d->L_max < 1 || d->L_max > SC_L_MAX_LIMIT) return SC_ERR_LEN;
-    // counts 2*X and K*L must stay exact in int32
-    if ((int64_t)d->K * d->L_max > (1ll << 29)) return SC_ERR_SHAPE;
+    // the counts stay exact: at most MAX_SPLIT parts of at most 2^24 products each
+    if ((int64_t)d->K * d->L_max > SC_KL_LIMIT) return SC_ERR_SHAPE;
     if (d->polarity != SC_BIPOLAR_XNOR && d->polarity != SC_UNIPOLAR_AND_SM) return SC_ERR_POLARITY;
     if (d->rng != SC_RNG_LFSR32 && d->rng != SC_RNG_SOBOL8_CBSG) return SC_ERR_RNG;
     if (d->rng == SC_RNG_SOBOL8_CBSG && d->L_max > CBSG_L_MAX) return SC_ERR_LEN;
     if (d->L_hint < 0 || d->L_hint > d->L_max) return SC_ERR_LEN;
-    if ((d->engine != SC_ENGINE_AUTO && d->engine != SC_ENGINE_VALU && d->engine != SC_ENGINE_MFMA) ||
-        d->reserved != 0)
-        return SC_ERR_ENGINE;
-    if (d->engine == SC_ENGINE_MFMA && (int64_t)d->K * d->L_max > MFMA_EXACT) return SC_ERR_ENGINE;
+    if (d->reserved != 0) return SC_ERR_RESERVED;
     if (d->lda < d->K || d->ldb < d->K || d->ldo < d->N) return SC_ERR_STRIDE;
     if (d->strideA < 0 || d->strideB < 0 || d->strideO < 0 || d->strideSA < 0 || d->strideSB < 0 ||
         d->strideL < 0)
@@ -250,48 +257,9 @@ static int check_desc(const sc_gemm_desc *d) {
     return SC_OK;
 }
 
-}  // namespace scg
-
-using namespace scg;
-
-extern "C" {
-
-int sc_version(void) { return 10200; }
-
-const char *sc_strerror(int code) {
-    switch (code) {
-        case SC_OK: return "SC_OK";
-        case SC_ERR_NULL: return "SC_ERR_NULL: a required pointer is NULL";
-        case SC_ERR_SHAPE: return "SC_ERR_SHAPE: bad batch/M/N/K (or K*L_max too large)";
-        case SC_ERR_LEN:
-            return "SC_ERR_LEN: L_max outside [1, SC_L_MAX_LIMIT] ([1, 256] for C-BSG) or L_hint "
-                   "outside [0, L_max]";
-        case SC_ERR_POLARITY: return "SC_ERR_POLARITY: unknown polarity";
-        case SC_ERR_RNG: return "SC_ERR_RNG: unknown rng or operand index";
-        case SC_ERR_WORKSPACE: return "SC_ERR_WORKSPACE: workspace missing or too small";
-        case SC_ERR_HIP: return "SC_ERR_HIP: a HIP call or kernel launch failed";
-        case SC_ERR_DEVICE_STATUS: return "SC_ERR_DEVICE_STATUS: some L_i outside [0, L_max]";
-        case SC_ERR_STRIDE: return "SC_ERR_STRIDE: a stride is too small or negative";
-        case SC_ERR_ENGINE:
-            return "SC_ERR_ENGINE: unknown engine, reserved field not 0, or MFMA engine with "
-                   "K*L_max > 2^24";
-        default: return "unknown status code";
-    }
-}
-
-int sc_gemm_workspace_size(const sc_gemm_desc *desc, size_t *bytes) {
-    if (bytes == nullptr) return SC_ERR_NULL;
-    const int rc = check_desc(desc);
-    if (rc != SC_OK) return rc;
-    Layout lay;
-    if (!make_layout(*desc, &lay)) return SC_ERR_SHAPE;
-    *bytes = lay.total;
-    return SC_OK;
-}
-
-int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const int8_t *B,
-            const float *sB, const int32_t *L_per_row, float *out, int32_t *counts, void *workspace,
-            size_t workspace_bytes, void *stream) {
+// Checks of one call (before anything is enqueued) and its workspace layout.
+static int check_call(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const int8_t *B,
+                      const float *sB, const int32_t *L_per_row, const float *out, Layout *lay) {
     const int rc = check_desc(desc);
     if (rc != SC_OK) return rc;
     const sc_gemm_desc &d = *desc;
@@ -301,14 +269,14 @@ int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const in
         (anyM && (sA == nullptr || L_per_row == nullptr)) || (anyN && sB == nullptr) ||
         (anyM && anyN && out == nullptr))
         return SC_ERR_NULL;
-    Layout lay;
-    if (!make_layout(d, &lay)) return SC_ERR_SHAPE;
-    if (workspace == nullptr || workspace_bytes < lay.total ||
-        (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-        return SC_ERR_WORKSPACE;
-    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-    uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
+    if (!make_layout(d, device_cus(), lay)) return SC_ERR_SHAPE;
+    return SC_OK;
+}
 
+// The launch sequence of one call on workspace ws (lay.total bytes, 256-byte aligned).
+static int enqueue(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, const float *sA, const int8_t *B,
+                   const float *sB, const int32_t *L_per_row, float *out, int32_t *counts, uint8_t *ws,
+                   hipStream_t st) {
     uint32_t *rA = reinterpret_cast<uint32_t *>(ws + lay.off_rA);
     // one batch entry with LFSR sequences: the scheduler's single block also clears the
     // status and makes the sequences (one launch fewer); otherwise k_draws does, first
@@ -326,26 +294,71 @@ int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const in
         launch_cbsg_table(rA, d.L_max, reinterpret_cast<uint16_t *>(ws + lay.off_CA), st) != hipSuccess)
         return SC_ERR_HIP;
     if ((e = launch_schedule(d, lay, L_per_row, ws, fuse, st)) != hipSuccess) return SC_ERR_HIP;
-    const bool mfma = lay.engine == SC_ENGINE_MFMA;
-    if (!mfma && lay.mode == MODE_AND && (e = launch_marginals(d, lay, A, B, ws, st)) != hipSuccess)
-        return SC_ERR_HIP;
     if (lay.rgen) {
         if ((e = launch_rchunks(d, lay, A, B, ws, st)) != hipSuccess) return SC_ERR_HIP;
     } else if (!lay.fused) {
-        e = mfma ? launch_mplanes(d, lay, A, B, ws, st) : launch_planes(d, lay, A, B, ws, st);
-        if (e != hipSuccess) return SC_ERR_HIP;
+        if ((e = launch_mplanes(d, lay, A, B, ws, st)) != hipSuccess) return SC_ERR_HIP;
     }
     if (d.prof_event_begin != nullptr &&
         hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_begin), st) != hipSuccess)
         return SC_ERR_HIP;
     e = lay.fused ? launch_fgemm(d, lay, A, B, sA, sB, out, counts, ws, st)
-                  : mfma ? launch_mgemm(d, lay, sA, sB, out, counts, ws, st)
-                         : launch_gemm(d, lay, sA, sB, out, counts, ws, st);
+                  : launch_mgemm(d, lay, sA, sB, out, counts, ws, st);
     if (e != hipSuccess) return SC_ERR_HIP;
     if (d.prof_event_end != nullptr &&
         hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_end), st) != hipSuccess)
         return SC_ERR_HIP;
     return SC_OK;
+}
+
+}  // namespace scg
+
+using namespace scg;
+
+extern "C" {
+
+int sc_version(void) { return 10200; }
+
+const char *sc_strerror(int code) {
+    switch (code) {
+        case SC_OK: return "SC_OK";
+        case SC_ERR_NULL: return "SC_ERR_NULL: a required pointer is NULL";
+        case SC_ERR_SHAPE: return "SC_ERR_SHAPE: bad batch/M/N/K (or K*L_max above 2^27)";
+        case SC_ERR_LEN:
+            return "SC_ERR_LEN: L_max outside [1, SC_L_MAX_LIMIT] ([1, 256] for C-BSG) or L_hint "
+                   "outside [0, L_max]";
+        case SC_ERR_POLARITY: return "SC_ERR_POLARITY: unknown polarity";
+        case SC_ERR_RNG: return "SC_ERR_RNG: unknown rng or operand index";
+        case SC_ERR_WORKSPACE: return "SC_ERR_WORKSPACE: workspace missing or too small";
+        case SC_ERR_HIP: return "SC_ERR_HIP: a HIP call or kernel launch failed";
+        case SC_ERR_DEVICE_STATUS: return "SC_ERR_DEVICE_STATUS: some L_i outside [0, L_max]";
+        case SC_ERR_STRIDE: return "SC_ERR_STRIDE: a stride is too small or negative";
+        case SC_ERR_RESERVED: return "SC_ERR_RESERVED: the reserved descriptor field is not 0";
+        default: return "unknown status code";
+    }
+}
+
+int sc_gemm_workspace_size(const sc_gemm_desc *desc, size_t *bytes) {
+    if (bytes == nullptr) return SC_ERR_NULL;
+    const int rc = check_desc(desc);
+    if (rc != SC_OK) return rc;
+    Layout lay;
+    if (!make_layout(*desc, device_cus(), &lay)) return SC_ERR_SHAPE;
+    *bytes = lay.total;
+    return SC_OK;
+}
+
+int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const int8_t *B,
+            const float *sB, const int32_t *L_per_row, float *out, int32_t *counts, void *workspace,
+            size_t workspace_bytes, void *stream) {
+    Layout lay;
+    const int rc = check_call(desc, A, sA, B, sB, L_per_row, out, &lay);
+    if (rc != SC_OK) return rc;
+    if (workspace == nullptr || workspace_bytes < lay.total ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return SC_ERR_WORKSPACE;
+    return enqueue(*desc, lay, A, sA, B, sB, L_per_row, out, counts, reinterpret_cast<uint8_t *>(workspace),
+                   reinterpret_cast<hipStream_t>(stream));
 }
 
 int sc_gemm_status(const void *workspace, void *stream) {

@@ -3,10 +3,10 @@
 // Data layout in device memory (all inside the caller's workspace):
 //
 //   status     one uint32 (bit 0: some L_i out of range), then one uint32: the longest
-//              tile-pair cycle count of the call (256-row MFMA GEMM), then one uint32: nonzero
+//              tile-pair cycle count of the call (256-row GEMM), then one uint32: nonzero
 //              when some 256-row pair holds more distinct lengths that are not multiples of
 //              32 than the int8-chunk GEMM has masked tables (rslots; it then masks its
-//              fragments); all cleared by k_draws
+//              fragments); all cleared by k_draws (or k_schedule)
 //   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
 //   CA         C-BSG only: CA[L][beta] = #{l < L : rA_l < beta}, uint16 [L_max+1][257]
 //   rtab       int8-chunk GEMM only: for each 32-cycle group G, the fp4 slot row of every
@@ -14,35 +14,29 @@
 //   per batch entry b of A (batch entries):
 //     perm[MT*BM]      sorted position -> original row (or -1 for padding)
 //     Ls[MT*BM]        stream length at each sorted position
-//     RA[MT*BM]        row marginal  sum_d sum_{l<L} zA   (bipolar, both sequences)
-//     tileL[MT]        cycles the GEMM runs for row tile t (max L in tile, padded to 4; MFMA
-//                      engine with 256-row blocks: max L of the tile pair, padded to 8)
+//     tileL[MT]        cycles the GEMM runs for row tile t: the longest L of the tile (of
+//                      the tile pair with 256-row blocks), rounded up to 8
 //     tileOff[MT]      word offset of tile t's planes inside Ap
-//     Ap               bit planes of A: for tile t, words [KB][tileL[t]][BM]
-//     SA               sign planes of A (unipolar; bipolar C-BSG): [MT][KB][BM]
-//   part       partial counts when GEMM tiles are split along the element blocks
+//     Ap               fp4 planes of A (or int8 chunks, below)
+//   part       partial counts when GEMM tiles are split along the inner (element, cycle) range
 //   per batch entry of B (1 if B is broadcast, else batch entries):
-//     Bp               bit planes of B: [NT][KB][LBS][BN]
-//     SB               sign planes of B (unipolar): [NT][KB][BN]
-//     RB               prefix marginals RB[j][L] = sum_d sum_{l<L} zB, L = 0..L_max
-//                      (bipolar with the LFSR sequence only)
+//     Bp               fp4 planes of B (or int8 chunks)
 //
-// A "bit plane" word packs 32 consecutive inner-dimension elements d = 32*kb .. 32*kb+31
-// of one row at one cycle l: bit t = z[row][32*kb + t][l].  With C-BSG the planes of A
-// are indexed by B's draw counter k instead of the cycle (see k_planes).
+// Each stream bit is an fp4 (e2m1) value in {-1, 0, +1} ("nibble planes").  A slot is
+// (octet o of 8 cycles, element quad dq of 4 elements) and holds 16 bytes: dword e =
+// element 4*dq+e, nibble c = cycle 8*o+c, with value +1 (0x2), -1 (0xA) or 0.  Slots are
+// ordered s = o * KQP + dq and each slot stores its 128 rows contiguously: A tile t is
+// uint4 [Lloop/8 * KQP][128], B tile is uint4 [LBS/8 * KQP][128].  A row of length L has
+// zero nibbles at cycles >= L.
 //
-// MFMA engine: Ap and Bp hold fp4 (e2m1) "nibble planes" instead; there are no
-// marginals and no sign planes.  A slot is (octet o of 8 cycles, element quad dq of 4
-// elements) and holds 16 bytes: dword e = element 4*dq+e, nibble c = cycle 8*o+c, with
-// value +1 (0x2), -1 (0xA) or 0.  Slots are ordered s = o * KQP + dq and each slot
-// stores its 128 rows contiguously: A tile t is uint4 [Lloop/8 * KQP][128], B tile is
-// uint4 [LBS/8 * KQP][128].  A row of length L has zero nibbles at cycles >= L.
+// 256 x 256 GEMM blocks with comparator streams (rgen): no planes.  Ap and Bp hold the int8
+// operands in 32-element chunks instead: pair t of 256 rows (A in the scheduler's order) is
+// bytes [KC][256][32], byte e of row r of chunk c = element 32c + e, with -128 read as -127
+// (the same comparator boundaries) and 0x80 (-128) marking an element >= K or a padding
+// row.  The GEMM builds the fp4 fragments from them.
 //
-// MFMA engine, 256 x 256 GEMM blocks with comparator streams (rgen): no planes.  Ap and Bp
-// hold the int8 operands in 32-element chunks instead: pair t of 256 rows (A in the
-// scheduler's order) is bytes [KC][256][32], byte e of row r of chunk c = element 32c + e,
-// with -128 read as -127 (the same comparator boundaries) and 0x80 (-128) marking an
-// element >= K or a padding row.  The GEMM builds the fp4 fragments from them.
+// N <= 128 with comparator streams (fused): no planes either; the GEMM builds its fragments
+// from the int8 rows themselves.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -51,24 +45,19 @@
 
 #include "../../include/scgemm.h"
 
+static_assert(SC_KL_LIMIT == 8ll << 24, "K * L_max limit: MAX_SPLIT parts of 2^24 products");
+
 namespace scg {
 
 constexpr int BM = 128;          // rows of A per GEMM tile
 constexpr int BN = 128;          // rows of B per GEMM tile
-constexpr int LSTEP = 4;         // GEMM cycle loop granularity (tile lengths padded to it)
-constexpr int LCH = 32;          // cycles per LDS stage and per plane-generation block
+constexpr int LCH = 32;          // cycle granularity of the draw arrays and B's planes
 constexpr uint32_t STATUS_BAD_LENGTH = 1u;
-constexpr int CUS = 256;         // compute units of an MI355X (work-unit balancing target)
-constexpr int MAX_SPLIT = 8;
+constexpr int DEFAULT_CUS = 256; // compute units of an MI355X, when no device can be queried
+constexpr int MAX_SPLIT = 8;     // most parts a GEMM tile is split into along its inner range
 constexpr int CBSG_L_MAX = 256;  // one period of the 8-bit Sobol sequences
 constexpr int CA_COLS = 257;     // boundaries 0..256
 
-// counting modes of the GEMM hot loop and its decode
-constexpr int MODE_AND = 0;      // bipolar, LFSR: AND counts plus both marginals
-constexpr int MODE_SIGNED = 1;   // unipolar: popc((a & b) ^ sA ^ sB), signed AND counts
-constexpr int MODE_CBSG = 2;     // bipolar C-BSG: popc((D & Z) ^ sA) plus A's marginal
-
-// MFMA engine
 constexpr int MSTEP = 8;         // cycles per octet (tile lengths padded to it)
 constexpr int MSTAGE = 4;        // slots per LDS stage of the MFMA GEMM (2 MFMA k-steps)
 constexpr int MFMA_BLOCKS_PER_CU = 2;   // resident 128-row MFMA GEMM blocks per CU (LDS bound)
@@ -91,7 +80,7 @@ __host__ __device__ inline double quad_split_time(int64_t tiles, int s, double p
 }
 constexpr int OCH = 8;           // octets per block of the nibble-plane generator
 constexpr int RSLOTS = 4;        // int8-chunk GEMM: tables masked to a row length, per cycle group
-constexpr int64_t MFMA_EXACT = 1ll << 24;   // K * L_max bound for exact fp32 counts
+constexpr int64_t MFMA_EXACT = 1ll << 24;   // products one fp32 accumulator sums exactly
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -113,34 +102,30 @@ __device__ __forceinline__ T *ws_ptr(uint8_t *ws, size_t off) {
 }
 
 struct Layout {
-    int KB;            // words per cycle per row = ceil(K/32)
-    int MT, NT;        // row tiles of A and B (MFMA engine: NT rounded up to a multiple
-                       // of mbn / 128, the B plane tiles one GEMM block takes)
+    int MT, NT;        // row tiles of A and B (NT rounded up to a multiple of mbn / 128, the
+                       // B tiles one GEMM block takes)
     int LBS;           // cycle stride of B planes and length of draw arrays (L_max rounded to LCH)
-    int LP;            // L_max rounded up to LSTEP
     int nbB;           // batch entries of B planes (1 when B is broadcast)
-    int mode;          // MODE_AND, MODE_SIGNED or MODE_CBSG (VALU engine)
-    int engine;        // SC_ENGINE_VALU or SC_ENGINE_MFMA (resolved, never AUTO)
-    int KQP;           // MFMA: element quads per octet, ceil(K/4) rounded up to 4
-    int tstep;         // tile cycle counts are rounded up to this (LSTEP or MSTEP)
-    int mbn;           // MFMA engine: columns of B per GEMM block (256, or 128 when N <= 128)
-    int fused;         // MFMA engine, N <= 128, comparator streams: the GEMM builds its fp4
-                       // fragments from the int8 operands (no planes in the workspace)
-    int mbm;           // MFMA engine: rows of A per GEMM block: 256 (row tiles taken in pairs
-                       // that run at the pair's longest length; MT even) when mbn = 256 and
-                       // MT > 1, else 128
+    int KQP;           // element quads per octet, ceil(K/4) rounded up to 4
+    int mbn;           // columns of B per GEMM block (256, or 128 when N <= 128)
+    int fused;         // N <= 128, comparator streams: the GEMM builds its fp4 fragments from
+                       // the int8 operands (no planes in the workspace)
+    int mbm;           // rows of A per GEMM block: 256 (row tiles taken in pairs that run at
+                       // the pair's longest length; MT even) when mbn = 256 and MT > 1, else 128
     int rgen;          // 256-row GEMM with comparator streams: fragments built in the GEMM
                        // from int8 chunks and a per-group table (no planes)
     int narrow;        // rgen with N <= 64: blocks of 256 rows x 64 columns
     int rslots;        // rgen: tables masked to a row length per cycle group (0 when narrow)
     int KC;            // 32-element chunks per row, ceil(K/32)
+    int cus;           // compute units of the device the call runs on
     int64_t words_per_L;   // plane words of one 128-row tile per cycle of its length
     size_t off_rA, off_rB, off_status, off_CA, off_rtab;
-    size_t off_perm, off_Ls, off_RA, off_tileL, off_tileOff, off_Ap, off_SA;
+    size_t off_perm, off_Ls, off_tileL, off_tileOff, off_Ap;
     size_t stride_batchA;          // bytes per A batch entry block
-    size_t off_Bp, off_SB, off_RB;
+    size_t off_Bp;
     size_t stride_batchB;          // bytes per B batch entry block
-    int S;             // splits of the element blocks per GEMM tile (1 = no split)
+    int S;             // splits of the inner range per GEMM tile (1 = no split)
+    int Smin;          // fewest splits that keep every part's fp32 sums exact (<= 2^24 products)
     int F;             // 256-row GEMM: tiles 0 .. F-1 run whole, tiles F.. in S parts each
     double q_perL, q_Lmean;   // 256-row GEMM split model: seconds per cycle of one tile, mean L
     int q_one;                // 256-row GEMM split model: all rows have one length
@@ -149,8 +134,9 @@ struct Layout {
     size_t total;
 };
 
-// Host-side layout computation (no HIP calls).  Returns false on overflow.
-bool make_layout(const sc_gemm_desc &d, Layout *lay);
+// Host-side layout computation for a device with `cus` compute units (no HIP calls).
+// Returns false on overflow or when no split count up to MAX_SPLIT keeps the counts exact.
+bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay);
 
 // Kernel launchers (sc_kernels.hip).  All return hipSuccess or the launch error.
 hipError_t launch_draws(uint64_t seed, int rng, int n, uint32_t *rA, uint32_t *rB,
@@ -159,14 +145,8 @@ hipError_t launch_cbsg_table(const uint32_t *rA, int L_max, uint16_t *CA, hipStr
 // draws: also clear the status words and make the comparator sequences (one batch entry only)
 hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L,
                            uint8_t *ws, bool draws, hipStream_t st);
-hipError_t launch_marginals(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,
-                            const int8_t *B, uint8_t *ws, hipStream_t st);
-hipError_t launch_planes(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,
-                         const int8_t *B, uint8_t *ws, hipStream_t st);
-hipError_t launch_gemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,
-                       float *out, int32_t *counts, uint8_t *ws, hipStream_t st);
 
-// MFMA engine (sc_mfma.hip)
+// counting GEMM (sc_mfma.hip)
 hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,
                           const int8_t *B, uint8_t *ws, hipStream_t st);
 hipError_t launch_mgemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,

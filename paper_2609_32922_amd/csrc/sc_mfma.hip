@@ -11,8 +11,9 @@
 //             counter k, B holds its comparator stream on r^B as above; bipolar then
 //             gives X = (K L + P) / 2 and unipolar S = P (Sec. 4.2, Eq. (6))
 // v_mfma_scale_f32_32x32x64_f8f6f4 with unit scales sums 64 such products into fp32;
-// every partial sum is an integer of magnitude <= K L <= 2^24, so the count is exact
-// and independent of the summation order.
+// a work unit sums at most 2^24 products per output (longer inner ranges are split, see
+// make_layout), so every partial sum is an exact integer, the int32 partial counts of a
+// split tile add exactly, and the count is independent of the summation order.
 //
 //   k_mplanes     nibble planes of A (sorted rows, per-row lengths) or B, one block per
 //                 128-row tile x 64 cycles x 64 elements; element parameters and an
@@ -1124,7 +1125,8 @@ __device__ __forceinline__ void q_stage(int st, int nst, int64_t k0, int64_t k1,
 
 // The division of the call's tiles into units: (F, S) from the host, or, when the host
 // split every tile (F = 0), the split count chosen again with the longest tile pair the
-// scheduler found (never above the host's, for which grid and partial sums are sized).
+// scheduler found (never above the host's, for which grid and partial sums are sized, nor
+// below Smin, which keeps every part's sums exact).
 __device__ __forceinline__ void q_division(const MGemmArgs &g, const Layout &lay, uint8_t *ws, int &F, int &S) {
     const int tiles = g.batch * (lay.MT / 2) * (lay.NT / 2);
     F = g.F;
@@ -1132,9 +1134,9 @@ __device__ __forceinline__ void q_division(const MGemmArgs &g, const Layout &lay
     if (F == 0 && S > 1) {
         const double Lmax = (double)ws_ptr<uint32_t>(ws, lay.off_status)[1];
         double best = 0.0;
-        for (int s = 1; s <= g.S; s *= 2) {
+        for (int s = lay.Smin; s <= g.S; s *= 2) {
             const double est = quad_split_time(tiles, s, lay.q_perL, lay.q_Lmean, Lmax, lay.q_one != 0, lay.q_slots);
-            if (s == 1 || est < best * 0.97) {
+            if (s == lay.Smin || est < best * 0.97) {
                 best = est;
                 S = s;
             }

@@ -20,8 +20,8 @@ def lib():
     return L
 
 
-def _declared_functions():
-    text = open(HEADER).read()
+def _declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(sc_\w+)\s*\(", text, flags=re.M)))
 
@@ -34,6 +34,52 @@ def test_every_declared_symbol_is_exported(lib):
         assert hasattr(so, n), n
 
 
+def test_every_header_is_served_by_a_library(lib):
+    # include/scgemm.h by libscgemm, include/scpeak.h by libscpeak (the benchmark's VALU
+    # peak measurement); no other header
+    from paper_2609_32922_amd import peak
+    served = {"scgemm.h": lib.LIB_PATH, "scpeak.h": peak.LIB_PATH}
+    headers = sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
+    assert headers == sorted(served)
+    for h, path in served.items():
+        so = ctypes.CDLL(path)
+        names = _declared_functions(os.path.join(ROOT, "include", h))
+        assert names
+        for n in names:
+            assert hasattr(so, n), (h, n)
+
+
+def test_peak_result_layout_matches_header(tmp_path):
+    from paper_2609_32922_amd import peak
+    src = tmp_path / "peak.c"
+    src.write_text("""
+#include <stdio.h>
+#include <stddef.h>
+#include "scpeak.h"
+#define F(f) printf("%s %zu\\n", #f, offsetof(sc_peak_result, f));
+int main(void) {
+  printf("size %zu\\n", sizeof(sc_peak_result));
+  F(seconds) F(lane_ops_per_s) F(bitops_per_s) F(clock_hz) F(cus) F(waves_per_simd)
+  return 0;
+}
+""")
+    exe = tmp_path / "peak"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    got = dict(ln.split()[:2] for ln in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                         check=True).stdout.split("\n") if ln)
+    R = peak.ScPeakResult
+    assert int(got["size"]) == ctypes.sizeof(R)
+    for name, _ in R._fields_:
+        assert int(got[name]) == getattr(R, name).offset, name
+    # argument errors return before any HIP call
+    so = peak.load()
+    r = peak.ScPeakResult()
+    assert so.sc_peak_valu_bitop(0, 10, ctypes.byref(r)) == -1
+    assert so.sc_peak_valu_bitop(9, 10, ctypes.byref(r)) == -1
+    assert so.sc_peak_valu_bitop(1, 0, ctypes.byref(r)) == -1
+    assert so.sc_peak_valu_bitop(1, 10, None) == -1
+
+
 def test_desc_layout_matches_header(lib, tmp_path):
     src = tmp_path / "layout.c"
     src.write_text("""
@@ -44,10 +90,10 @@ def test_desc_layout_matches_header(lib, tmp_path):
 int main(void) {
   printf("size %zu\\n", sizeof(sc_gemm_desc));
   F(batch) F(M) F(N) F(K) F(lda) F(ldb) F(ldo) F(strideA) F(strideB) F(strideO)
-  F(strideSA) F(strideSB) F(strideL) F(L_max) F(polarity) F(rng) F(L_hint) F(engine)
+  F(strideSA) F(strideSB) F(strideL) F(L_max) F(polarity) F(rng) F(L_hint)
   F(reserved) F(seed)
   F(prof_event_begin) F(prof_event_end)
-  printf("L_MAX %d K_LIMIT %d\\n", SC_L_MAX_LIMIT, SC_K_LIMIT);
+  printf("L_MAX %d K_LIMIT %d KL_LIMIT %lld\\n", SC_L_MAX_LIMIT, SC_K_LIMIT, (long long)SC_KL_LIMIT);
   return 0;
 }
 """)
@@ -61,6 +107,7 @@ int main(void) {
         assert int(got[name]) == getattr(D, name).offset, name
     last = [ln for ln in lines if ln.startswith("L_MAX")][0].split()
     assert int(last[1]) == lib.SC_L_MAX_LIMIT and int(last[3]) == lib.SC_K_LIMIT
+    assert int(last[5]) == lib.SC_KL_LIMIT
 
 
 def _desc(lib, **kw):
@@ -77,7 +124,7 @@ def _desc(lib, **kw):
     ("M", -1, -2), ("K", -5, -2), ("batch", -1, -2), ("K", (1 << 20) + 1, -2),
     ("L_max", 0, -3), ("L_max", 4097, -3), ("polarity", 2, -4), ("rng", 2, -5), ("rng", -1, -5),
     ("L_hint", 65, -3), ("L_hint", -1, -3), ("lda", 255, -9), ("ldo", 63, -9), ("strideA", -1, -9),
-    ("engine", 3, -10), ("engine", -1, -10), ("reserved", 1, -10),
+    ("reserved", 1, -10), ("reserved", -1, -10),
 ])
 def test_workspace_size_rejects_bad_desc(lib, field, value, code):
     n = ctypes.c_size_t(0)
@@ -93,24 +140,27 @@ def test_cbsg_length_limit(lib):
     n = ctypes.c_size_t(0)
     d = _desc(lib, rng=1, L_max=257, L_hint=0)
     assert so.sc_gemm_workspace_size(ctypes.byref(d), ctypes.byref(n)) == lib.SC_ERR_LEN
-    # on the VALU engine C-BSG keeps a count table but no marginals of B
-    lfsr = lib.sc_gemm_workspace_size(_desc(lib, L_max=256, N=4096, ldo=4096, engine=1))
-    cbsg = lib.sc_gemm_workspace_size(_desc(lib, rng=1, L_max=256, N=4096, ldo=4096, engine=1))
-    assert cbsg < lfsr
 
 
-def test_mfma_engine_exactness_bound(lib):
-    # fp32 counts are exact only while K * L_max <= 2^24: an explicit MFMA request past
-    # it is refused, AUTO takes the VALU engine there
+def test_exactness_bound_splits(lib):
+    # fp32 sums stay exact for 2^24 products per part: past that the inner range is split
+    # (int32 partial sums, more workspace), and past 8 parts (K * L_max > 2^27) refused
     so = lib.load()
     n = ctypes.c_size_t(0)
-    big = _desc(lib, K=65536, lda=65536, ldb=65536, L_max=512, engine=lib.SC_ENGINE_MFMA)
-    assert so.sc_gemm_workspace_size(ctypes.byref(big), ctypes.byref(n)) == lib.SC_ERR_ENGINE
-    for eng in (lib.SC_ENGINE_AUTO, lib.SC_ENGINE_VALU):
-        ok = _desc(lib, K=65536, lda=65536, ldb=65536, L_max=512, engine=eng)
-        assert lib.sc_gemm_workspace_size(ok) > 0
-    at = _desc(lib, K=65536, lda=65536, ldb=65536, L_max=256, engine=lib.SC_ENGINE_MFMA)
-    assert lib.sc_gemm_workspace_size(at) > 0
+    # 4096 x 4096: 256 tiles of 256 x 256, one round on 256 CUs, so nothing is split at
+    # K * L_max = 2^24; one chunk more and every tile is split in two
+    at = lib.sc_gemm_workspace_size(_desc(lib, M=4096, N=4096, ldo=4096, K=4096, lda=4096, ldb=4096,
+                                          L_max=4096))
+    past = lib.sc_gemm_workspace_size(_desc(lib, M=4096, N=4096, ldo=4096, K=4128, lda=4128, ldb=4128,
+                                            L_max=4096))
+    assert past >= at + 2 * 4096 * 4096 * 4
+    for M, N in ((64, 64), (64, 300), (300, 300), (300, 64)):
+        top = _desc(lib, M=M, N=N, ldo=N, K=32768, lda=32768, ldb=32768, L_max=4096)
+        assert lib.sc_gemm_workspace_size(top) > 0
+        over = _desc(lib, M=M, N=N, ldo=N, K=32769, lda=32769, ldb=32769, L_max=4096)
+        assert so.sc_gemm_workspace_size(ctypes.byref(over), ctypes.byref(n)) == lib.SC_ERR_SHAPE
+        cb = _desc(lib, M=M, N=N, ldo=N, K=524288, lda=524288, ldb=524288, L_max=256, rng=1)
+        assert lib.sc_gemm_workspace_size(cb) > 0
 
 
 def test_workspace_size_values(lib):

@@ -45,16 +45,12 @@ def _to_dev(g, dev):
             torch.from_numpy(np.ascontiguousarray(g.L)).to(dev))
 
 
-ENGINES = [1, 2]            # SC_ENGINE_VALU, SC_ENGINE_MFMA
-ENGINE_IDS = ["valu", "mfma"]
-
-
-def _run(g, dev, check_status=True, rng=0, engine=0):
+def _run(g, dev, check_status=True, rng=0):
     import torch
     import paper_2609_32922_amd as scg
     A, sA, B, sB, L = _to_dev(g, dev)
     out, cnt = scg.gemm(A, sA, B, sB, L, L_max=g.L_max, polarity=g.polarity, seed=g.seed,
-                        want_counts=True, check_status=check_status, rng=rng, engine=engine)
+                        want_counts=True, check_status=check_status, rng=rng)
     torch.cuda.synchronize()
     return out.cpu().numpy(), cnt.cpu().numpy()
 
@@ -84,11 +80,10 @@ def test_comparator_sequence_matches_oracle(dev, oracle_mod):
             assert np.array_equal(r, oracle_mod.comparator_sequence(seed, op, 4096))
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
-def test_bipolar_64x256x64_full(dev, oracle_mod, engine):
+def test_bipolar_64x256x64_full(dev, oracle_mod):
     g = W.bipolar_64x256x64().gemms[0]
-    _note("bipolar_64x256x64 full engine %d" % engine)
-    out, cnt = _run(g, dev, engine=engine)
+    _note("bipolar_64x256x64 full")
+    out, cnt = _run(g, dev)
     _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "64x256x64")
 
 
@@ -115,31 +110,29 @@ FUZZ = [
 ]
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
 @pytest.mark.parametrize("case", FUZZ, ids=[str(c) for c in FUZZ])
-def test_fuzz_full_compare(dev, oracle_mod, case, engine):
+def test_fuzz_full_compare(dev, oracle_mod, case):
     batch, M, N, K, L_max, L_lo, pol, bcast, seed = case
     rng = np.random.default_rng(seed)
     g = W.random_gemm(rng, batch, M, N, K, L_max, pol, seed, L_lo=L_lo, broadcast_B=bcast)
-    _note("fuzz %s engine %d" % (case, engine))
-    out, cnt = _run(g, dev, engine=engine)
+    _note("fuzz %s" % (case,))
+    out, cnt = _run(g, dev)
     for b in range(batch):
         _compare(g, b, np.arange(M), np.arange(N), out, cnt, oracle_mod, "fuzz%s b%d" % (case, b))
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
-def test_zero_lengths_and_K0(dev, oracle_mod, engine):
+def test_zero_lengths_and_K0(dev, oracle_mod):
     rng = np.random.default_rng(31)
     g = W.random_gemm(rng, 1, 150, 140, 40, 64, 0, 31)
     g.L[0, ::3] = 0
-    _note("zero lengths engine %d" % engine)
-    out, cnt = _run(g, dev, engine=engine)
+    _note("zero lengths")
+    out, cnt = _run(g, dev)
     assert np.all(cnt[0, ::3] == 0) and np.all(out[0, ::3] == 0)
     _compare(g, 0, np.arange(150), np.arange(140), out, cnt, oracle_mod, "zeroL")
     for pol in (0, 1):
         g0 = W.random_gemm(rng, 1, 10, 12, 0, 16, pol, 5)
         _note("K=0 polarity %d" % pol)
-        out, cnt = _run(g0, dev, engine=engine)
+        out, cnt = _run(g0, dev)
         assert np.all(cnt == 0) and np.all(out == 0)
 
 
@@ -160,21 +153,17 @@ def test_out_of_range_lengths_set_status(dev):
     _run(g, dev, check_status=True)          # a good call clears the status
 
 
-def test_deterministic_repeat_and_engines_agree(dev):
+def test_deterministic_repeat(dev):
     rng = np.random.default_rng(51)
     g = W.random_gemm(rng, 1, 260, 300, 160, 96, 0, 51)
     _note("determinism")
-    o1, c1 = _run(g, dev, engine=2)
-    o2, c2 = _run(g, dev, engine=2)
+    o1, c1 = _run(g, dev)
+    o2, c2 = _run(g, dev)
     assert np.array_equal(c1, c2) and np.array_equal(o1.view(np.uint32), o2.view(np.uint32))
-    # the two engines give bit-identical counts and decoded floats
-    o3, c3 = _run(g, dev, engine=1)
-    assert np.array_equal(c1, c3) and np.array_equal(o1.view(np.uint32), o3.view(np.uint32))
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
 @pytest.mark.parametrize("polarity", [0, 1])
-def test_longest_streams(dev, oracle_mod, polarity, engine):
+def test_longest_streams(dev, oracle_mod, polarity):
     # L_max at the library's limit (4096 cycles), rows at exactly L_max and at 0, on a
     # ragged 300 x 270 shape (an odd count of 128-row tiles, so the 256-row MFMA blocks
     # take a padded pair); every output against the oracle
@@ -183,8 +172,8 @@ def test_longest_streams(dev, oracle_mod, polarity, engine):
     g = W.random_gemm(rng, 1, 300, 270, 100, scg.SC_L_MAX_LIMIT, polarity, 201 + polarity)
     g.L[0, :7] = scg.SC_L_MAX_LIMIT
     g.L[0, 7:11] = 0
-    _note("longest streams polarity %d engine %d" % (polarity, engine))
-    out, cnt = _run(g, dev, engine=engine)
+    _note("longest streams polarity %d" % polarity)
+    out, cnt = _run(g, dev)
     _compare(g, 0, np.arange(300), np.arange(270), out, cnt, oracle_mod, "Lmax%d pol%d" % (g.L_max, polarity))
 
 
@@ -204,21 +193,6 @@ def test_split_partials_extreme(dev, oracle_mod, polarity):
     assert np.array_equal(cnt[0], np.broadcast_to(cnt[0][:1], cnt[0].shape))
     rows = np.union1d(_sample(M, rng, 4), [0, 5375, 5376, 5600, 5900, 6200, 6303])
     _compare(g, 0, rows, np.arange(N), out, cnt, oracle_mod, "extreme pol%d" % polarity)
-
-
-@pytest.mark.parametrize("name", ["vitb16_fc1_L128", "vitb16_fc1_mp64", "ditxl2_proj_mlp_group96"])
-def test_engines_agree_full_size(dev, name):
-    # Every output of the full-size layers: the MFMA engine (256 x 256 tiles, whole tiles
-    # plus a split tail at uniform L, every tile split when the lengths vary) against the
-    # VALU engine, bit for bit.  Each engine is pinned to the oracle by the tests above.
-    w = W.WORKLOADS[name]()
-    for g in w.gemms:
-        _note("engines agree %s/%s" % (name, g.name))
-        o_m, c_m = _run(g, dev, engine=2)
-        o_v, c_v = _run(g, dev, engine=1)
-        bad = np.argwhere(c_m != c_v)
-        assert bad.size == 0, "%s/%s: %d count mismatches, first at %s" % (name, g.name, len(bad), bad[0])
-        assert np.array_equal(o_m.view(np.uint32), o_v.view(np.uint32)), name + ": decoded floats differ"
 
 
 # --------------------------------------------------------------------------
@@ -257,7 +231,7 @@ def _rgen_gemm(case):
 def test_rgen_full_compare(dev, oracle_mod, case):
     g = _rgen_gemm(case)
     _note("int8-chunk GEMM %s" % (case,))
-    out, cnt = _run(g, dev, engine=2)
+    out, cnt = _run(g, dev)
     for b in range(g.batch):
         _compare(g, b, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "rgen%s b%d" % (case, b))
 
@@ -280,7 +254,7 @@ def test_rgen_length_ladders(dev, oracle_mod, case, polarity):
     g = W.random_gemm(rng, 2, 300, 260, 40, L_max, polarity, 91 + polarity)
     g.L = rng.choice(np.array(lengths, np.int32), g.L.shape).astype(np.int32)
     _note("length ladder %s polarity %d" % (name, polarity))
-    out, cnt = _run(g, dev, engine=2)
+    out, cnt = _run(g, dev)
     for b in range(g.batch):
         _compare(g, b, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "ladder %s pol%d b%d" % (name, polarity, b))
 
@@ -292,10 +266,9 @@ INT8_MIN_SHAPES = [
 ]
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
 @pytest.mark.parametrize("polarity", [0, 1])
 @pytest.mark.parametrize("shape", INT8_MIN_SHAPES, ids=[str(x) for x in INT8_MIN_SHAPES])
-def test_int8_min(dev, oracle_mod, shape, polarity, engine):
+def test_int8_min(dev, oracle_mod, shape, polarity):
     # -128 lies outside the documented [-127, 127] but has the comparator boundaries of
     # -127 in both polarities (a unipolar magnitude boundary past 256: a one on every
     # cycle); every path must match the oracle on it, rows that end early included
@@ -305,8 +278,8 @@ def test_int8_min(dev, oracle_mod, shape, polarity, engine):
     g = W.random_gemm(rng, 1, M, N, K, 80, polarity, seed)
     g.A[0, ::5, ::3] = -128
     g.B[0, ::7, 1::4] = -128
-    _note("int8 minimum %s polarity %d engine %d" % (shape, polarity, engine))
-    out, cnt = _run(g, dev, rng=rng_kind, engine=engine)
+    _note("int8 minimum %s polarity %d" % (shape, polarity))
+    out, cnt = _run(g, dev, rng=rng_kind)
     _compare(g, 0, np.arange(M), np.arange(N), out, cnt, oracle_mod, "int8min %s pol%d" % (shape, polarity),
              rng=rng_kind)
 
@@ -321,11 +294,11 @@ def _sample(n, rng, k):
     return np.array(sorted(set(i for i in base + extra if 0 <= i < n)), dtype=np.int64)
 
 
-def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None, seq=0, engine=0):
+def _check_workload(w, dev, oracle_mod, nrows=40, ncols=96, batches=None, seq=0):
     rng = np.random.default_rng(7)
     for g in w.gemms:
-        _note("%s/%s full size %s rng %d engine %d" % (w.name, g.name, g.A.shape, seq, engine))
-        out, cnt = _run(g, dev, rng=seq, engine=engine)
+        _note("%s/%s full size %s rng %d" % (w.name, g.name, g.A.shape, seq))
+        out, cnt = _run(g, dev, rng=seq)
         KL = g.K * g.L.astype(np.int64)
         if g.polarity == 0:
             assert np.all(cnt >= 0) and np.all(cnt <= KL[:, :, None])
@@ -364,18 +337,16 @@ def test_schedule_long_batch_entries(dev, oracle_mod, case):
     assert np.all(cnt[1, M - 1] == 0)
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
-def test_workload_vitb16_fc1_L128(dev, oracle_mod, engine):
-    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod, engine=engine)
+def test_workload_vitb16_fc1_L128(dev, oracle_mod):
+    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod)
 
 
 def test_workload_vitb16_fc1_mp64(dev, oracle_mod):
     _check_workload(W.vitb16_fc1_mp64(), dev, oracle_mod)
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
-def test_workload_ditxl2_proj_mlp_group96(dev, oracle_mod, engine):
-    _check_workload(W.ditxl2_proj_mlp_group96(), dev, oracle_mod, engine=engine)
+def test_workload_ditxl2_proj_mlp_group96(dev, oracle_mod):
+    _check_workload(W.ditxl2_proj_mlp_group96(), dev, oracle_mod)
 
 
 def test_workload_vitl14_336_qk_mlp(dev, oracle_mod):
@@ -454,7 +425,6 @@ def test_rgen_strided(dev, oracle_mod, polarity, shift):
     d.strideA, d.strideB, d.strideO = sA_, sB_, sO_
     d.strideSA, d.strideSB, d.strideL = M, N, M
     d.L_max, d.polarity, d.rng, d.L_hint, d.seed = L_max, polarity, 0, 0, 171
-    d.engine = 2
     tA, tB, tsa, tsb, tL = (torch.from_numpy(a).to(dev) for a in (Abuf, Bbuf, sa, sb, L))
     out = torch.zeros(batch * sO_, dtype=torch.float32, device=dev)
     cnt = torch.zeros(batch * sO_, dtype=torch.int32, device=dev)
@@ -511,21 +481,19 @@ CBSG_FUZZ = [
 ]
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
 @pytest.mark.parametrize("case", CBSG_FUZZ, ids=[str(c) for c in CBSG_FUZZ])
-def test_cbsg_fuzz_full_compare(dev, oracle_mod, case, engine):
+def test_cbsg_fuzz_full_compare(dev, oracle_mod, case):
     batch, M, N, K, L_max, L_lo, pol, bcast, seed = case
     rng = np.random.default_rng(seed)
     g = W.random_gemm(rng, batch, M, N, K, L_max, pol, seed, L_lo=L_lo, broadcast_B=bcast)
-    _note("cbsg fuzz %s engine %d" % (case, engine))
-    out, cnt = _run(g, dev, rng=1, engine=engine)
+    _note("cbsg fuzz %s" % (case,))
+    out, cnt = _run(g, dev, rng=1)
     for b in range(batch):
         _compare(g, b, np.arange(M), np.arange(N), out, cnt, oracle_mod,
                  "cbsg%s b%d" % (case, b), rng=1)
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
-def test_cbsg_extreme_values(dev, oracle_mod, engine):
+def test_cbsg_extreme_values(dev, oracle_mod):
     """Saturated and zero operands: c = 0, c = L and c = L - c hit every branch of the
     interval planes (empty interval, full interval, sign flips)."""
     rng = np.random.default_rng(131)
@@ -534,8 +502,8 @@ def test_cbsg_extreme_values(dev, oracle_mod, engine):
         vals = np.array([-127, -126, -1, 0, 1, 126, 127], np.int8)
         g.A[0] = rng.choice(vals, g.A[0].shape)
         g.B[0] = rng.choice(vals, g.B[0].shape)
-        _note("cbsg extremes polarity %d engine %d" % (pol, engine))
-        out, cnt = _run(g, dev, rng=1, engine=engine)
+        _note("cbsg extremes polarity %d" % pol)
+        out, cnt = _run(g, dev, rng=1)
         _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod,
                  "cbsg extremes %d" % pol, rng=1)
 
@@ -566,9 +534,8 @@ def test_cbsg_bad_lengths_set_status(dev):
     assert ei.value.code == scg.SC_ERR_DEVICE_STATUS
 
 
-@pytest.mark.parametrize("engine", ENGINES, ids=ENGINE_IDS)
-def test_cbsg_workload_vitb16_fc1_L128(dev, oracle_mod, engine):
-    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod, nrows=24, ncols=64, seq=1, engine=engine)
+def test_cbsg_workload_vitb16_fc1_L128(dev, oracle_mod):
+    _check_workload(W.vitb16_fc1_L128(), dev, oracle_mod, nrows=24, ncols=64, seq=1)
 
 
 def test_cbsg_workload_vitb16_fc1_mp64(dev, oracle_mod):
@@ -580,32 +547,57 @@ def test_cbsg_workload_ditxl2_proj_mlp_group96(dev, oracle_mod):
 
 
 # --------------------------------------------------------------------------
-# the MFMA engine's exactness bound: fp32 sums of +-1 products stay exact while every
-# partial sum is an integer of magnitude <= K * L <= 2^24
+# exactness of the fp32 sums: a work unit sums at most 2^24 products per output; past
+# that the inner range is split and the parts' int32 partial counts are added
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("polarity", [0, 1])
-def test_mfma_exact_at_the_bound(dev, oracle_mod, polarity):
-    import paper_2609_32922_amd as scg
+def test_exact_at_the_bound(dev, oracle_mod, polarity):
     rng = np.random.default_rng(171 + polarity)
-    K, L = 65536, 256                          # K * L = 2^24 exactly
+    K, L = 65536, 256                          # K * L = 2^24 exactly: one unit may hold it all
     g = W.random_gemm(rng, 1, 3, 5, K, L, polarity, 171, L_lo=L)
     # saturated operands drive the counts to their extremes (|2X - K L| up to K L)
     g.A[0, 0] = 127
     g.B[0, 0] = 127 if polarity == 0 else -127
     g.A[0, 1] = -127
-    _note("mfma at K*L = 2^24, polarity %d" % polarity)
-    out, cnt = _run(g, dev, engine=scg.SC_ENGINE_MFMA)
+    _note("at K*L = 2^24, polarity %d" % polarity)
+    out, cnt = _run(g, dev)
     _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "bound")
 
 
-def test_auto_engine_past_the_bound(dev, oracle_mod):
-    """K * L_max = 2^25: AUTO runs the VALU engine (int32 counts), MFMA is refused."""
-    import paper_2609_32922_amd as scg
-    rng = np.random.default_rng(181)
-    g = W.random_gemm(rng, 1, 2, 3, 65536, 512, 0, 181, L_lo=500)
-    _note("auto engine at K*L_max = 2^25")
-    out, cnt = _run(g, dev, engine=scg.SC_ENGINE_AUTO)
-    _compare(g, 0, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "auto past bound")
-    with pytest.raises(scg.ScError) as ei:
-        _run(g, dev, engine=scg.SC_ENGINE_MFMA)
-    assert ei.value.code == scg.SC_ERR_ENGINE
+PAST_BOUND = [
+    # M, N, K, L_max, rng: every GEMM variant past K * L_max = 2^24: fragments
+    # from int8 rows (N <= 128), 128-row planes (M <= 128), int8 chunks in 256 x 256 and in
+    # 256 x 64 blocks, and with C-BSG the 256-row and 128-row planes GEMMs
+    # (the planes cases sit just past the bound: their planes take (M + N) K L / 2 bytes)
+    (3, 5, 65536, 512, 0),
+    (3, 129, 4128, 4096, 0),
+    (300, 300, 16384, 2048, 0),
+    (300, 17, 16384, 2048, 0),
+    (200, 200, 65600, 256, 1),
+    (3, 5, 65600, 256, 1),
+]
+
+
+@pytest.mark.parametrize("polarity", [0, 1])
+@pytest.mark.parametrize("case", PAST_BOUND, ids=[str(c) for c in PAST_BOUND])
+def test_exact_past_the_bound(dev, oracle_mod, case, polarity):
+    """Saturated rows and columns: every product +1 (or -1), so an unsplit fp32 sum would
+    pass 2^24 and round; the counts must still be exact.  Rows of full length and a few
+    shorter ones; the oracle on sampled rows and columns (B's streams of every column would
+    not fit in memory)."""
+    M, N, K, L_max, rng_kind = case
+    seed = 181 + polarity
+    rng = np.random.default_rng(seed + M + N)
+    g = W.random_gemm(rng, 1, M, N, K, L_max, polarity, seed, L_lo=L_max - 40)
+    g.L[0, :2] = L_max
+    g.A[0, 0] = 127
+    g.A[0, 1] = -127
+    g.B[0, 0] = 127
+    g.B[0, N - 1] = -127
+    _note("past the bound %s polarity %d" % (case, polarity))
+    out, cnt = _run(g, dev, rng=rng_kind)
+    rows = np.union1d([0, 1, M - 1], rng.choice(M, size=min(M, 3), replace=False))
+    cols = np.union1d([0, N - 1], rng.choice(N, size=min(N, 4), replace=False))
+    _compare(g, 0, rows, cols, out, cnt, oracle_mod, "past bound %s pol%d" % (case, polarity), rng=rng_kind)
+    if polarity == 0:
+        assert cnt[0, 0, 0] == K * L_max           # every XNOR is 1 (cycles and elements)
