@@ -119,3 +119,41 @@ def test_device_pipeline_end_to_end(dev, oracle_mod):
         nz = o_ref != 0
         assert np.all(o[~nz] == 0)
         assert np.max(np.abs(o[nz] - o_ref[nz]) / np.abs(o_ref[nz])) <= 1e-6
+
+
+def test_device_pipeline_with_threshold_table(dev, oracle_mod):
+    """The policy of Sec. 4.4 with its calibrated-threshold table: per layer the table gives
+    (thresholds, ladder) for the operator's timestep and layer bucket (or the operator-level
+    fallback); the device turns the row metric into lengths, which drive the SC GEMM."""
+    import os
+
+    import torch
+    import paper_2609_32922_amd as scg
+    from paper_2609_32922_amd.thresholds import ThresholdTable, mp_lengths_from_table
+    table = ThresholdTable.load(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                                             "thresholds_synthetic.json"))
+    rng = np.random.default_rng(6)
+    X = rng.laplace(0.0, 1.0, (260, 120)).astype(np.float32)
+    Wt = (rng.standard_normal((300, 120)) * 0.02).astype(np.float32)
+    for op, t, layer, want in [("mlp_fc1", 3, 27, "bucket"), ("mlp_fc1", 40, 0, "operator"),
+                               ("mlp_fc2", 12, 22, "bucket")]:
+        _note("table pipeline %s t=%d layer=%d" % (op, t, layer))
+        qX, sX, mX = scg.quantize(_t(X, dev), want_rowmax=True)
+        qW, sW, _ = scg.quantize(_t(Wt, dev), per_tensor=True)
+        L, thr = mp_lengths_from_table(mX, table, op, t, layer)
+        assert thr.source == want
+        L_max = thr.ladder[0]
+        out, cnt = scg.gemm(qX, sX, qW, sW, L, L_max=L_max, polarity=1, seed=13, want_counts=True,
+                            check_status=True)
+        torch.cuda.synchronize()
+        oq, osx, om = oracle_mod.quantize_rows_fp32(X)
+        ow, osw = oracle_mod.quantize_tensor_fp32(Wt)
+        oL = oracle_mod.mp_lengths_fp32(om, thr.tau, thr.ladder)
+        assert np.array_equal(L.cpu().numpy(), oL)
+        assert len(set(oL.tolist())) > 1
+        c_ref, o_ref = oracle_mod.sc_gemm(oq, ow, osx, osw, oL, L_max, 1, 13)
+        assert np.array_equal(cnt.cpu().numpy(), c_ref)
+        o = out.cpu().numpy().astype(np.float64)
+        nz = o_ref != 0
+        assert np.all(o[~nz] == 0)
+        assert np.max(np.abs(o[nz] - o_ref[nz]) / np.abs(o_ref[nz])) <= 1e-6
