@@ -146,6 +146,29 @@ int sc_gemm(const sc_gemm_desc *desc,
             void *workspace, size_t workspace_bytes,
             void *stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): sc_gemm with the same arguments except
+ * the workspace, which the library provides instead -- a static device array of
+ * SC_NOALLOC_WORKSPACE_BYTES on each device the library runs on, held until the process
+ * ends.  It calls no hipMalloc, hipFree or other allocating routine.
+ *   Returns SC_ERR_WORKSPACE when sc_gemm_workspace_size(desc) exceeds
+ *   SC_NOALLOC_WORKSPACE_BYTES (e.g. 6304 x 768 x 3072 at L = 128 needs 62 MiB), and the
+ *   other codes as sc_gemm.
+ *   status_out  NULLABLE device int32: after the call it holds the call's device status
+ *               word, 0 when every L_i was in [0, L_max], nonzero (bit 0) otherwise.
+ * Every call on a device uses that device's one array, which keeps the last call's
+ * contents (each call rewrites all it reads): calls that overlap in time on one device
+ * race, so order them, e.g. on one stream.
+ */
+#define SC_NOALLOC_WORKSPACE_BYTES ((size_t)64 << 20)
+int sc_gemm_noalloc(const sc_gemm_desc *desc,
+                    const int8_t *A, const float *sA,
+                    const int8_t *B, const float *sB,
+                    const int32_t *L_per_row,
+                    float *out, int32_t *counts, int32_t *status_out,
+                    void *stream);
+
 /* Synchronises `stream` and reads the device status word that the last sc_gemm on
  * `workspace` wrote: SC_OK, or SC_ERR_DEVICE_STATUS if some L_i was out of range. */
 int sc_gemm_status(const void *workspace, void *stream);

@@ -9,13 +9,13 @@ back to the CPU: without the built library every call raises.
 """
 from __future__ import annotations
 
-from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_ERR_RESERVED, SC_KL_LIMIT,  # noqa: F401
+from ._lib import (SC_BIPOLAR_XNOR, SC_ERR_DEVICE_STATUS, SC_ERR_RESERVED, SC_KL_LIMIT, SC_NOALLOC_WORKSPACE_BYTES,  # noqa: F401
                    SC_L_MAX_LIMIT, SC_OK, SC_RNG_LFSR32, SC_RNG_SOBOL8_CBSG, SC_UNIPOLAR_AND_SM,
-                   ScError, ScGemmDesc, load, sc_comparator_sequence, sc_gemm, sc_gemm_status,
+                   ScError, ScGemmDesc, load, sc_comparator_sequence, sc_gemm, sc_gemm_noalloc, sc_gemm_status,
                    sc_gemm_workspace_size, sc_mp_lengths, sc_quantize, sc_version, strerror)
 
 __all__ = ["gemm", "make_desc", "comparator_sequence", "quantize", "mp_lengths", "Workspace",
-           "ScGemmDesc", "ScError", "sc_gemm", "sc_gemm_workspace_size", "sc_gemm_status",
+           "ScGemmDesc", "ScError", "sc_gemm", "sc_gemm_noalloc", "sc_gemm_workspace_size", "sc_gemm_status",
            "sc_comparator_sequence", "sc_quantize", "sc_mp_lengths", "SC_BIPOLAR_XNOR",
            "SC_UNIPOLAR_AND_SM", "SC_RNG_LFSR32", "SC_RNG_SOBOL8_CBSG"]
 

@@ -31,6 +31,7 @@ SC_RNG_SOBOL8_CBSG = 1
 SC_L_MAX_LIMIT = 4096
 SC_K_LIMIT = 1 << 20
 SC_KL_LIMIT = 1 << 27
+SC_NOALLOC_WORKSPACE_BYTES = 64 << 20
 
 
 class ScGemmDesc(ctypes.Structure):
@@ -85,6 +86,8 @@ def load():
     lib.sc_gemm_workspace_size.restype = ctypes.c_int
     lib.sc_gemm.argtypes = [pdesc, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.sc_gemm.restype = ctypes.c_int
+    lib.sc_gemm_noalloc.argtypes = [pdesc, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.sc_gemm_noalloc.restype = ctypes.c_int
     lib.sc_gemm_status.argtypes = [vp, vp]
     lib.sc_gemm_status.restype = ctypes.c_int
     lib.sc_comparator_sequence.argtypes = [u64, i32, i32, i32, vp, vp]
@@ -121,6 +124,13 @@ def sc_gemm(desc: ScGemmDesc, A: int, sA: int, B: int, sB: int, L_per_row: int, 
     """Raw call with integer device addresses; returns the status code."""
     return int(load().sc_gemm(ctypes.byref(desc), A, sA, B, sB, L_per_row, out, counts or None,
                               workspace, workspace_bytes, stream or None))
+
+
+def sc_gemm_noalloc(desc: ScGemmDesc, A: int, sA: int, B: int, sB: int, L_per_row: int, out: int,
+                    counts: int, status_out: int, stream: int) -> int:
+    """Raw call of the allocation-free entry point (the library's own static workspace)."""
+    return int(load().sc_gemm_noalloc(ctypes.byref(desc), A, sA, B, sB, L_per_row, out, counts or None,
+                                      status_out or None, stream or None))
 
 
 def sc_gemm_status(workspace: int, stream: int) -> int:

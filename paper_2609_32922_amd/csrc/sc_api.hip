@@ -4,6 +4,7 @@
 #include <math.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "sc_internal.h"
 
@@ -311,6 +312,30 @@ static int enqueue(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, co
     return SC_OK;
 }
 
+// The workspace of sc_gemm_noalloc: a static device array, one copy per device, held until
+// the process ends.  Host code never uses its name as an address: the device address of
+// each device's copy is looked up once (hipGetSymbolAddress, with that device current) and
+// kept per device.
+static __device__ __align__(256) uint8_t scratch[SC_NOALLOC_WORKSPACE_BYTES];
+
+static bool scratch_address(uint8_t **ptr) {
+    constexpr int MAXDEV = 64;
+    static std::mutex mu;
+    static uint8_t *addr[MAXDEV] = {};
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAXDEV) return false;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr ||
+            (reinterpret_cast<uintptr_t>(p) & 255u) != 0)
+            return false;
+        addr[dev] = static_cast<uint8_t *>(p);
+    }
+    *ptr = addr[dev];
+    return true;
+}
+
 }  // namespace scg
 
 using namespace scg;
@@ -359,6 +384,25 @@ int sc_gemm(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const in
         return SC_ERR_WORKSPACE;
     return enqueue(*desc, lay, A, sA, B, sB, L_per_row, out, counts, reinterpret_cast<uint8_t *>(workspace),
                    reinterpret_cast<hipStream_t>(stream));
+}
+
+int sc_gemm_noalloc(const sc_gemm_desc *desc, const int8_t *A, const float *sA, const int8_t *B,
+                    const float *sB, const int32_t *L_per_row, float *out, int32_t *counts,
+                    int32_t *status_out, void *stream) {
+    Layout lay;
+    const int rc = check_call(desc, A, sA, B, sB, L_per_row, out, &lay);
+    if (rc != SC_OK) return rc;
+    if (lay.total > SC_NOALLOC_WORKSPACE_BYTES) return SC_ERR_WORKSPACE;
+    uint8_t *ws = nullptr;
+    if (!scratch_address(&ws)) return SC_ERR_HIP;
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    const int e = enqueue(*desc, lay, A, sA, B, sB, L_per_row, out, counts, ws, st);
+    if (e != SC_OK) return e;
+    // the status word (offset 0 of every workspace) of this call, for the caller
+    if (status_out != nullptr &&
+        hipMemcpyAsync(status_out, ws, sizeof(int32_t), hipMemcpyDeviceToDevice, st) != hipSuccess)
+        return SC_ERR_HIP;
+    return SC_OK;
 }
 
 int sc_gemm_status(const void *workspace, void *stream) {
