@@ -144,3 +144,30 @@ def test_cbsg_scc_is_small(oracle_mod):
                     k0 += 1
             vals.append(abs(_scc(za, zb)))
     assert np.mean(vals) < 0.05
+
+
+def test_zero_a_is_an_exact_zero_of_the_product(oracle_mod):
+    """Eq. (6): gating makes B's bits on A's 1-cycles and on its 0-cycles both follow B's own
+    sequence, so the product is bias-free at finite L (App. A.1: ad - bc = 0).  For A = 0
+    (boundary 128) and L = 2^m, the first L points of dimension 1 put exactly L/2 of A's bits
+    at 1, B's generator then runs the same prefix of L/2 draws on both branches, and the XNOR
+    count is L/2 for every B value and seed: the decode is exactly 0.  Streams from the same
+    two Sobol dimensions without gating miss this for about half of the (B, L, seed) cases,
+    so the property pins the gating itself."""
+    B = np.arange(-127, 128, dtype=np.int8).reshape(-1, 1)
+    A = np.zeros((1, 1), np.int8)
+    ungated_misses = 0
+    for seed in range(6):
+        rA = oracle_mod.sobol8(1, oracle_mod.sobol_shift(seed, 0))
+        rB = oracle_mod.sobol8(2, oracle_mod.sobol_shift(seed, 1))
+        for m in range(1, 9):
+            L = 2 ** m
+            c, o = oracle_mod.sc_gemm_cbsg(A, B, np.ones(1, np.float32), np.ones(255, np.float32),
+                                           np.array([L], np.int32), 256, 0, seed)
+            assert np.all(c == L // 2), (seed, L)
+            assert np.all(o == 0.0)
+            for q in range(-127, 128):
+                zA = rA[:L] < oracle_mod.beta_bipolar(0)
+                zB = rB[:L] < oracle_mod.beta_bipolar(q)
+                ungated_misses += int((zA == zB).sum()) != L // 2
+    assert ungated_misses > 1000
