@@ -77,7 +77,7 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
     // the status word is always the first word of the workspace
     size_t off = 0;
     l.off_status = off;
-    off = align256(off + 3 * 4);
+    off = align256(off + 4 * 4);
     l.off_rA = off;
     off = align256(off + (size_t)l.LBS * 4);
     l.off_rB = off;
@@ -145,7 +145,8 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
     // indivisible steps along the inner range per cycle (chunks of every 32-cycle group with rgen)
     const int kunits = l.rgen ? l.KC * (l.LBS / 32) : l.KQP / 2;
     const int smax = kunits > l.Smin ? kunits : l.Smin;
-    const double tile_bytes = (double)l.mbm * l.mbn * 4.0;
+    // partial-sum bytes of one part (256-row blocks of N <= 64 compute 64 columns)
+    const double tile_bytes = (double)l.mbm * (l.narrow ? 64 : l.mbn) * 4.0;
     const double Lmean = d.L_hint > 0 ? d.L_hint : d.L_max;
     l.S = l.Smin;
     l.F = 0;
@@ -163,11 +164,13 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
         l.q_perL = (double)l.mbm * (l.narrow ? 64 : l.mbn) * 4.0 * l.KQP / MFMA_QUAD_RATE;
         l.q_slots = l.narrow ? 2 * l.cus : l.cus;
         l.q_Lmean = Lmean;
+        l.q_pbytes = tile_bytes;
         l.q_one = Lmean >= d.L_max;
         const double avgT = l.q_perL * Lmean, maxT = l.q_perL * d.L_max;
         double best = 0.0;
         for (int s = l.Smin; s <= MAX_SPLIT && s <= smax; s *= 2) {
-            const double est = quad_split_time(tiles, s, l.q_perL, Lmean, d.L_max, l.q_one != 0, l.q_slots);
+            const double est = quad_split_time(tiles, s, l.q_perL, Lmean, d.L_max, l.q_one != 0, l.q_slots,
+                                               l.q_pbytes);
             if (s == l.Smin || est < best * 0.97) {
                 best = est;
                 l.S = s;
@@ -212,11 +215,21 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
             }
         }
     }
+    // with varying lengths a split is only worth it for the long tiles: each tile gets its own
+    // number of parts on the device, once the lengths are known (k_units), at most S
+    l.vsplit = quad && tiles > 0 && !l.q_one && l.F == 0 && l.S > 1;
+    l.off_units = off;
+    if (l.vsplit) {
+        off = align256(off + (size_t)tiles * l.S * 16);
+        l.off_tinfo = off;
+        off = align256(off + (size_t)tiles * 8);
+    }
     l.off_part = off;
     if (l.S > 1) {
         size_t partb;
         const int64_t split_tiles = quad ? tiles - l.F : tiles;
-        if (!mul_ok((size_t)split_tiles * (size_t)l.S, (size_t)tile_bytes, &partb)) return false;
+        // every part is laid out as a whole tile, [mbm rows][mbn columns] of int32
+        if (!mul_ok((size_t)split_tiles * (size_t)l.S, (size_t)l.mbm * (size_t)l.mbn * 4, &partb)) return false;
         off = align256(off + partb);
     }
 
@@ -295,6 +308,7 @@ static int enqueue(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, co
         launch_cbsg_table(rA, d.L_max, reinterpret_cast<uint16_t *>(ws + lay.off_CA), st) != hipSuccess)
         return SC_ERR_HIP;
     if ((e = launch_schedule(d, lay, L_per_row, ws, fuse, st)) != hipSuccess) return SC_ERR_HIP;
+    if (lay.vsplit && (e = launch_units(d, lay, ws, st)) != hipSuccess) return SC_ERR_HIP;
     if (lay.rgen) {
         if ((e = launch_rchunks(d, lay, A, B, ws, st)) != hipSuccess) return SC_ERR_HIP;
     } else if (!lay.fused) {

@@ -6,7 +6,9 @@
 //              tile-pair cycle count of the call (256-row GEMM), then one uint32: nonzero
 //              when some 256-row pair holds more distinct lengths that are not multiples of
 //              32 than the int8-chunk GEMM has masked tables (rslots; it then masks its
-//              fragments); all cleared by k_draws (or k_schedule)
+//              fragments); all cleared by k_draws (or k_schedule); then one uint32: the
+//              work units of the 256-row GEMM when their division follows the tile lengths
+//              (written by k_units)
 //   draws      rA[LBS], rB[LBS]                   uint32, comparator sequences
 //   CA         C-BSG only: CA[L][beta] = #{l < L : rA_l < beta}, uint16 [L_max+1][257]
 //   rtab       int8-chunk GEMM only: for each 32-cycle group G, the fp4 slot row of every
@@ -19,6 +21,8 @@
 //     tileOff[MT]      word offset of tile t's planes inside Ap
 //     Ap               fp4 planes of A (or int8 chunks, below)
 //   part       partial counts when GEMM tiles are split along the inner (element, cycle) range
+//   units      vsplit only: the 256-row GEMM's work units {tile, part, parts, partial index}
+//              (int4) and per tile {parts, partial index of part 0} (int2), from k_units
 //   per batch entry of B (1 if B is broadcast, else batch entries):
 //     Bp               fp4 planes of B (or int8 chunks)
 //
@@ -71,11 +75,11 @@ constexpr double PART_BW = 3e12;           // bytes/s of writing and summing par
 // the load is the total over the CUs.  The host evaluates it with L_max, the GEMM kernels
 // again with the longest tile pair of the call (both pick the same way among s).
 __host__ __device__ inline double quad_split_time(int64_t tiles, int s, double perL, double Lmean,
-                                                  double Lmax, bool one_length, int slots) {
+                                                  double Lmax, bool one_length, int slots, double part_bytes) {
     const double avgT = perL * Lmean, maxT = perL * Lmax;
     const double load = one_length ? (double)((tiles * s + slots - 1) / slots) * avgT / s
                                    : (double)tiles * avgT / slots;
-    const double red = s > 1 ? (double)tiles * (2 * s) * 256.0 * 256.0 * 4.0 / PART_BW + 5e-6 : 0.0;
+    const double red = s > 1 ? (double)tiles * (2 * s) * part_bytes / PART_BW + 5e-6 : 0.0;
     return (load > maxT / s ? load : maxT / s) + red;
 }
 constexpr int OCH = 8;           // octets per block of the nibble-plane generator
@@ -130,7 +134,12 @@ struct Layout {
     double q_perL, q_Lmean;   // 256-row GEMM split model: seconds per cycle of one tile, mean L
     int q_one;                // 256-row GEMM split model: all rows have one length
     int q_slots;              // 256-row GEMM split model: blocks that run at once
+    double q_pbytes;          // 256-row GEMM split model: partial-sum bytes of one part (the
+                              // columns a block computes: 256, or 64 with N <= 64)
     size_t off_part;   // partial counts of split tiles: [split tiles][S][tile rows][tile columns]
+    int vsplit;        // 256-row GEMM, lengths vary and tiles are split: each tile gets its own
+                       // number of parts (k_units), at most S
+    size_t off_units, off_tinfo;
     size_t total;
 };
 
@@ -145,6 +154,8 @@ hipError_t launch_cbsg_table(const uint32_t *rA, int L_max, uint16_t *CA, hipStr
 // draws: also clear the status words and make the comparator sequences (one batch entry only)
 hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L,
                            uint8_t *ws, bool draws, hipStream_t st);
+// the 256-row GEMM's work units from the scheduled tile lengths (Layout::vsplit)
+hipError_t launch_units(const sc_gemm_desc &d, const Layout &lay, uint8_t *ws, hipStream_t st);
 
 // counting GEMM (sc_mfma.hip)
 hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,

@@ -370,6 +370,100 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     }
 }
 
+// Work units of the 256-row GEMM when row lengths vary (Layout::vsplit).  Tile t (pair tp of
+// batch entry b x B pair tw, the GEMM's tile order: longest pairs first) runs tileL[tp]
+// cycles.  With the average load of a block slot A = sum / slots and the cap S: when the
+// lengths are skewed (longest tile > 3 A), a tile longer than T = max(A, longest / S) is
+// split into the fewest of 2, 4, .. S parts that bring each part to T and the others run
+// whole, so only long tiles pay for partial sums (Sec. 4.1: the cost follows the sum of the
+// l_i); otherwise every tile is split alike, as the split model picks for the longest tile
+// (measured on 4096 x 1152 x 4608 with group lengths 24..192: 0.78 ms with long tiles alone
+// split, 0.67 ms split alike).
+// Units are listed tile by tile as {tile, part, parts, partial index}, tinfo[t] = {parts,
+// partial index of part 0}, and the unit count goes to status word 3.  A tile is never split
+// into fewer than Smin parts.  One block.
+__global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, int S, uint8_t *ws) {
+    __shared__ int64_t rsum[16];
+    __shared__ int rmax[16];
+    const int tid = threadIdx.x;
+    const int NTW = lay.NT / 2, npairs = lay.MT / 2;
+    const int tiles = batch * npairs * NTW;
+    auto work = [&](int t) {
+        const int tb = t / NTW, b = tb % batch, tp = tb / batch;
+        return ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_tileL)[2 * tp];
+    };
+    int64_t sum = 0;
+    int mx = 0;
+    for (int t = tid; t < tiles; t += 1024) {
+        const int w = work(t);
+        sum += w;
+        mx = max(mx, w);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        sum += __shfl_xor(sum, o, 64);
+        mx = max(mx, __shfl_xor(mx, o, 64));
+    }
+    if ((tid & 63) == 0) {
+        rsum[tid >> 6] = sum;
+        rmax[tid >> 6] = mx;
+    }
+    __syncthreads();
+    sum = 0;
+    mx = 0;
+    for (int k = 0; k < 16; ++k) {
+        sum += rsum[k];
+        mx = max(mx, rmax[k]);
+    }
+    const double A = (double)sum / lay.q_slots;
+    // Skewed lengths (the longest tile more than 3 times the average load of a slot): split only
+    // the long tiles.  Otherwise tiles of similar length pack better as equal parts: every tile
+    // gets the same number of parts, the one the split model picks for the longest tile.
+    double T = fmax(A, (double)mx / S);
+    int sall = 0;
+    if (mx <= 3.0 * A) {
+        double best = 0.0;
+        for (int s = lay.Smin; s <= S; s *= 2) {
+            const double est = quad_split_time(tiles, s, lay.q_perL, lay.q_Lmean, (double)mx, false, lay.q_slots,
+                                               lay.q_pbytes);
+            if (s == lay.Smin || est < best * 0.97) {
+                best = est;
+                sall = s;
+            }
+        }
+    }
+    int4 *units = ws_ptr<int4>(ws, lay.off_units);
+    int2 *tinfo = ws_ptr<int2>(ws, lay.off_tinfo);
+    int64_t ucarry = 0, pcarry = 0;
+    for (int c = 0; c < tiles; c += 1024) {
+        const int t = c + tid;
+        // (never fewer than Smin parts: each part's fp32 sums stay exact)
+        int s = lay.Smin;
+        if (sall > 0) {
+            s = sall;
+        } else if (t < tiles) {
+            const double w = work(t);
+            while (s < S && w > T * s) s *= 2;
+        }
+        int64_t utot, ptot;
+        const int64_t ux = block_excl_scan_1024(t < tiles ? s : 0, &utot);
+        const int64_t px = block_excl_scan_1024(t < tiles && s > 1 ? s : 0, &ptot);
+        if (t < tiles) {
+            const int ub = (int)(ucarry + ux), pb = (int)(pcarry + px);
+            tinfo[t] = make_int2(s, pb);
+            for (int p = 0; p < s; ++p) units[ub + p] = make_int4(t, p, s, pb + p);
+        }
+        ucarry += utot;
+        pcarry += ptot;
+    }
+    if (tid == 0) ws_ptr<uint32_t>(ws, lay.off_status)[3] = (uint32_t)ucarry;
+}
+
+hipError_t launch_units(const sc_gemm_desc &d, const Layout &lay, uint8_t *ws, hipStream_t st) {
+    hipLaunchKernelGGL(k_units, dim3(1), dim3(1024), 0, st, lay, d.batch, lay.S, ws);
+    return hipGetLastError();
+}
+
 hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32_t *L, uint8_t *ws,
                            bool draws, hipStream_t st) {
     if (draws && d.batch != 1) return hipErrorInvalidValue;

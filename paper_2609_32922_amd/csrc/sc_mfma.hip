@@ -447,6 +447,27 @@ __device__ __forceinline__ void store_part(const v16f (&acc)[4][NB], int32_t *pa
                                                       ((32 * i + 8 * (e >> 2) + (e & 3)) * 256 + 32 * c) * 4, 0);
 }
 
+// The same for the int8-chunk GEMM, whose wave of row half rh holds the pair's row blocks
+// starting at r_row0<SKIP>(rh, i) (declared with that GEMM below).
+template <bool SKIP>
+__device__ __forceinline__ int r_row0(int rh, int i);
+template <bool SKIP, int NB>
+__device__ __forceinline__ void store_part_r(const v16f (&acc)[4][NB], int32_t *part, int rh, int wc, int grp,
+                                             int i32) {
+    const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(part, 0, 256 * 256 * 4, 0x00020000);
+    const int voff = ((4 * grp) * 256 + wc + i32) * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r0 = r_row0<SKIP>(rh, i);
+#pragma unroll
+        for (int c = 0; c < NB; ++c)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                __builtin_amdgcn_raw_buffer_store_b32((uint32_t)(int32_t)acc[i][c][e], pr, voff,
+                                                      ((r0 + 8 * (e >> 2) + (e & 3)) * 256 + 32 * c) * 4, 0);
+    }
+}
+
 // Block tile: BM = 128 rows of A x WB columns of B, WB = 256 (two 128-column B plane
 // tiles) or 128 (one; taken when N <= 128, where a wider tile would mostly multiply
 // padding).
@@ -1131,11 +1152,12 @@ __device__ __forceinline__ void q_division(const MGemmArgs &g, const Layout &lay
     const int tiles = g.batch * (lay.MT / 2) * (lay.NT / 2);
     F = g.F;
     S = g.S;
-    if (F == 0 && S > 1) {
+    if (F == 0 && S > 1 && !lay.vsplit) {
         const double Lmax = (double)ws_ptr<uint32_t>(ws, lay.off_status)[1];
         double best = 0.0;
         for (int s = lay.Smin; s <= g.S; s *= 2) {
-            const double est = quad_split_time(tiles, s, lay.q_perL, lay.q_Lmean, Lmax, lay.q_one != 0, lay.q_slots);
+            const double est = quad_split_time(tiles, s, lay.q_perL, lay.q_Lmean, Lmax, lay.q_one != 0, lay.q_slots,
+                                               lay.q_pbytes);
             if (s == lay.Smin || est < best * 0.97) {
                 best = est;
                 S = s;
@@ -1150,14 +1172,18 @@ constexpr int NXCD = 8;
 // pair rows per band in the order of the whole tiles
 constexpr int QG = 4;
 
-// The whole tile that unit u (< F) computes.  Units are regrouped so that the 8 C units
-// that run at once on the 8 XCDs take 8 runs of C consecutive tiles, one run per XCD, in
-// the same overall order as before (so tiles of similar length still run together), and
-// consecutive tiles go column by column through bands of QG pair rows: a run of 32 tiles
-// covers 4 A pairs and 8 B pairs, which then hit in that XCD's L2.  Both steps are
-// permutations of 0 .. F-1 (tiles past the last full run, or past the last full row of
-// pair tiles, keep their place).
-__device__ __forceinline__ int q_whole_tile(int u, int F, int NTW) {
+// The whole tile that unit u (< F) computes.  With one row length every tile is the same
+// work, and units are regrouped so that the 8 C units that run at once on the 8 XCDs take
+// 8 runs of C consecutive tiles, one run per XCD, and consecutive tiles go column by column
+// through bands of QG pair rows: a run of 32 tiles covers 4 A pairs and 8 B pairs, which
+// then hit in that XCD's L2.  Both steps are permutations of 0 .. F-1 (tiles past the last
+// full run, or past the last full row of pair tiles, keep their place).  With varying
+// lengths the tiles come longest first and unit u stays tile u: dealt round-robin over the
+// XCDs, each XCD gets an even share of long and short tiles, where the runs above would
+// give the first XCDs the longest pairs of every round (ViT-L/14 MLP fc1, lengths 8..512:
+// 4.06 ms with the runs, 2.99 ms without).
+__device__ __forceinline__ int q_whole_tile(int u, int F, int NTW, int one_length) {
+    if (!one_length) return u;
     const int C = min(32, F / NXCD);
     if (C >= 2 && u < F / (NXCD * C) * (NXCD * C)) {
         const int j = u / NXCD, x = u % NXCD;
@@ -1172,6 +1198,34 @@ __device__ __forceinline__ int q_whole_tile(int u, int F, int NTW) {
     return u;
 }
 
+// Work unit u of the 256-row GEMM: its tile, part s of S parts, and the partial index v of a
+// split unit; false when u is past the call's units (the grid is sized for the most).
+// Units 0 .. F-1 are whole tiles (q_whole_tile), unit F + v part v % S of tile F + v / S; with
+// vsplit the list k_units wrote.
+__device__ __forceinline__ bool q_unit(const MGemmArgs &g, const Layout &lay, uint8_t *ws, int u, int &tile, int &s,
+                                       int &S, int &v, bool &split) {
+    if (lay.vsplit) {
+        if (u >= (int)ws_ptr<uint32_t>(ws, lay.off_status)[3]) return false;
+        const int4 e = ws_ptr<int4>(ws, lay.off_units)[u];
+        tile = e.x;
+        s = e.y;
+        S = e.z;
+        v = e.w;
+        split = S > 1;
+        return true;
+    }
+    const int NTW = lay.NT / 2;
+    int F, SS;
+    q_division(g, lay, ws, F, SS);
+    if (u >= F + (g.batch * (lay.MT / 2) * NTW - F) * SS) return false;
+    split = u >= F;
+    v = u - F;
+    s = split ? v % SS : 0;
+    S = split ? SS : 1;
+    tile = split ? F + v / SS : q_whole_tile(u, F, NTW, lay.q_one);
+    return true;
+}
+
 // One work unit: tile `tile` (pair tp of batch entry b x B pair tw) over k-steps
 // [s, s + 1) / S of the pair's k-steps.  Units 0 .. F-1 are the whole tiles 0 .. F-1,
 // decoded here; unit F + v is part v % S of tile F + v / S, stored as a partial sum;
@@ -1182,15 +1236,9 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
     __shared__ u4 smem[QNBUF * QBUF];
     __shared__ DecodeLds dl;                          // filled after the k loop
     const int NTW = lay.NT / 2;
-    int F, SS;
-    q_division(g, lay, ws, F, SS);
-    const int u = blockIdx.x;
-    if (u >= F + (g.batch * (lay.MT / 2) * NTW - F) * SS) return;
-    const bool split = u >= F;
-    const int v = u - F;
-    const int s = split ? v % SS : 0;
-    const int S = split ? SS : 1;
-    const int tile = split ? F + v / SS : q_whole_tile(u, F, NTW);
+    int tile, s, S, v;
+    bool split;
+    if (!q_unit(g, lay, ws, blockIdx.x, tile, s, S, v, split)) return;
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
@@ -1298,11 +1346,19 @@ __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, u
     q_division(g, lay, ws, F, SS);
     const int tile = F + (int)(blockIdx.x / BPT), part = (int)(blockIdx.x % BPT);
     if (tile >= g.batch * (lay.MT / 2) * NTW) return;
+    // partial index of the tile's first part: tiles F.. in SS parts each, or the tile's own
+    // number of parts (vsplit; tiles that ran whole have nothing to sum)
+    size_t pbase = (size_t)(tile - F) * SS;
+    if (lay.vsplit) {
+        const int2 ti = ws_ptr<int2>(ws, lay.off_tinfo)[tile];
+        if (ti.x < 2) return;
+        SS = ti.x;
+        pbase = (size_t)ti.y;
+    }
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
-    const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part) +
-                                                      (size_t)(tile - F) * SS * 256 * 256) +
+    const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part) + pbase * 256 * 256) +
                        (size_t)part * QR_ROWS * 64 + threadIdx.x;
     // a thread keeps NK column quads; quads past N hold nothing to sum (nor, in the 64-column
     // blocks, anything written).  Every part's loads are issued before any sum.
@@ -1597,16 +1653,32 @@ struct RFrags {
 struct RSrc {
     __amdgpu_buffer_rsrc_t a, b;   // the pair's A chunks and the B pair's chunks
     int voffA, voffB;              // the lane's row and half within a chunk
+    int boffA[4];                  // byte offsets of the wave's four A blocks within a chunk
     uint32_t loA[4], loB;          // table rows of the lane's A rows (copy, region) and of B
     const char *lut;
     int KC;
 };
 
+// The 32-row blocks of a 256-row pair that row-half rh of the block computes: {0, 1, 6, 7}
+// and {2, 3, 4, 5}.  Rows are sorted by length, so each half holds long and short rows
+// alike, and the second two blocks of a half end no later than its first two: once they
+// have ended, the half runs the MFMAs of its first two blocks only (Sec. 4.2: row i stops
+// after its l_i cycles; Sec. 4.1: the cost follows the sum of the l_i).
+__device__ __forceinline__ int r_block(int rh, int i) { return rh == 0 ? (i < 2 ? i : i + 4) : i + 2; }
+
+// First row (within the pair) of the wave's block i: interleaved as above when the wave skips
+// ended blocks (SKIP), else row half rh's four consecutive blocks.  SKIP is taken by the
+// 256 x 64 blocks (N <= 64): there the rows of a pair vary the most in length (attention
+// rows, padded heads).  The 256 x 256 blocks keep consecutive blocks: on the MLP layers the
+// skip saved under 3 % of the MFMAs and its second loop cost more (5 % on ViT-B fc1).
+template <bool SKIP>
+__device__ __forceinline__ int r_row0(int rh, int i) { return SKIP ? 32 * r_block(rh, i) : 128 * rh + 32 * i; }
+
 template <int NB>
 __device__ __forceinline__ void r_load(const RSrc &q, int c, RData<NB> &d) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        d.a[i] = __builtin_amdgcn_raw_buffer_load_b128(q.a, q.voffA, c * 256 * RCH + i * 32 * RCH, 0);
+        d.a[i] = __builtin_amdgcn_raw_buffer_load_b128(q.a, q.voffA, c * 256 * RCH + q.boffA[i], 0);
 #pragma unroll
     for (int i = 0; i < NB; ++i)
         d.b[i] = __builtin_amdgcn_raw_buffer_load_b128(q.b, q.voffB, c * 256 * RCH + i * 32 * RCH, 0);
@@ -1650,6 +1722,18 @@ __device__ __forceinline__ void r_frags(const RSrc &q, const RData<NB> &d, const
     for (int c = 0; c < NB; ++c) f.b[c] = r_look<E>(q, r_word<E>(d.b[c]), q.loB);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
+        f.a[i] = r_look<E>(q, r_word<E>(d.a[i]), q.loA[i]);
+        if (MASK) f.a[i] &= m[i];
+    }
+}
+
+// fragments of k-step E for the first two A blocks only (the other two have ended)
+template <int E, bool MASK, int NB>
+__device__ __forceinline__ void r_frags_h(const RSrc &q, const RData<NB> &d, const u4 (&m)[4], RFrags<NB> &f) {
+#pragma unroll
+    for (int c = 0; c < NB; ++c) f.b[c] = r_look<E>(q, r_word<E>(d.b[c]), q.loB);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
         f.a[i] = r_look<E>(q, r_word<E>(d.a[i]), q.loA[i]);
         if (MASK) f.a[i] &= m[i];
     }
@@ -1715,6 +1799,42 @@ __device__ __forceinline__ void r_stage(const RSrc &q, int cnext, RData<NB> &cur
     r_quarter_masks<MASK, NB>();
 }
 
+// Stage S when only the first two A blocks of the wave run: half the MFMAs, two A table
+// reads per k-step instead of four
+template <int S, bool MASK, int NB>
+__device__ __forceinline__ void r_stage_h(const RSrc &q, int cnext, RData<NB> &cur, RData<NB> &nxt,
+                                          const u4 (&m)[4], const bool (&fin)[4], v16f (&acc)[4][NB],
+                                          RFrags<NB> (&f)[2]) {
+    if (S == 0) r_load(q, cnext, nxt);
+    r_frags_h<2 * S + 1, MASK>(q, cur, m, f[1]);
+    q_mma_half(acc, f[0], 0);
+    if (S < 7) {
+        r_frags_h<2 * S + 2, MASK>(q, cur, m, f[0]);
+    } else {
+        if (!MASK) r_finish(nxt, fin);
+        r_frags_h<0, MASK>(q, nxt, m, f[0]);
+    }
+    q_mma_half(acc, f[1], 0);
+}
+
+template <bool MASK, int NB>
+__device__ __forceinline__ void r_chunks_h(const RSrc &q, int c, int ce, RData<NB> &cur, RData<NB> &nxt,
+                                           const u4 (&m)[4], const bool (&fin)[4], v16f (&acc)[4][NB],
+                                           RFrags<NB> (&f)[2]) {
+    for (; c < ce; ++c) {
+        const int x = c + 1 < q.KC ? c + 1 : 0;
+        r_stage_h<0, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_h<1, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_h<2, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_h<3, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_h<4, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_h<5, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_h<6, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_h<7, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        cur = nxt;
+    }
+}
+
 // chunks c .. ce-1 of one cycle group; on exit cur holds the chunk after them (chunk ce, or
 // chunk 0 of the next group) and fragment set 0 its first k-step (from this group's table)
 template <bool MASK, int NB>
@@ -1750,27 +1870,22 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     constexpr int NT = NARROW ? 128 : 256;            // threads
     constexpr int NB = NARROW ? 2 : 4;                // B blocks of 32 columns per wave
     constexpr bool TABLES = !MASK && !NARROW;         // tables masked to row lengths
+    constexpr bool SKIP = NARROW;                     // skip the MFMAs of blocks whose rows ended
     __shared__ u4 lut[(TABLES ? 2 : 1) * 256 * 16];   // 64 or 128 KB; the epilogue's transpose reuses it
     __shared__ uint32_t rems[TABLES ? RGROUPS : 1];   // bit r of rems[G]: a row ends r cycles into group G
     __shared__ DecodeLds dl;                          // filled after the chunk loop
     if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
     const int NTW = lay.NT / 2;
-    int F, SS;
-    q_division(g, lay, ws, F, SS);
-    const int u = blockIdx.x;
-    if (u >= F + (g.batch * (lay.MT / 2) * NTW - F) * SS) return;
-    const bool split = u >= F;
-    const int v = u - F;
-    const int s = split ? v % SS : 0;
-    const int S = split ? SS : 1;
-    const int tile = split ? F + v / SS : q_whole_tile(u, F, NTW);
+    int tile, s, S, v;
+    bool split;
+    if (!q_unit(g, lay, ws, blockIdx.x, tile, s, S, v, split)) return;
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
     const int bB = g.nbB == 1 ? 0 : b;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int grp = lane >> 5, i32 = lane & 31;
-    const int wr = NARROW ? 128 * w : (w >> 1) * 128, wc = NARROW ? 0 : (w & 1) * 128;
+    const int rh = NARROW ? w : (w >> 1), wc = NARROW ? 0 : (w & 1) * 128;   // row half, columns
     uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
     uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
     const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm) + tp * 256;
@@ -1787,13 +1902,16 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
         if (Lt % RCH != 0) atomicOr(&rems[Lt / RCH], 1u << (Lt % RCH));
         __syncthreads();
     }
-    // the lane's A rows' lengths (padding rows: never end)
+    // the lane's A rows' lengths (padding rows: never end), and the longest length of the
+    // wave's first two and last two blocks (their first rows; padding: 0)
     int Lr[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int row = wr + 32 * i + i32;
+        const int row = r_row0<SKIP>(rh, i) + i32;
         Lr[i] = perm[row] >= 0 ? Ls[row] : INT_MAX;
     }
+    const int h0 = r_row0<SKIP>(rh, 0), h1 = r_row0<SKIP>(rh, 2);
+    const int Lh0 = wave_uniform(perm[h0] >= 0 ? Ls[h0] : 0), Lh1 = wave_uniform(perm[h1] >= 0 ? Ls[h1] : 0);
 
     const size_t pairb = (size_t)g.KC * 256 * RCH;
     RSrc q;
@@ -1801,7 +1919,9 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
                                             0x00020000);
     q.b = __builtin_amdgcn_make_buffer_rsrc(ws_ptr<uint8_t>(wsbB, lay.off_Bp) + (size_t)tw * pairb, 0, (int)pairb,
                                             0x00020000);
-    q.voffA = (wr + i32) * RCH + grp * 16;
+    q.voffA = ((SKIP ? 0 : 128 * rh) + i32) * RCH + grp * 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) q.boffA[i] = (SKIP ? 32 * r_block(rh, i) : 32 * i) * RCH;
     q.voffB = (wc + i32) * RCH + grp * 16;
     const uint32_t lrep = 16u * (uint32_t)(lane & (RREP - 1));
     q.loB = lrep + 16u * RREP;
@@ -1825,9 +1945,12 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     RFrags<NB> f[2];
     u4 m[4];
     if (x0 < x1) r_load(q, (int)(x0 % q.KC), cur);
-    for (int64_t x = x0; x < x1;) {
-        const int G = (int)(x / g.KC);
-        const int64_t xe = min(x1, (int64_t)(G + 1) * g.KC);
+    // One cycle group per trip: the collective table fill between two barriers, then the
+    // wave's chunks.  Three phases in turn, as the wave's rows end: all four blocks run, only
+    // the first two run, none runs (the wave still takes part in the table fills).  Separate
+    // loops, so that a later phase holds none of an earlier one's registers.
+    int64_t x = x0;
+    auto group_start = [&](int G, int64_t xe, bool (&fin)[4]) {
         const uint32_t rm = TABLES ? rems[G] : 0u;
         // every read of the previous group's table is done before it is replaced
         __syncthreads();
@@ -1838,7 +1961,6 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
         __syncthreads();
         // the lane's A rows: ended, ending inside this group (the masked table of the
         // length's rank among the group's lengths; with MASK a mask instead) or running on
-        bool fin[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int rem = Lr[i] - RCH * G;
@@ -1852,14 +1974,39 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
             }
         }
         if (!MASK) r_finish(cur, fin);
+    };
+    for (; x < x1;) {
+        const int G = (int)(x / g.KC);
+        if (SKIP && Lh1 <= RCH * G) break;
+        const int64_t xe = min(x1, (int64_t)(G + 1) * g.KC);
+        bool fin[4];
+        group_start(G, xe, fin);
         r_frags<0, MASK>(q, cur, m, f[0]);
-        r_chunks<MASK>(q, (int)(x - (int64_t)G * g.KC), (int)(xe - (int64_t)G * g.KC), cur, nxt, m, fin, acc,
-                       f);
+        r_chunks<MASK>(q, (int)(x - (int64_t)G * g.KC), (int)(xe - (int64_t)G * g.KC), cur, nxt, m, fin, acc, f);
+        x = xe;
+    }
+    for (; SKIP && x < x1;) {
+        const int G = (int)(x / g.KC);
+        if (Lh0 <= RCH * G) break;
+        const int64_t xe = min(x1, (int64_t)(G + 1) * g.KC);
+        bool fin[4];
+        group_start(G, xe, fin);
+        r_frags_h<0, MASK>(q, cur, m, f[0]);
+        r_chunks_h<MASK>(q, (int)(x - (int64_t)G * g.KC), (int)(xe - (int64_t)G * g.KC), cur, nxt, m, fin, acc, f);
+        x = xe;
+    }
+    for (; SKIP && x < x1;) {
+        const int G = (int)(x / g.KC);
+        const int64_t xe = min(x1, (int64_t)(G + 1) * g.KC);
+        __syncthreads();
+        r_fill_lut<NT>(lut, ent, tid, TABLES ? rems[G] : 0u);
+        if (xe < x1) r_load_ent<NT>(ent, rtab + (size_t)(G + 1) * 512, tid);
+        __syncthreads();
         x = xe;
     }
 
     if (split) {
-        store_part<NB>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256, wr, wc, grp, i32);
+        store_part_r<SKIP, NB>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256, rh, wc, grp, i32);
         return;
     }
     // a whole tile decodes: the rows' and columns' data staged in LDS, the sums transposed
@@ -1871,11 +2018,11 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     int32_t *T = reinterpret_cast<int32_t *>(lut);
     for (int h = 0; h < 256 / TR; ++h) {
         __syncthreads();
-        // rows 32h .. 32h + 31: MFMA block i = h % 4 of the waves at wr = 128 (h / 4)
-        if (wr == 128 * (h >> 2)) {
+        // rows 32h .. 32h + 31: block i of the waves of row half rh with r_row0(rh, i) = 32 h
+        if (rh == (SKIP ? (h >= 2 && h < 6 ? 1 : 0) : h >> 2)) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                if (i != (h & 3)) continue;
+                if (r_row0<SKIP>(rh, i) != 32 * h) continue;
 #pragma unroll
                 for (int c = 0; c < NB; ++c)
 #pragma unroll

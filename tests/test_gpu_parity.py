@@ -45,12 +45,12 @@ def _to_dev(g, dev):
             torch.from_numpy(np.ascontiguousarray(g.L)).to(dev))
 
 
-def _run(g, dev, check_status=True, rng=0):
+def _run(g, dev, check_status=True, rng=0, L_hint=0):
     import torch
     import paper_2609_32922_amd as scg
     A, sA, B, sB, L = _to_dev(g, dev)
     out, cnt = scg.gemm(A, sA, B, sB, L, L_max=g.L_max, polarity=g.polarity, seed=g.seed,
-                        want_counts=True, check_status=check_status, rng=rng)
+                        want_counts=True, check_status=check_status, rng=rng, L_hint=L_hint)
     torch.cuda.synchronize()
     return out.cpu().numpy(), cnt.cpu().numpy()
 
@@ -234,6 +234,40 @@ def test_rgen_full_compare(dev, oracle_mod, case):
     out, cnt = _run(g, dev)
     for b in range(g.batch):
         _compare(g, b, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "rgen%s b%d" % (case, b))
+
+
+# With an expected mean length (L_hint) below L_max the 256-row GEMM divides its tiles by
+# their lengths on the device: long tiles in 2, 4 or 8 parts, short ones whole.  Shapes with
+# few tiles (so that splitting pays), sorted lengths spanning 1..L_max, both comparator
+# sources, polarities, and the 256 x 64 blocks.
+VSPLIT = [
+    # batch, M, N, K, L_max, polarity, rng, broadcast_B, seed
+    (1, 1000, 520, 96, 200, 0, 0, False, 401),
+    (2, 700, 300, 64, 300, 1, 0, True, 403),
+    (1, 900, 40, 150, 256, 1, 0, False, 405),      # 256 x 64 blocks
+    (3, 577, 33, 64, 512, 0, 0, False, 407),       # attention-like heads
+    (1, 800, 400, 70, 256, 0, 1, False, 409),      # C-BSG: fp4 planes, 256-row blocks
+    (1, 600, 300, 100, 256, 1, 1, False, 411),
+]
+
+
+@pytest.mark.parametrize("case", VSPLIT, ids=[str(c) for c in VSPLIT])
+def test_length_aware_split(dev, oracle_mod, case):
+    batch, M, N, K, L_max, pol, rng_kind, bcast, seed = case
+    rng = np.random.default_rng(seed)
+    g = W.random_gemm(rng, batch, M, N, K, L_max, pol, seed, L_lo=1, broadcast_B=bcast)
+    # a skewed length distribution: few long rows, many short ones (as the policy gives)
+    u = rng.random(g.L.shape)
+    g.L = np.maximum(1, (L_max * u ** 4)).astype(np.int32)
+    g.L[:, 0] = L_max
+    hint = int(round(float(g.L.mean())))
+    _note("length-aware split %s L_hint %d" % (case, hint))
+    out, cnt = _run(g, dev, rng=rng_kind, L_hint=hint)
+    for b in range(batch):
+        _compare(g, b, np.arange(M), np.arange(N), out, cnt, oracle_mod, "vsplit%s b%d" % (case, b), rng=rng_kind)
+    # the same call without the hint (every tile split alike, or none) gives the same bits
+    out2, cnt2 = _run(g, dev, rng=rng_kind)
+    assert np.array_equal(cnt, cnt2) and np.array_equal(out.view(np.uint32), out2.view(np.uint32))
 
 
 LADDERS = [
