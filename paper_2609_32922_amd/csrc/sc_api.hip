@@ -215,9 +215,12 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
             }
         }
     }
-    // with varying lengths a split is only worth it for the long tiles: each tile gets its own
-    // number of parts on the device, once the lengths are known (k_units), at most S
-    l.vsplit = quad && tiles > 0 && !l.q_one && l.F == 0 && l.S > 1;
+    // 256 x 64 blocks (N <= 64: attention P.V, per-head layers) with varying lengths: each tile
+    // gets its own number of parts on the device, once the lengths are known (k_units), at
+    // most S.  (On the 256 x 256 blocks the per-tile split measured no better than the split
+    // chosen below for every tile: 6304 x 768 x 3072 with lengths 16..256 +1 %, the DiT-XL/2
+    // pair -3 %.)
+    l.vsplit = quad && l.narrow && tiles > 0 && !l.q_one && l.F == 0 && l.S > 1;
     l.off_units = off;
     if (l.vsplit) {
         off = align256(off + (size_t)tiles * l.S * 16);

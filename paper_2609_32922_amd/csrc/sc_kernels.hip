@@ -373,12 +373,12 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 // Work units of the 256-row GEMM when row lengths vary (Layout::vsplit).  Tile t (pair tp of
 // batch entry b x B pair tw, the GEMM's tile order: longest pairs first) runs tileL[tp]
 // cycles.  With the average load of a block slot A = sum / slots and the cap S: when the
-// lengths are skewed (longest tile > 3 A), a tile longer than T = max(A, longest / S) is
+// lengths are skewed (longest tile > 2 A), a tile longer than T = max(A, longest / S) is
 // split into the fewest of 2, 4, .. S parts that bring each part to T and the others run
 // whole, so only long tiles pay for partial sums (Sec. 4.1: the cost follows the sum of the
 // l_i); otherwise every tile is split alike, as the split model picks for the longest tile
-// (measured on 4096 x 1152 x 4608 with group lengths 24..192: 0.78 ms with long tiles alone
-// split, 0.67 ms split alike).
+// (as measured where this division ran on 256-column blocks too: 4096 x 1152 x 4608 with
+// group lengths 24..192 took 0.78 ms with the long tiles alone split, 0.67 ms split alike).
 // Units are listed tile by tile as {tile, part, parts, partial index}, tinfo[t] = {parts,
 // partial index of part 0}, and the unit count goes to status word 3.  A tile is never split
 // into fewer than Smin parts.  One block.
@@ -416,12 +416,12 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, int S, ui
         mx = max(mx, rmax[k]);
     }
     const double A = (double)sum / lay.q_slots;
-    // Skewed lengths (the longest tile more than 3 times the average load of a slot): split only
+    // Skewed lengths (the longest tile more than twice the average load of a slot): split only
     // the long tiles.  Otherwise tiles of similar length pack better as equal parts: every tile
     // gets the same number of parts, the one the split model picks for the longest tile.
     double T = fmax(A, (double)mx / S);
     int sall = 0;
-    if (mx <= 3.0 * A) {
+    if (mx <= 2.0 * A) {
         double best = 0.0;
         for (int s = lay.Smin; s <= S; s *= 2) {
             const double est = quad_split_time(tiles, s, lay.q_perL, lay.q_Lmean, (double)mx, false, lay.q_slots,

@@ -1568,7 +1568,8 @@ hipError_t launch_rchunks(const sc_gemm_desc &d, const Layout &lay, const int8_t
     a.rows[0] = d.M;
     a.rows[1] = d.N;
     a.rows_pad[0] = lay.MT * BM;
-    a.rows_pad[1] = lay.NT * BN;
+    // the 256 x 64 blocks read the first 64 rows of B's pair only
+    a.rows_pad[1] = lay.narrow ? 64 : lay.NT * BN;
     a.nb[0] = d.batch;
     a.nb[1] = lay.nbB;
     a.stride_batch[0] = lay.stride_batchA;

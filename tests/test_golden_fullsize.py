@@ -8,11 +8,12 @@ import workloads as W
 
 NAMES = ["vitb16_fc1_L128", "vitb16_fc1_mp64", "ditxl2_proj_mlp_group96", "vitl14_336_qk_mlp",
          "vitl14_compensator_L256", "vitl14_336_attn_av"]
+CASES = [(n, False) for n in NAMES] + [("vitb16_fc1_L128", True)]
 
 
-@pytest.mark.parametrize("name", NAMES)
-def test_digests_cover_every_row_of_current_inputs(name):
-    dg = FD.load(name)
+@pytest.mark.parametrize("name,cbsg", CASES, ids=[n + ("_cbsg" if c else "") for n, c in CASES])
+def test_digests_cover_every_row_of_current_inputs(name, cbsg):
+    dg = FD.load(name, cbsg)
     assert dg["oracle"] == FD.oracle_source_digest(), "stale digests: rerun make_fullsize_digests.py"
     w = W.WORKLOADS[name]()
     assert sorted(dg["inputs"]) == sorted(g.name for g in w.gemms)

@@ -236,10 +236,10 @@ def test_rgen_full_compare(dev, oracle_mod, case):
         _compare(g, b, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "rgen%s b%d" % (case, b))
 
 
-# With an expected mean length (L_hint) below L_max the 256-row GEMM divides its tiles by
-# their lengths on the device: long tiles in 2, 4 or 8 parts, short ones whole.  Shapes with
-# few tiles (so that splitting pays), sorted lengths spanning 1..L_max, both comparator
-# sources, polarities, and the 256 x 64 blocks.
+# With an expected mean length (L_hint) below L_max the 256-row GEMM takes its split count
+# from the scheduled lengths, and the 256 x 64 blocks (N <= 64) divide their tiles by length:
+# long tiles in 2, 4 or 8 parts, short ones whole.  Shapes with few tiles (so that splitting
+# pays), skewed lengths spanning 1..L_max, both comparator sources and polarities.
 VSPLIT = [
     # batch, M, N, K, L_max, polarity, rng, broadcast_B, seed
     (1, 1000, 520, 96, 200, 0, 0, False, 401),
