@@ -345,37 +345,44 @@ struct MGemmArgs {
     int64_t strideSA, strideSB, strideO, ldo;
     float *out;
     int32_t *counts;
+    int vec_out, vec_cnt;   // four adjacent columns of out (counts) at a multiple of 4 are 16-byte aligned
 };
 
-// decode and store four adjacent columns j0.. (ncol of them in range) of original row i of
-// batch entry b from the fp4 product sums: Li its length, scale = sA_i * 127^2, sBj the
-// columns' scales
-template <bool BIP>
-__device__ __forceinline__ void mdecode4_store(const int32_t (&P)[4], int i, int Li, float scale,
-                                               const float (&sBj)[4], int j0, int ncol, int b,
-                                               const MGemmArgs &g) {
-    const int KL = g.K * Li;
+// Eq. (1) decode in fp32, one formula for every kernel: row i of scale sA_i and length L
+// gets the factor f_i = (sA_i 127^2) / L (0 when L = 0), and the output is (P f_i) sB_j,
+// P the row's product sum (bipolar: 2X - K L; unipolar: the signed AND count S), an exact
+// integer held in fp32.
+__device__ __forceinline__ float decode_factor(float sAi, int L) {
+    return L > 0 ? (sAi * 16129.0f) / (float)L : 0.0f;
+}
+
+// Store four adjacent columns j0.. (ncol of them in range) of original row i of batch entry
+// b from their product sums: P as fp32 for the output; for the counts (bipolar: X = (K L +
+// P) / 2) the exact int32 sums Pi when PINT, else P itself (an exact integer below 2^24).
+template <bool BIP, bool PINT>
+__device__ __forceinline__ void decode4_store(const float (&P)[4], const int32_t (&Pi)[4], int i, int Li, float f,
+                                              const float (&sBj)[4], int j0, int ncol, int b, const MGemmArgs &g) {
     float o[4];
-    int32_t cnt[4];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        // bipolar: P = 2X - K L; unipolar: P = S
-        cnt[c] = BIP ? (KL + P[c]) / 2 : P[c];
-        o[c] = Li > 0 ? (float)P[c] / (float)Li * (scale * sBj[c]) : 0.0f;
-        if (Li == 0) cnt[c] = 0;
-    }
-    float *op = g.out + (size_t)b * g.strideO + (size_t)i * g.ldo + j0;
-    if (ncol == 4 && (reinterpret_cast<uintptr_t>(op) & 15) == 0) {
-        *reinterpret_cast<float4 *>(op) = make_float4(o[0], o[1], o[2], o[3]);
+    for (int c = 0; c < 4; ++c) o[c] = (P[c] * f) * sBj[c];
+    const size_t off = (size_t)b * g.strideO + (size_t)i * g.ldo + j0;
+    if (ncol == 4 && g.vec_out) {
+        *reinterpret_cast<float4 *>(g.out + off) = make_float4(o[0], o[1], o[2], o[3]);
     } else {
-        for (int c = 0; c < ncol; ++c) op[c] = o[c];
+        for (int c = 0; c < ncol; ++c) g.out[off + c] = o[c];
     }
     if (g.counts) {
-        int32_t *cp = g.counts + (size_t)b * g.strideO + (size_t)i * g.ldo + j0;
-        if (ncol == 4 && (reinterpret_cast<uintptr_t>(cp) & 15) == 0) {
-            *reinterpret_cast<int4 *>(cp) = make_int4(cnt[0], cnt[1], cnt[2], cnt[3]);
+        const int KL = Li > 0 ? g.K * Li : 0;
+        int32_t cnt[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int32_t p = PINT ? Pi[c] : (int32_t)P[c];
+            cnt[c] = Li > 0 ? (BIP ? (KL + p) / 2 : p) : 0;
+        }
+        if (ncol == 4 && g.vec_cnt) {
+            *reinterpret_cast<int4 *>(g.counts + off) = make_int4(cnt[0], cnt[1], cnt[2], cnt[3]);
         } else {
-            for (int c = 0; c < ncol; ++c) cp[c] = cnt[c];
+            for (int c = 0; c < ncol; ++c) g.counts[off + c] = cnt[c];
         }
     }
 }
@@ -388,19 +395,20 @@ __device__ __forceinline__ void mdecode4(const int32_t (&P)[4], int p, int j0, i
     const int i = ws_ptr<int32_t>(wsa, lay.off_perm)[p];
     if (i < 0) return;
     const int Li = ws_ptr<int32_t>(wsa, lay.off_Ls)[p];
-    const float scale = g.sA[(size_t)b * g.strideSA + i] * 16129.0f;
+    const float f = decode_factor(g.sA[(size_t)b * g.strideSA + i], Li);
     const float *sBb = g.sB + (size_t)b * g.strideSB;
     float sBj[4];
+    const float Pf[4] = {(float)P[0], (float)P[1], (float)P[2], (float)P[3]};
 #pragma unroll
     for (int c = 0; c < 4; ++c) sBj[c] = sBb[c < ncol ? j0 + c : j0];
-    mdecode4_store<BIP>(P, i, Li, scale, sBj, j0, ncol, b, g);
+    decode4_store<BIP, true>(Pf, P, i, Li, f, sBj, j0, ncol, b, g);
 }
 
-// What the decode of a whole 256 x 256 tile needs, staged in LDS once per tile: per row of
-// the pair its original row (-1: padding), length and scale times 127^2; per column its scale.
+// What the decode of a whole 256-row tile needs, staged in LDS once per tile: per row of
+// the pair its original row (-1: padding), length and decode factor; per column its scale.
 struct DecodeLds {
     int32_t row[256], len[256];
-    float scale[256], sB[256];
+    float f[256], sB[256];
 };
 
 template <int NT>
@@ -408,26 +416,47 @@ __device__ __forceinline__ void d_stage(DecodeLds &d, const int32_t *perm, const
                                         const MGemmArgs &g, int tid) {
     for (int r = tid; r < 256; r += NT) {
         const int i = perm[r];
+        const int L = i >= 0 ? Ls[r] : 0;
         d.row[r] = i;
-        d.len[r] = i >= 0 ? Ls[r] : 0;
-        d.scale[r] = i >= 0 ? g.sA[(size_t)b * g.strideSA + i] * 16129.0f : 0.0f;
+        d.len[r] = L;
+        d.f[r] = i >= 0 ? decode_factor(g.sA[(size_t)b * g.strideSA + i], L) : 0.0f;
         const int j = tw * 256 + r;
         d.sB[r] = j < g.N ? g.sB[(size_t)b * g.strideSB + j] : 0.0f;
     }
 }
 
-// decode of row r of the pair, column quad cq of the tile, from the staged data
-template <bool BIP>
-__device__ __forceinline__ void d_decode4(const DecodeLds &d, const int4 &qv, int r, int cq, int tw, int b,
-                                          const MGemmArgs &g) {
+// Decode of TR rows of a whole tile from their sums T (fp32, row-major, row stride TS, the
+// tile's columns from 0): thread tid takes column quad tid % NQ of rows tid / NQ + k NT / NQ.
+// All of a thread's LDS reads are issued before its stores.
+template <bool BIP, int NT, int NQ, int TR, int TS>
+__device__ __forceinline__ void d_rows(const DecodeLds &d, const float *T, int row0, int tw, int b,
+                                       const MGemmArgs &g, int tid) {
+    constexpr int RPW = NT / NQ, KQ = TR / RPW;
+    const int cq = tid % NQ, r0 = tid / NQ;
     const int j0 = tw * 256 + 4 * cq;
-    if (j0 >= g.N || d.row[r] < 0) return;
-    const int32_t P[4] = {qv.x, qv.y, qv.z, qv.w};
     const int ncol = min(4, g.N - j0);
+    if (ncol <= 0) return;
     float sBj[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) sBj[c] = d.sB[4 * cq + (c < ncol ? c : 0)];
-    mdecode4_store<BIP>(P, d.row[r], d.len[r], d.scale[r], sBj, j0, ncol, b, g);
+    float4 v[KQ];
+    int row[KQ], len[KQ];
+    float f[KQ];
+#pragma unroll
+    for (int k = 0; k < KQ; ++k) {
+        const int rl = r0 + RPW * k;
+        v[k] = *reinterpret_cast<const float4 *>(&T[rl * TS + 4 * cq]);
+        row[k] = d.row[row0 + rl];
+        len[k] = d.len[row0 + rl];
+        f[k] = d.f[row0 + rl];
+    }
+#pragma unroll
+    for (int k = 0; k < KQ; ++k) {
+        if (row[k] < 0) continue;
+        const float P[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+        const int32_t none[4] = {0, 0, 0, 0};
+        decode4_store<BIP, false>(P, none, row[k], len[k], f[k], sBj, j0, ncol, b, g);
+    }
 }
 
 // A part's int32 partial sums [256 rows][256 columns] from a wave's 4 x NB blocks of 32 x 32
@@ -1307,7 +1336,7 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
                      b, tw, g, tid);
         constexpr int TS = 256 + 4, TR = 64;
         static_assert(TR * TS * 4 <= QNBUF * QBUF * 16, "the epilogue transpose must fit the LDS buffers");
-        int32_t *T = reinterpret_cast<int32_t *>(smem);
+        float *T = reinterpret_cast<float *>(smem);
         for (int h = 0; h < 256 / TR; ++h) {
             __syncthreads();
             // rows 64h .. 64h + 63: MFMA blocks i = 2 (h % 2), 2 (h % 2) + 1 of the waves at wr = 128 (h / 2)
@@ -1320,15 +1349,11 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
 #pragma unroll
                         for (int e = 0; e < 16; ++e)
                             T[(32 * (i & 1) + 8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] =
-                                (int32_t)acc[i][c][e];
+                                acc[i][c][e];
                 }
             }
             __syncthreads();
-            for (int k = 0; k < TR * 64 / 256; ++k) {
-                const int idx = tid + 256 * k;        // 64 rows x 64 column quads
-                const int rl = idx >> 6, cq = idx & 63;
-                d_decode4<BIP>(dl, *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]), TR * h + rl, cq, tw, b, g);
-            }
+            d_rows<BIP, 256, 64, TR, TS>(dl, T, TR * h, tw, b, g, tid);
         }
     }
 }
@@ -2016,7 +2041,7 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     d_stage<NT>(dl, perm, Ls, b, tw, g, tid);
     constexpr int TS = 256 + 4, TR = 32;
     static_assert(TR * TS * 4 <= 256 * 16 * 16, "the epilogue transpose must fit the table");
-    int32_t *T = reinterpret_cast<int32_t *>(lut);
+    float *T = reinterpret_cast<float *>(lut);
     for (int h = 0; h < 256 / TR; ++h) {
         __syncthreads();
         // rows 32h .. 32h + 31: block i of the waves of row half rh with r_row0(rh, i) = 32 h
@@ -2028,17 +2053,11 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
                 for (int c = 0; c < NB; ++c)
 #pragma unroll
                     for (int e = 0; e < 16; ++e)
-                        T[(8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] = (int32_t)acc[i][c][e];
+                        T[(8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] = acc[i][c][e];
             }
         }
         __syncthreads();
-        constexpr int NQ = NARROW ? 16 : 64;      // column quads of the block
-#pragma unroll
-        for (int k = 0; k < TR * NQ / NT; ++k) {
-            const int idx = tid + NT * k;         // 32 rows x NQ column quads
-            const int rl = idx / NQ, cq = idx % NQ;
-            d_decode4<BIP>(dl, *reinterpret_cast<const int4 *>(&T[rl * TS + 4 * cq]), TR * h + rl, cq, tw, b, g);
-        }
+        d_rows<BIP, NT, NARROW ? 16 : 64, TR, TS>(dl, T, TR * h, tw, b, g, tid);
     }
 }
 
@@ -2090,6 +2109,8 @@ static MGemmArgs make_gemm_args(const sc_gemm_desc &d, const Layout &lay, const 
     g.ldo = d.ldo;
     g.out = out;
     g.counts = counts;
+    g.vec_out = reinterpret_cast<uintptr_t>(out) % 16 == 0 && d.ldo % 4 == 0 && d.strideO % 4 == 0;
+    g.vec_cnt = reinterpret_cast<uintptr_t>(counts) % 16 == 0 && d.ldo % 4 == 0 && d.strideO % 4 == 0;
     return g;
 }
 
