@@ -215,24 +215,42 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
             }
         }
     }
-    // 256 x 64 blocks (N <= 64: attention P.V, per-head layers) with varying lengths: each tile
-    // gets its own number of parts on the device, once the lengths are known (k_units), at
-    // most S.  (On the 256 x 256 blocks the per-tile split measured no better than the split
-    // chosen below for every tile: 6304 x 768 x 3072 with lengths 16..256 +1 %, the DiT-XL/2
-    // pair -3 %.)
-    l.vsplit = quad && l.narrow && tiles > 0 && !l.q_one && l.F == 0 && l.S > 1;
+    // Int8-chunk GEMM with varying lengths: the work of a tile follows its rows' lengths
+    // (Sec. 4.1: the cost follows the sum of the l_i), known only on the device.  There the
+    // tiles' chunk steps are laid end to end and cut into sk_slots equal ranges, one per GEMM
+    // block (k_units): a tile inside a range runs whole, one that a cut crosses runs in
+    // pieces that the split-sum pass adds.  A range holds at most RSTEP_EXACT steps, so every
+    // whole tile and piece sums exactly.
+    // (Short tiles, a few chunk steps each, keep the division below: their pieces' partial sums
+    // and their in-GEMM decodes would cost as much as the steps; ViT-L/14 Q.K^T heads with
+    // K = 64 took 0.61 ms cut into ranges against 0.41 ms split alike.)
+    l.pcols = l.narrow ? 64 : l.mbn;
+    l.vsplit = quad && l.rgen && tiles > 0 && !l.q_one &&
+               (int64_t)l.KC * ((int64_t)(Lmean + 31) / 32) >= 16;
     l.off_units = off;
+    int64_t pieces = quad ? (tiles - l.F) * (int64_t)l.S : tiles * (int64_t)l.S;
     if (l.vsplit) {
-        off = align256(off + (size_t)tiles * l.S * 16);
+        const int64_t wmax = tiles * (int64_t)l.KC * (l.LBS / 32);
+        int64_t sl = l.q_slots;
+        if (wmax > sl * RSTEP_EXACT) sl = (wmax + RSTEP_EXACT - 1) / RSTEP_EXACT;
+        if (sl > (1 << 20)) return false;
+        l.sk_slots = (int)sl;
+        l.F = 0;
+        l.S = 1;
+        off = align256(off + (size_t)(tiles + sl) * 16);
         l.off_tinfo = off;
         off = align256(off + (size_t)tiles * 8);
+        l.off_slot = off;
+        off = align256(off + (size_t)(sl + 1) * 4);
+        // a cut inside a tile adds one piece to it and may make it a split tile: at most two
+        // pieces per cut
+        pieces = 2 * sl;
     }
     l.off_part = off;
-    if (l.S > 1) {
+    if (pieces > 0 && (l.S > 1 || l.vsplit)) {
         size_t partb;
-        const int64_t split_tiles = quad ? tiles - l.F : tiles;
-        // every part is laid out as a whole tile, [mbm rows][mbn columns] of int32
-        if (!mul_ok((size_t)split_tiles * (size_t)l.S, (size_t)l.mbm * (size_t)l.mbn * 4, &partb)) return false;
+        // every piece is [mbm rows][pcols columns] of int32
+        if (!mul_ok((size_t)pieces, (size_t)l.mbm * (size_t)l.pcols * 4, &partb)) return false;
         off = align256(off + partb);
     }
 

@@ -21,8 +21,10 @@
 //     tileOff[MT]      word offset of tile t's planes inside Ap
 //     Ap               fp4 planes of A (or int8 chunks, below)
 //   part       partial counts when GEMM tiles are split along the inner (element, cycle) range
-//   units      vsplit only: the 256-row GEMM's work units {tile, part, parts, partial index}
-//              (int4) and per tile {parts, partial index of part 0} (int2), from k_units
+//   units      vsplit only (k_units): the 256-row GEMM's work units {tile, first chunk step,
+//              end chunk step, partial index or -1} (int4), per tile {pieces, partial index
+//              of piece 0} (int2), and per GEMM block the first of its units (uint32,
+//              sk_slots + 1 of them)
 //   per batch entry of B (1 if B is broadcast, else batch entries):
 //     Bp               fp4 planes of B (or int8 chunks)
 //
@@ -85,6 +87,8 @@ __host__ __device__ inline double quad_split_time(int64_t tiles, int s, double p
 constexpr int OCH = 8;           // octets per block of the nibble-plane generator
 constexpr int RSLOTS = 4;        // int8-chunk GEMM: tables masked to a row length, per cycle group
 constexpr int64_t MFMA_EXACT = 1ll << 24;   // products one fp32 accumulator sums exactly
+constexpr int64_t RSTEP_EXACT = MFMA_EXACT / (32 * 32);   // int8-chunk GEMM chunk steps (32 cycles x
+                                                          // 32 elements) one accumulator sums exactly
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -136,10 +140,12 @@ struct Layout {
     int q_slots;              // 256-row GEMM split model: blocks that run at once
     double q_pbytes;          // 256-row GEMM split model: partial-sum bytes of one part (the
                               // columns a block computes: 256, or 64 with N <= 64)
-    size_t off_part;   // partial counts of split tiles: [split tiles][S][tile rows][tile columns]
-    int vsplit;        // 256-row GEMM, lengths vary and tiles are split: each tile gets its own
-                       // number of parts (k_units), at most S
-    size_t off_units, off_tinfo;
+    size_t off_part;   // partial counts of split tiles: [pieces][256 rows][pcols columns] int32
+    int pcols;         // columns of a piece of partial counts: 256, or 64 for the 256 x 64 blocks
+    int vsplit;        // int8-chunk GEMM with varying lengths: the tiles' chunk steps, end to
+                       // end, are cut into sk_slots equal ranges, one per GEMM block (k_units)
+    int sk_slots;      // vsplit: GEMM blocks, each running one range of the work
+    size_t off_units, off_tinfo, off_slot;
     size_t total;
 };
 

@@ -370,97 +370,65 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     }
 }
 
-// Work units of the 256-row GEMM when row lengths vary (Layout::vsplit).  Tile t (pair tp of
-// batch entry b x B pair tw, the GEMM's tile order: longest pairs first) runs tileL[tp]
-// cycles.  With the average load of a block slot A = sum / slots and the cap S: when the
-// lengths are skewed (longest tile > 2 A), a tile longer than T = max(A, longest / S) is
-// split into the fewest of 2, 4, .. S parts that bring each part to T and the others run
-// whole, so only long tiles pay for partial sums (Sec. 4.1: the cost follows the sum of the
-// l_i); otherwise every tile is split alike, as the split model picks for the longest tile
-// (as measured where this division ran on 256-column blocks too: 4096 x 1152 x 4608 with
-// group lengths 24..192 took 0.78 ms with the long tiles alone split, 0.67 ms split alike).
-// Units are listed tile by tile as {tile, part, parts, partial index}, tinfo[t] = {parts,
-// partial index of part 0}, and the unit count goes to status word 3.  A tile is never split
-// into fewer than Smin parts.  One block.
-__global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, int S, uint8_t *ws) {
-    __shared__ int64_t rsum[16];
-    __shared__ int rmax[16];
+// Work division of the int8-chunk GEMM when row lengths vary (Layout::vsplit).  Tile t (pair
+// tp of batch entry b x B pair tw, in the GEMM's tile order: longest pairs first) runs w_t =
+// ceil(tileL / 32) x KC chunk steps (32-cycle groups x 32-element chunks; at least 1, so that
+// a tile of rows of length 0 still writes its zeros).  The steps of all tiles are laid end to
+// end and cut into sk_slots ranges of T = ceil(W / sk_slots) steps, range s for GEMM block s:
+// every block gets the same share of the sum of the row lengths (Sec. 4.1: the cost follows
+// the sum of the l_i).  A tile inside one range runs whole and is decoded by its block; a tile
+// that c cuts cross runs as c + 1 pieces, whose partial sums the split-sum pass adds.
+// Written: units {tile, first step, end step, partial index or -1} in tile order, which is
+// range order; slot[s] = the first unit of range s (slot[sk_slots] = the unit count);
+// tinfo[t] = {pieces, partial index of piece 0}.  One block.
+__global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *ws) {
     const int tid = threadIdx.x;
-    const int NTW = lay.NT / 2, npairs = lay.MT / 2;
+    const int NTW = lay.NT / 2, npairs = lay.MT / 2, slots = lay.sk_slots;
     const int tiles = batch * npairs * NTW;
-    auto work = [&](int t) {
+    auto work = [&](int t) -> int64_t {
         const int tb = t / NTW, b = tb % batch, tp = tb / batch;
-        return ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_tileL)[2 * tp];
+        const int L = ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_tileL)[2 * tp];
+        const int64_t w = (int64_t)((L + 31) / 32) * lay.KC;
+        return w > 0 ? w : 1;
     };
-    int64_t sum = 0;
-    int mx = 0;
-    for (int t = tid; t < tiles; t += 1024) {
-        const int w = work(t);
-        sum += w;
-        mx = max(mx, w);
+    int64_t W = 0;
+    for (int c = 0; c < tiles; c += 1024) {
+        int64_t tot;
+        block_excl_scan_1024(c + tid < tiles ? work(c + tid) : 0, &tot);
+        W += tot;
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        sum += __shfl_xor(sum, o, 64);
-        mx = max(mx, __shfl_xor(mx, o, 64));
-    }
-    if ((tid & 63) == 0) {
-        rsum[tid >> 6] = sum;
-        rmax[tid >> 6] = mx;
-    }
-    __syncthreads();
-    sum = 0;
-    mx = 0;
-    for (int k = 0; k < 16; ++k) {
-        sum += rsum[k];
-        mx = max(mx, rmax[k]);
-    }
-    const double A = (double)sum / lay.q_slots;
-    // Skewed lengths (the longest tile more than twice the average load of a slot): split only
-    // the long tiles.  Otherwise tiles of similar length pack better as equal parts: every tile
-    // gets the same number of parts, the one the split model picks for the longest tile.
-    double T = fmax(A, (double)mx / S);
-    int sall = 0;
-    if (mx <= 2.0 * A) {
-        double best = 0.0;
-        for (int s = lay.Smin; s <= S; s *= 2) {
-            const double est = quad_split_time(tiles, s, lay.q_perL, lay.q_Lmean, (double)mx, false, lay.q_slots,
-                                               lay.q_pbytes);
-            if (s == lay.Smin || est < best * 0.97) {
-                best = est;
-                sall = s;
-            }
-        }
-    }
+    const int64_t T = (W + slots - 1) / slots;
     int4 *units = ws_ptr<int4>(ws, lay.off_units);
     int2 *tinfo = ws_ptr<int2>(ws, lay.off_tinfo);
-    int64_t ucarry = 0, pcarry = 0;
+    uint32_t *slot = ws_ptr<uint32_t>(ws, lay.off_slot);
+    int64_t ccarry = 0, ucarry = 0, pcarry = 0;
     for (int c = 0; c < tiles; c += 1024) {
         const int t = c + tid;
-        // (never fewer than Smin parts: each part's fp32 sums stay exact)
-        int s = lay.Smin;
-        if (sall > 0) {
-            s = sall;
-        } else if (t < tiles) {
-            const double w = work(t);
-            while (s < S && w > T * s) s *= 2;
-        }
-        int64_t utot, ptot;
-        const int64_t ux = block_excl_scan_1024(t < tiles ? s : 0, &utot);
-        const int64_t px = block_excl_scan_1024(t < tiles && s > 1 ? s : 0, &ptot);
+        const int64_t w = t < tiles ? work(t) : 0;
+        int64_t ctot, utot, ptot;
+        const int64_t C = ccarry + block_excl_scan_1024(w, &ctot);
+        const int np = t < tiles ? (int)((C + w - 1) / T - C / T + 1) : 0;
+        const int64_t U = ucarry + block_excl_scan_1024(np, &utot);
+        const int64_t P = pcarry + block_excl_scan_1024(np > 1 ? np : 0, &ptot);
         if (t < tiles) {
-            const int ub = (int)(ucarry + ux), pb = (int)(pcarry + px);
-            tinfo[t] = make_int2(s, pb);
-            for (int p = 0; p < s; ++p) units[ub + p] = make_int4(t, p, s, pb + p);
+            tinfo[t] = make_int2(np, np > 1 ? (int)P : -1);
+            for (int p = 0; p < np; ++p) {
+                const int64_t s0 = C / T + p;
+                const int64_t a = p == 0 ? C : s0 * T, e = p == np - 1 ? C + w : (s0 + 1) * T;
+                units[U + p] = make_int4(t, (int)(a - C), (int)(e - C), np > 1 ? (int)(P + p) : -1);
+                if (a % T == 0) slot[a / T] = (uint32_t)(U + p);
+            }
         }
+        ccarry += ctot;
         ucarry += utot;
         pcarry += ptot;
     }
-    if (tid == 0) ws_ptr<uint32_t>(ws, lay.off_status)[3] = (uint32_t)ucarry;
+    // ranges past the end of the work hold no unit
+    for (int64_t s = (W + T - 1) / T + tid; s <= slots; s += 1024) slot[s] = (uint32_t)ucarry;
 }
 
 hipError_t launch_units(const sc_gemm_desc &d, const Layout &lay, uint8_t *ws, hipStream_t st) {
-    hipLaunchKernelGGL(k_units, dim3(1), dim3(1024), 0, st, lay, d.batch, lay.S, ws);
+    hipLaunchKernelGGL(k_units, dim3(1), dim3(1024), 0, st, lay, d.batch, ws);
     return hipGetLastError();
 }
 

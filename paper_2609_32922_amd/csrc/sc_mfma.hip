@@ -56,6 +56,7 @@
 
 namespace scg {
 
+typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));   // one slot row: 32 nibbles
@@ -459,42 +460,43 @@ __device__ __forceinline__ void d_rows(const DecodeLds &d, const float *T, int r
     }
 }
 
-// A part's int32 partial sums [256 rows][256 columns] from a wave's 4 x NB blocks of 32 x 32
-// accumulators at (wr, wc): one lane offset, each element's offset in a scalar register.
+// Partial sums of a piece of a 256-row tile, in the MFMA's own layout: [row block rb of 32
+// rows][column block cb of 32 columns][quad q][lane][4] int32, with (rb, cb) numbered
+// rb * (PC / 32) + cb for a piece PC columns wide.  Lane (grp, i32) of quad q holds rows
+// 32 rb + 8 q + 4 grp + j (j = 0..3) of column 32 cb + i32: the four accumulator elements
+// 4q .. 4q + 3 of its 32 x 32 block, stored as one 16-byte store (a wave writes 1 KB at a time).
+template <int PC>
+__device__ __forceinline__ void store_block(const v16f &a, __amdgpu_buffer_rsrc_t pr, int lane, int rb, int cb) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const v4i v = {(int)a[4 * q], (int)a[4 * q + 1], (int)a[4 * q + 2], (int)a[4 * q + 3]};
+        __builtin_amdgcn_raw_buffer_store_b128(v, pr, lane * 16, (((rb * (PC / 32) + cb) * 4 + q) * 64) * 16, 0);
+    }
+}
+
+// A wave's 4 x NB blocks of 32 x 32 at rows wr + 32 i, columns wc + 32 c (256-column pieces)
 template <int NB>
-__device__ __forceinline__ void store_part(const v16f (&acc)[4][NB], int32_t *part, int wr, int wc, int grp,
-                                           int i32) {
+__device__ __forceinline__ void store_part(const v16f (&acc)[4][NB], int32_t *part, int wr, int wc, int lane) {
     const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(part, 0, 256 * 256 * 4, 0x00020000);
-    const int voff = ((wr + 4 * grp) * 256 + wc + i32) * 4;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int c = 0; c < NB; ++c)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                __builtin_amdgcn_raw_buffer_store_b32((uint32_t)(int32_t)acc[i][c][e], pr, voff,
-                                                      ((32 * i + 8 * (e >> 2) + (e & 3)) * 256 + 32 * c) * 4, 0);
+        for (int c = 0; c < NB; ++c) store_block<256>(acc[i][c], pr, lane, wr / 32 + i, wc / 32 + c);
 }
 
 // The same for the int8-chunk GEMM, whose wave of row half rh holds the pair's row blocks
-// starting at r_row0<SKIP>(rh, i) (declared with that GEMM below).
+// starting at r_row0<SKIP>(rh, i) (declared with that GEMM below); a piece is the block's
+// columns wide (256, or 64 for the 256 x 64 blocks).
 template <bool SKIP>
 __device__ __forceinline__ int r_row0(int rh, int i);
 template <bool SKIP, int NB>
-__device__ __forceinline__ void store_part_r(const v16f (&acc)[4][NB], int32_t *part, int rh, int wc, int grp,
-                                             int i32) {
-    const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(part, 0, 256 * 256 * 4, 0x00020000);
-    const int voff = ((4 * grp) * 256 + wc + i32) * 4;
+__device__ __forceinline__ void store_part_r(const v16f (&acc)[4][NB], int32_t *part, int rh, int wc, int lane) {
+    constexpr int PC = NB == 2 ? 64 : 256;
+    const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(part, 0, 256 * PC * 4, 0x00020000);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int r0 = r_row0<SKIP>(rh, i);
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int c = 0; c < NB; ++c)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                __builtin_amdgcn_raw_buffer_store_b32((uint32_t)(int32_t)acc[i][c][e], pr, voff,
-                                                      ((r0 + 8 * (e >> 2) + (e & 3)) * 256 + 32 * c) * 4, 0);
-    }
+        for (int c = 0; c < NB; ++c) store_block<PC>(acc[i][c], pr, lane, r_row0<SKIP>(rh, i) / 32, wc / 32 + c);
 }
 
 // Block tile: BM = 128 rows of A x WB columns of B, WB = 256 (two 128-column B plane
@@ -1227,22 +1229,12 @@ __device__ __forceinline__ int q_whole_tile(int u, int F, int NTW, int one_lengt
     return u;
 }
 
-// Work unit u of the 256-row GEMM: its tile, part s of S parts, and the partial index v of a
-// split unit; false when u is past the call's units (the grid is sized for the most).
-// Units 0 .. F-1 are whole tiles (q_whole_tile), unit F + v part v % S of tile F + v / S; with
-// vsplit the list k_units wrote.
+// Work unit u of the 256-row GEMM when every tile has one division (not vsplit): its tile,
+// part s of S parts, and the partial index v of a split unit; false when u is past the call's
+// units (the grid is sized for the most).  Units 0 .. F-1 are whole tiles (q_whole_tile),
+// unit F + v part v % S of tile F + v / S.
 __device__ __forceinline__ bool q_unit(const MGemmArgs &g, const Layout &lay, uint8_t *ws, int u, int &tile, int &s,
                                        int &S, int &v, bool &split) {
-    if (lay.vsplit) {
-        if (u >= (int)ws_ptr<uint32_t>(ws, lay.off_status)[3]) return false;
-        const int4 e = ws_ptr<int4>(ws, lay.off_units)[u];
-        tile = e.x;
-        s = e.y;
-        S = e.z;
-        v = e.w;
-        split = S > 1;
-        return true;
-    }
     const int NTW = lay.NT / 2;
     int F, SS;
     q_division(g, lay, ws, F, SS);
@@ -1328,7 +1320,7 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
 
     if (split) {
         // partial sums of this unit as int32 [256 rows][256 columns]
-        store_part<4>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256, wr, wc, grp, i32);
+        store_part<4>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256, wr, wc, lane);
     } else {
         // the rows' and columns' data staged in LDS, the sums transposed through LDS, 64 rows
         // at a time, so that each thread decodes four adjacent columns of one row
@@ -1358,21 +1350,21 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
     }
 }
 
-// sums the partial counts of every part of the split tiles F.. and decodes (256 / QR_ROWS
-// blocks per tile of QR_ROWS rows each; thread = row x four adjacent columns).  8-row blocks
-// when few tiles are split, so that enough waves keep loads in flight; 32-row blocks when many
-// are (less per-block overhead).
-template <bool BIP, int QR_ROWS>
+// Sums the partial counts of every piece of the split tiles F.. and decodes.  Pieces are in
+// the MFMA layout (store_block), PC columns wide; a thread takes NK quads of it, each four
+// rows of one column, and a block of 256 threads 256 NK quads (BPT blocks per tile).  Few
+// quads per thread when few tiles are split, so that enough waves keep loads in flight; more
+// when many are (less per-block overhead).  With vsplit, tinfo gives each tile's pieces
+// (tiles that ran whole have none).
+template <bool BIP, int NK, int PC>
 __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, uint8_t *ws) {
-    constexpr int NK = QR_ROWS * 64 / 256;    // column quads per thread
-    constexpr int BPT = 256 / QR_ROWS;        // blocks per tile
+    constexpr int QPT = 256 * PC / 4;         // quads per tile
+    constexpr int BPT = QPT / (256 * NK);     // blocks per tile
     const int NTW = lay.NT / 2;
     int F, SS;
     q_division(g, lay, ws, F, SS);
     const int tile = F + (int)(blockIdx.x / BPT), part = (int)(blockIdx.x % BPT);
     if (tile >= g.batch * (lay.MT / 2) * NTW) return;
-    // partial index of the tile's first part: tiles F.. in SS parts each, or the tile's own
-    // number of parts (vsplit; tiles that ran whole have nothing to sum)
     size_t pbase = (size_t)(tile - F) * SS;
     if (lay.vsplit) {
         const int2 ti = ws_ptr<int2>(ws, lay.off_tinfo)[tile];
@@ -1383,24 +1375,20 @@ __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, u
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
-    const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part) + pbase * 256 * 256) +
-                       (size_t)part * QR_ROWS * 64 + threadIdx.x;
-    // a thread keeps NK column quads; quads past N hold nothing to sum (nor, in the 64-column
-    // blocks, anything written).  Every part's loads are issued before any sum.
-    const bool colok = tw * 256 + 4 * (int)(threadIdx.x & 63) < g.N;
-    const int ns = colok ? SS : 0;
-    // (8-row blocks: every part's loads in flight at once; 32-row blocks: one part at a time)
+    const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part)) + pbase * QPT +
+                       (size_t)part * 256 * NK + threadIdx.x;
+    // (NK <= 2: every piece's loads in flight at once; else one piece at a time)
     constexpr int SB = NK <= 2 ? MAX_SPLIT : 1;
     int4 sum[NK];
 #pragma unroll
     for (int k = 0; k < NK; ++k) sum[k] = make_int4(0, 0, 0, 0);
-    for (int s0 = 0; s0 < ns; s0 += SB) {
+    for (int s0 = 0; s0 < SS; s0 += SB) {
         int4 q[SB][NK];
 #pragma unroll
         for (int s = 0; s < SB; ++s)
 #pragma unroll
             for (int k = 0; k < NK; ++k)
-                q[s][k] = s0 + s < ns ? base[(size_t)(s0 + s) * 256 * 64 + 256 * k] : make_int4(0, 0, 0, 0);
+                q[s][k] = s0 + s < SS ? base[(size_t)(s0 + s) * QPT + 256 * k] : make_int4(0, 0, 0, 0);
 #pragma unroll
         for (int s = 0; s < SB; ++s)
 #pragma unroll
@@ -1411,24 +1399,46 @@ __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, u
                 sum[k].w += q[s][k].w;
             }
     }
-    const int32_t *perm = ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_perm);
+    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
+    const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm) + tp * 256;
+    const int32_t *Ls = ws_ptr<int32_t>(wsa, lay.off_Ls) + tp * 256;
+    const float *sBb = g.sB + (size_t)b * g.strideSB;
+    const int lane = threadIdx.x & 63, grp = lane >> 5, i32 = lane & 31;
 #pragma unroll
     for (int k = 0; k < NK; ++k) {
-        const int idx = threadIdx.x + 256 * k;
-        const int rl = part * QR_ROWS + (idx >> 6), cq = idx & 63;
-        const int j0 = tw * 256 + 4 * cq;
-        if (j0 >= g.N || perm[tp * 256 + rl] < 0) continue;
+        const int qd = (part * 256 * NK + 256 * k + (int)threadIdx.x) >> 6;   // quad index of the wave
+        const int blk = qd >> 2, q = qd & 3;
+        const int r0 = (blk / (PC / 32)) * 32 + 8 * q + 4 * grp;
+        const int j = tw * 256 + (blk % (PC / 32)) * 32 + i32;
+        if (j >= g.N) continue;
+        const float sBj = sBb[j];
         const int32_t P[4] = {sum[k].x, sum[k].y, sum[k].z, sum[k].w};
-        mdecode4<BIP>(P, tp * 256 + rl, j0, min(4, g.N - j0), b, g, lay, ws);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int i = perm[r0 + e];
+            if (i < 0) continue;
+            const int Li = Ls[r0 + e];
+            const float f = decode_factor(g.sA[(size_t)b * g.strideSA + i], Li);
+            const size_t off = (size_t)b * g.strideO + (size_t)i * g.ldo + j;
+            g.out[off] = ((float)P[e] * f) * sBj;
+            if (g.counts) g.counts[off] = Li > 0 ? (BIP ? (g.K * Li + P[e]) / 2 : P[e]) : 0;
+        }
     }
 }
 
 template <bool BIP>
 static hipError_t launch_qreduce(const MGemmArgs &g, const Layout &lay, uint8_t *ws, unsigned tail, hipStream_t st) {
-    if (tail * 8u < 1024u)
-        hipLaunchKernelGGL((k_qgemm_reduce<BIP, 8>), dim3(tail * 32u), dim3(256), 0, st, g, lay, ws);
-    else
-        hipLaunchKernelGGL((k_qgemm_reduce<BIP, 32>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
+    if (lay.pcols == 64) {
+        if (tail * 16u < 1024u)
+            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 1, 64>), dim3(tail * 16u), dim3(256), 0, st, g, lay, ws);
+        else
+            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 4, 64>), dim3(tail * 4u), dim3(256), 0, st, g, lay, ws);
+    } else {
+        if (tail * 8u < 1024u)
+            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 2, 256>), dim3(tail * 32u), dim3(256), 0, st, g, lay, ws);
+        else
+            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 8, 256>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
+    }
     return hipGetLastError();
 }
 
@@ -1902,14 +1912,38 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     __shared__ DecodeLds dl;                          // filled after the chunk loop
     if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
     const int NTW = lay.NT / 2;
-    int tile, s, S, v;
+    // the block's units: one, or with vsplit its range of the work (k_units)
+    int ub = blockIdx.x, ue = blockIdx.x + 1;
+    if (lay.vsplit) {
+        const uint32_t *sl = ws_ptr<uint32_t>(ws, lay.off_slot);
+        ub = (int)sl[blockIdx.x];
+        ue = (int)sl[blockIdx.x + 1];
+    }
+    for (int u = ub; u < ue; ++u) {
+    // (the previous unit's epilogue is done with the LDS)
+    if (u != ub) __syncthreads();
+    int tile, s = 0, S = 1, v = -1;
+    int64_t ux0 = 0, ux1 = 0;
     bool split;
-    if (!q_unit(g, lay, ws, blockIdx.x, tile, s, S, v, split)) return;
+    if (lay.vsplit) {
+        const int4 e = ws_ptr<int4>(ws, lay.off_units)[u];
+        tile = e.x;
+        ux0 = e.y;
+        ux1 = e.z;
+        v = e.w;
+        split = v >= 0;
+    } else if (!q_unit(g, lay, ws, u, tile, s, S, v, split)) {
+        return;
+    }
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
     const int bB = g.nbB == 1 ? 0 : b;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    // the thread index passes through an empty asm statement on every unit, so that nothing
+    // derived from it is hoisted out of the unit loop and held (spilled) across it
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, w = tid >> 6;
     const int grp = lane >> 5, i32 = lane & 31;
     const int rh = NARROW ? w : (w >> 1), wc = NARROW ? 0 : (w & 1) * 128;   // row half, columns
     uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
@@ -1919,7 +1953,9 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     const int ngroups = (int)(round_up(ws_ptr<int32_t>(wsa, lay.off_tileL)[2 * tp], RCH) / RCH);
 
     const int64_t nch = (int64_t)ngroups * g.KC;
-    const int64_t x0 = (int64_t)s * nch / S, x1 = (int64_t)(s + 1) * nch / S;
+    // the unit's chunk steps (a tile of rows of length 0 has none)
+    const int64_t x1 = lay.vsplit ? min(ux1, nch) : (int64_t)(s + 1) * nch / S;
+    const int64_t x0 = lay.vsplit ? min(ux0, x1) : (int64_t)s * nch / S;
 
     if (TABLES) {
         if (tid < ngroups) rems[tid] = 0u;
@@ -2032,8 +2068,8 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     }
 
     if (split) {
-        store_part_r<SKIP, NB>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * 256, rh, wc, grp, i32);
-        return;
+        store_part_r<SKIP, NB>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * lay.pcols, rh, wc, lane);
+        continue;
     }
     // a whole tile decodes: the rows' and columns' data staged in LDS, the sums transposed
     // through LDS, 32 rows at a time, so that each thread decodes four adjacent columns of
@@ -2059,13 +2095,15 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
         __syncthreads();
         d_rows<BIP, NT, NARROW ? 16 : 64, TR, TS>(dl, T, TR * h, tw, b, g, tid);
     }
+    }
 }
 
 template <bool BIP, bool NARROW>
 static hipError_t launch_rgemm_w(const MGemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
     const unsigned tiles = (unsigned)(g.batch * (lay.MT / 2) * (lay.NT / 2));
     const unsigned tail = tiles - (unsigned)g.F;
-    const dim3 grid((unsigned)g.F + tail * (unsigned)g.S), block(NARROW ? 128 : 256);
+    const dim3 grid(lay.vsplit ? (unsigned)lay.sk_slots : (unsigned)g.F + tail * (unsigned)g.S),
+        block(NARROW ? 128 : 256);
     hipLaunchKernelGGL((k_rgemm<BIP, false, NARROW>), grid, block, 0, st, g, lay, ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
