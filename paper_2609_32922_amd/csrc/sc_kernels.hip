@@ -205,6 +205,8 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
                                                    int M, int L_max, Layout lay, uint8_t *ws, uint64_t seed,
                                                    int rng, int ndraws) {
     __shared__ int hist[SC_L_MAX_LIMIT + 1];
+    __shared__ int hstart[SC_L_MAX_LIMIT + 1];
+    __shared__ int dpair[2048 + 1];
     const int b = blockIdx.x, tid = threadIdx.x;
     uint8_t *wsb = ws + (size_t)b * lay.stride_batchA;
     int32_t *perm = ws_ptr<int32_t>(wsb, lay.off_perm);
@@ -214,6 +216,19 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     uint32_t *status = ws_ptr<uint32_t>(ws, lay.off_status);
     const int32_t *Lb = L + (size_t)b * strideL;
 
+    // Up to SREG * 1024 rows the lengths are loaded once, all loads in flight together (issued
+    // first, so that their latency overlaps the sequences and the clearing below), and kept in
+    // registers for the scatter; longer batch entries loop (and load them twice).
+    constexpr int SREG = 20;
+    const bool cached = M <= SREG * 1024;
+    int lv[SREG];
+    if (cached) {
+#pragma unroll
+        for (int k = 0; k < SREG; ++k) {
+            const int i = k * 1024 + tid;
+            lv[k] = i < M ? Lb[i] : 0;
+        }
+    }
     if (ndraws > 0) {
         // one batch entry: this block also clears the status words and makes the comparator
         // sequences (the work of k_draws), before any of its own status updates
@@ -230,17 +245,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     }
     for (int v = tid; v <= L_max; v += 1024) hist[v] = 0;
     __syncthreads();
-    // Up to SREG * 1024 rows the lengths are loaded once, all loads in flight together, and
-    // kept in registers for the scatter; longer batch entries loop (and load them twice).
-    constexpr int SREG = 8;
-    const bool cached = M <= SREG * 1024;
-    int lv[SREG];
     if (cached) {
-#pragma unroll
-        for (int k = 0; k < SREG; ++k) {
-            const int i = k * 1024 + tid;
-            lv[k] = i < M ? Lb[i] : 0;
-        }
 #pragma unroll
         for (int k = 0; k < SREG; ++k) {
             if (lv[k] < 0 || lv[k] > L_max) {
@@ -261,14 +266,18 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         }
     }
     __syncthreads();
-    // start position of each length bucket, longest lengths first
+    // start position of each length bucket, longest lengths first (also kept in hstart: the
+    // scatter below moves hist[l] on to the end of l's run)
     int64_t carry = 0;
     for (int c = 0; c <= L_max; c += 1024) {
         const int idx = L_max - (c + tid);
         const int64_t v = idx >= 0 ? hist[idx] : 0;
         int64_t tot;
         const int64_t ex = block_excl_scan_1024(v, &tot);
-        if (idx >= 0) hist[idx] = (int)(carry + ex);
+        if (idx >= 0) {
+            hist[idx] = (int)(carry + ex);
+            hstart[idx] = (int)(carry + ex);
+        }
         carry += tot;
         __syncthreads();
     }
@@ -299,6 +308,40 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         perm[p] = -1;
         Ls[p] = 0;
     }
+    // The int8-chunk GEMM keeps, per cycle group, a table of A masked to each row length
+    // that ends inside the group: rslots of them.  Rows are sorted, so the distinct lengths of
+    // a pair are the runs of equal length that meet it; a pair that more lengths which are not
+    // multiples of 32 meet than there are tables makes the GEMM mask its fragments instead.
+    // Each such length adds one to every pair its run [hstart[l], end) meets (a difference
+    // array over pairs, then a scan); end = hstart[l - 1] (runs in order of decreasing
+    // length), or M.  (Up to 2048 pairs per pass; the first pass runs beside the scatter.)
+    const int npairs = lay.rgen ? lay.MT / 2 : 0;
+    for (int q0 = 0; q0 < npairs; q0 += 2048) {
+        const int nq = min(npairs - q0, 2048);
+        if (q0 > 0) __syncthreads();
+        for (int q = tid; q <= nq; q += 1024) dpair[q] = 0;
+        __syncthreads();
+        for (int l = tid; l <= L_max; l += 1024) {
+            const int start = hstart[l], end = l == 0 ? M : hstart[l - 1];
+            if (l % 32 == 0 || end <= start) continue;
+            const int qa = max(start >> 8, q0), qb = min((end - 1) >> 8, q0 + nq - 1);
+            if (qa > qb) continue;
+            atomicAdd(&dpair[qa - q0], 1);
+            atomicAdd(&dpair[qb + 1 - q0], -1);
+        }
+        __syncthreads();
+        int64_t pc = 0;
+        bool over = false;
+        for (int c = 0; c < nq; c += 1024) {
+            const int q = c + tid;
+            int64_t tot;
+            const int64_t v = q < nq ? dpair[q] : 0;
+            const int64_t ex = block_excl_scan_1024(v, &tot);
+            over = over || (q < nq && pc + ex + v > lay.rslots);
+            pc += tot;
+        }
+        if (__syncthreads_or(over) && tid == 0) atomicOr(status + 2, 1u);
+    }
     __syncthreads();
     // After the scatter hist[l] is the end of length l's run of sorted positions (runs in
     // order of decreasing length, ends non-increasing in l): the length at sorted position
@@ -314,7 +357,8 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         return lo;
     };
     // tile lengths (first sorted row of a tile holds its longest length; a pair of tiles
-    // that one 256-row block takes runs at the pair's longest length) and offsets
+    // that one 256-row block takes runs at the pair's longest length) and, for the GEMMs that
+    // read planes, the tiles' plane offsets
     carry = 0;
     for (int c = 0; c < lay.MT; c += 1024) {
         const int t = c + tid;
@@ -324,50 +368,15 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
             tl = (int)round_up(length_at(t0 * BM), MSTEP);
             tileL[t] = tl;
         }
-        int64_t tot;
-        const int64_t ex = block_excl_scan_1024((int64_t)tl * lay.words_per_L, &tot);
-        if (t < lay.MT) tileOff[t] = carry + ex;
-        carry += tot;
+        if (!lay.rgen) {
+            int64_t tot;
+            const int64_t ex = block_excl_scan_1024((int64_t)tl * lay.words_per_L, &tot);
+            if (t < lay.MT) tileOff[t] = carry + ex;
+            carry += tot;
+        }
     }
     // the first tile pair holds the batch entry's longest rows
     if (tid == 0 && lay.mbm == 2 * BM) atomicMax(status + 1, (uint32_t)round_up(length_at(0), MSTEP));
-    // The int8-chunk GEMM keeps, per cycle group, a table of A masked to each row length
-    // that ends inside the group: RSLOTS of them.  Rows are sorted, so the distinct lengths
-    // of a pair are the first rows of runs of equal length; a pair with more such lengths
-    // that are not multiples of 32 than tables makes the GEMM mask its fragments instead.
-    if (lay.rgen) {
-        // After the scatter hist[l] is the end of length l's run of sorted positions, and the
-        // run starts where the run of l + 1 ends.  Each length that is not a multiple of 32
-        // adds one to every pair its run meets (a difference array over pairs, then a scan).
-        const int npairs = lay.MT / 2;
-        __shared__ int dpair[2048 + 1];
-        for (int q0 = 0; q0 < npairs; q0 += 2048) {
-            const int nq = min(npairs - q0, 2048);
-            __syncthreads();
-            for (int q = tid; q <= nq; q += 1024) dpair[q] = 0;
-            __syncthreads();
-            for (int l = tid; l <= L_max; l += 1024) {
-                const int end = hist[l], start = l == L_max ? 0 : hist[l + 1];
-                if (l % 32 == 0 || end <= start) continue;
-                const int qa = max(start >> 8, q0), qb = min((end - 1) >> 8, q0 + nq - 1);
-                if (qa > qb) continue;
-                atomicAdd(&dpair[qa - q0], 1);
-                atomicAdd(&dpair[qb + 1 - q0], -1);
-            }
-            __syncthreads();
-            int64_t carry = 0;
-            bool over = false;
-            for (int c = 0; c < nq; c += 1024) {
-                const int q = c + tid;
-                int64_t tot;
-                const int64_t v = q < nq ? dpair[q] : 0;
-                const int64_t ex = block_excl_scan_1024(v, &tot);
-                over = over || (q < nq && carry + ex + v > lay.rslots);
-                carry += tot;
-            }
-            if (__syncthreads_or(over) && tid == 0) atomicOr(status + 2, 1u);
-        }
-    }
 }
 
 // Work division of the int8-chunk GEMM when row lengths vary (Layout::vsplit).  Tile t (pair
