@@ -12,6 +12,10 @@ against the dense fp4 MFMA peak.  ``valu_bitop_peak`` is the measured rate of th
 work done as packed words on the vector ALUs (AND + accumulating popcount, 2 instructions
 per 32 bit pairs: libscpeak), with the clock under that load; ``value`` is also given as a
 multiple of it.  ``cpu_baseline`` times the CPU oracle on a bounded row sample.
+
+Before the warm-up steps the call runs untimed until its time per call settles
+(``clock_settle`` in the line): the GPU raises its clock over tens of milliseconds of load,
+and the timed steps are meant to show the sustained rate.  ``--no-settle`` skips that.
 """
 import argparse
 import json
@@ -45,6 +49,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-valu-peak", action="store_true",
                    help="skip the VALU AND + popcount peak measurement")
+    p.add_argument("--no-settle", action="store_true",
+                   help="start the warm-up steps without first running the call until its time "
+                        "settles (the GPU's clock then still ramps up during the timed steps)")
     p.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                    help="only run a plain device copy of BYTES bytes (3 times), to calibrate "
                         "the HBM byte counters against a kernel of known traffic")
@@ -129,6 +136,7 @@ def main():
                      seed=g.seed, out=out, workspace=ws, stream=stream, prof_events=pe,
                      L_hint=int(round(float(g.L.mean()))), rng=rng)
 
+    settle = None if args.no_settle else settle_clock(step, stream)
     for _ in range(args.warmup):
         step()
     for k in range(len(staged)):
@@ -184,8 +192,42 @@ def main():
             "steps": nsteps, "warmup": args.warmup, "ms_per_step": ms_per_step,
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
             "dtype": "fp4", "data": "synthetic", "config": cfg, "roofline": roofline,
-            "valu_bitop_peak": valu, "cpu_baseline": cpu}
+            "valu_bitop_peak": valu, "cpu_baseline": cpu, "clock_settle": settle}
     print(json.dumps(line), flush=True)
+
+
+def settle_clock(step, stream, batch=10, min_s=0.1, max_s=3.0, tol=0.01):
+    """Run the call untimed until its time per call settles, before the warm-up steps.
+
+    Under sustained load the GPU raises its shader clock over tens of milliseconds (ViT-B fc1 at
+    L = 128 measured 0.58 ms per call after 5 warm-up calls, 0.50 ms after 100), so a short
+    benchmark would time the ramp rather than the sustained rate a continuously running
+    deployment sees.  Batches of `batch` calls run until two consecutive batches differ by less
+    than `tol` and at least `min_s` seconds have passed (at most `max_s`).  Returns what it did.
+    """
+    import torch
+    t_start = time.perf_counter()
+    first = prev = last = None
+    n = 0
+    while True:
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(batch):
+            step()
+        e1.record(stream)
+        e1.synchronize()
+        n += batch
+        last = e0.elapsed_time(e1) / batch
+        if first is None:
+            first = last
+        el = time.perf_counter() - t_start
+        if el >= max_s or (el >= min_s and prev is not None and abs(last - prev) <= tol * prev):
+            break
+        prev = last
+    return {"calls": n, "seconds": time.perf_counter() - t_start, "first_batch_ms_per_step": first,
+            "last_batch_ms_per_step": last,
+            "kind": "untimed calls before the warm-up steps, until the time per call settles"}
 
 
 def gemm_kernel_name(g, comparator):
