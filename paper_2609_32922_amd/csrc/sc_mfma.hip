@@ -432,7 +432,7 @@ __device__ __forceinline__ void d_stage(DecodeLds &d, const int32_t *perm, const
 template <bool BIP, int NT, int NQ, int TR, int TS>
 __device__ __forceinline__ void d_rows(const DecodeLds &d, const float *T, int row0, int tw, int b,
                                        const MGemmArgs &g, int tid) {
-    constexpr int RPW = NT / NQ, KQ = TR / RPW;
+    constexpr int RPW = NT / NQ, KQ = TR / RPW, KB = KQ < 8 ? KQ : 8;   // rows per thread, per batch
     const int cq = tid % NQ, r0 = tid / NQ;
     const int j0 = tw * 256 + 4 * cq;
     const int ncol = min(4, g.N - j0);
@@ -440,23 +440,26 @@ __device__ __forceinline__ void d_rows(const DecodeLds &d, const float *T, int r
     float sBj[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) sBj[c] = d.sB[4 * cq + (c < ncol ? c : 0)];
-    float4 v[KQ];
-    int row[KQ], len[KQ];
-    float f[KQ];
 #pragma unroll
-    for (int k = 0; k < KQ; ++k) {
-        const int rl = r0 + RPW * k;
-        v[k] = *reinterpret_cast<const float4 *>(&T[rl * TS + 4 * cq]);
-        row[k] = d.row[row0 + rl];
-        len[k] = d.len[row0 + rl];
-        f[k] = d.f[row0 + rl];
-    }
+    for (int k0 = 0; k0 < KQ; k0 += KB) {
+        float4 v[KB];
+        int row[KB], len[KB];
+        float f[KB];
 #pragma unroll
-    for (int k = 0; k < KQ; ++k) {
-        if (row[k] < 0) continue;
-        const float P[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
-        const int32_t none[4] = {0, 0, 0, 0};
-        decode4_store<BIP, false>(P, none, row[k], len[k], f[k], sBj, j0, ncol, b, g);
+        for (int k = 0; k < KB; ++k) {
+            const int rl = r0 + RPW * (k0 + k);
+            v[k] = *reinterpret_cast<const float4 *>(&T[rl * TS + 4 * cq]);
+            row[k] = d.row[row0 + rl];
+            len[k] = d.len[row0 + rl];
+            f[k] = d.f[row0 + rl];
+        }
+#pragma unroll
+        for (int k = 0; k < KB; ++k) {
+            if (row[k] < 0) continue;
+            const float P[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+            const int32_t none[4] = {0, 0, 0, 0};
+            decode4_store<BIP, false>(P, none, row[k], len[k], f[k], sBj, j0, ncol, b, g);
+        }
     }
 }
 
@@ -2082,22 +2085,22 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
         continue;
     }
     d_stage<NT>(dl, perm, Ls, b, tw, g, tid);
-    constexpr int TS = 256 + 4, TR = 32;
-    static_assert(TR * TS * 4 <= 256 * 16 * 16, "the epilogue transpose must fit the table");
+    // TR rows per pass: all that fit the table's LDS (64 KB, or 128 KB with the masked tables)
+    constexpr int TS = NARROW ? 64 + 4 : 256 + 4, TR = NARROW ? 128 : (TABLES ? 64 : 32);
+    static_assert(TR * TS * 4 <= (TABLES ? 2 : 1) * 256 * 16 * 16, "the epilogue transpose must fit the table");
     float *T = reinterpret_cast<float *>(lut);
     for (int h = 0; h < 256 / TR; ++h) {
         __syncthreads();
-        // rows 32h .. 32h + 31: block i of the waves of row half rh with r_row0(rh, i) = 32 h
-        if (rh == (SKIP ? (h >= 2 && h < 6 ? 1 : 0) : h >> 2)) {
+        // rows TR h .. TR h + TR - 1: the blocks i of each wave with r_row0(rh, i) among them
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                if (r_row0<SKIP>(rh, i) != 32 * h) continue;
+        for (int i = 0; i < 4; ++i) {
+            const int rr = r_row0<SKIP>(rh, i) - TR * h;
+            if (rr < 0 || rr >= TR) continue;
 #pragma unroll
-                for (int c = 0; c < NB; ++c)
+            for (int c = 0; c < NB; ++c)
 #pragma unroll
-                    for (int e = 0; e < 16; ++e)
-                        T[(8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] = acc[i][c][e];
-            }
+                for (int e = 0; e < 16; ++e)
+                    T[(rr + 8 * (e >> 2) + 4 * grp + (e & 3)) * TS + wc + 32 * c + i32] = acc[i][c][e];
         }
         __syncthreads();
         d_rows<BIP, NT, NARROW ? 16 : 64, TR, TS>(dl, T, TR * h, tw, b, g, tid);
