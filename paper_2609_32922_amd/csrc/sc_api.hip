@@ -230,9 +230,9 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
     l.off_units = off;
     int64_t pieces = quad ? (tiles - l.F) * (int64_t)l.S : tiles * (int64_t)l.S;
     if (l.vsplit) {
-        // (k_units adds at most 5 steps' cost per tile for its decode and a minimum step, and
+        // (k_units adds at most 7 steps' cost per tile for its decode and a minimum step, and
         // a range of T = ceil(W / sl) <= RSTEP_EXACT steps sums exactly)
-        const int64_t wmax = tiles * ((int64_t)l.KC * (l.LBS / 32) + 5);
+        const int64_t wmax = tiles * ((int64_t)l.KC * (l.LBS / 32) + 7);
         int64_t sl = l.q_slots;
         if (wmax > sl * (RSTEP_EXACT - 1)) sl = (wmax + RSTEP_EXACT - 2) / (RSTEP_EXACT - 1);
         if (sl > (1 << 20)) return false;

@@ -383,11 +383,11 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 // tp of batch entry b x B pair tw, in the GEMM's tile order: longest pairs first) runs w_t =
 // ceil(tileL / 32) x KC chunk steps (32-cycle groups x 32-element chunks; at least 1, so that
 // a tile of rows of length 0 still writes its zeros) and then decodes, which costs about E
-// steps (measured: 13.6 us against 3.6 us per step for 256 x 256 blocks, 6 against 2.7 for
-// 256 x 64).  Tile t's cost w_t + E is laid end to end with the others' and the total cut
-// into sk_slots ranges of T = ceil(W / sk_slots), range s for GEMM block s: every block gets
-// the same share of the sum of the row lengths (Sec. 4.1: the cost follows the sum of the
-// l_i) and of the decodes.  A tile inside one range runs whole and is decoded by its block; a
+// steps with its prologue (measured: 13.6 + 3.7 us against 3.6 us per step for 256 x 256
+// blocks, E = 5; 6 + 3.6 against 2.7 for 256 x 64, E = 3).  Tile t's cost w_t + E is laid end
+// to end with the others' and the total cut into sk_slots ranges of T = ceil(W / sk_slots),
+// range s for GEMM block s: every block gets the same share of the sum of the row lengths
+// (Sec. 4.1: the cost follows the sum of the l_i) and of the decodes.  A tile inside one range runs whole and is decoded by its block; a
 // tile that c cuts cross through its steps runs as c + 1 pieces, whose partial sums the
 // split-sum pass adds (a cut through the decode's share leaves the steps to one piece).
 // Written: units {tile, first step, end step, partial index or -1} in tile order, which is
@@ -397,7 +397,7 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *
     const int tid = threadIdx.x;
     const int NTW = lay.NT / 2, npairs = lay.MT / 2, slots = lay.sk_slots;
     const int tiles = batch * npairs * NTW;
-    const int64_t E = lay.narrow ? 2 : 4;
+    const int64_t E = lay.narrow ? 3 : 5;
     auto work = [&](int t) -> int64_t {
         const int tb = t / NTW, b = tb % batch, tp = tb / batch;
         const int L = ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_tileL)[2 * tp];
