@@ -71,8 +71,10 @@ extern "C" {
 enum {
     SC_OK = 0,
     SC_ERR_NULL = -1,          /* a required pointer is NULL */
-    SC_ERR_SHAPE = -2,         /* batch, M, N or K negative, K > SC_K_LIMIT, or
-                                  K * L_max > SC_KL_LIMIT */
+    SC_ERR_SHAPE = -2,         /* batch, M, N or K negative, K > SC_K_LIMIT,
+                                  K * L_max > SC_KL_LIMIT, or a problem whose workspace
+                                  layout exceeds its limits (size_t overflow, more than
+                                  2^20 work ranges); checked before the pointers */
     SC_ERR_LEN = -3,           /* L_max outside [1, SC_L_MAX_LIMIT] ([1, 256] for C-BSG),
                                   or L_hint outside [0, L_max] */
     SC_ERR_POLARITY = -4,      /* polarity not one of SC_BIPOLAR_XNOR / SC_UNIPOLAR_AND_SM */

@@ -300,13 +300,14 @@ static int check_call(const sc_gemm_desc *desc, const int8_t *A, const float *sA
     const int rc = check_desc(desc);
     if (rc != SC_OK) return rc;
     const sc_gemm_desc &d = *desc;
+    // a descriptor whose workspace cannot be laid out is refused as sc_gemm_workspace_size refuses it
+    if (!make_layout(d, device_cus(), lay)) return SC_ERR_SHAPE;
     // a pointer may be NULL only when the array it points to has no elements
     const bool anyM = d.batch > 0 && d.M > 0, anyN = d.batch > 0 && d.N > 0;
     if ((anyM && d.K > 0 && A == nullptr) || (anyN && d.K > 0 && B == nullptr) ||
         (anyM && (sA == nullptr || L_per_row == nullptr)) || (anyN && sB == nullptr) ||
         (anyM && anyN && out == nullptr))
         return SC_ERR_NULL;
-    if (!make_layout(d, device_cus(), lay)) return SC_ERR_SHAPE;
     return SC_OK;
 }
 
