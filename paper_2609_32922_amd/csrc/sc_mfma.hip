@@ -32,7 +32,9 @@
 //                 per 32-cycle group indexed by the int8 byte), so no planes exist and the
 //                 loop has no stage buffers; rows ending inside a group read tables masked
 //                 to their length (a second variant masks every fragment when a row pair
-//                 holds too many such lengths); for N <= 64 blocks of 256 x 64, two per CU.
+//                 holds too many such lengths); for N <= 64 blocks of 256 x 64, two per CU,
+//                 two waves on each row half splitting every chunk's k-steps (two waves per
+//                 SIMD).
 //                 A block copies each group's table entries into LDS (prefetched during
 //                 the previous group); a whole tile decodes from row and column data
 //                 staged in LDS, a part stores int32 partial sums
@@ -60,6 +62,7 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));   // one slot row: 32 nibbles
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
 
 constexpr uint32_t NIB_POS = 0x2u;   // e2m1 +1.0
 constexpr uint32_t NIB_NEG = 0xAu;   // e2m1 -1.0
@@ -1680,10 +1683,25 @@ __device__ __forceinline__ void r_fill_lut(u4 *lut, const u4 (&ent)[512 / NT], i
     }
 }
 
-// NB: B blocks of 32 columns per wave (4: 128 x 128 per wave; 2: 128 x 64, N <= 64)
+// NB: B blocks of 32 columns per wave.  NB = 4: a wave takes 128 x 128 and every k-step
+// of a chunk (16 elements of each of its lane's rows).  NB = 2 (N <= 64): a wave takes
+// 128 x 64 and half of each chunk's k-steps (8 elements of each row), two waves sharing the
+// rows, so that a SIMD runs two waves and one wave's waits overlap the other's MFMAs.
+template <int NB>
+struct RShape;
+template <>
+struct RShape<4> {
+    typedef u4 V;
+    static constexpr int KS = 16;   // k-steps per chunk per wave
+};
+template <>
+struct RShape<2> {
+    typedef u2 V;
+    static constexpr int KS = 8;
+};
 template <int NB>
 struct RData {
-    u4 a[4], b[NB];    // 16 elements of the lane's 4 A rows and NB B columns (one chunk)
+    typename RShape<NB>::V a[4], b[NB];   // the chunk's elements of the lane's 4 A rows and NB B columns
 };
 template <int NB>
 struct RFrags {
@@ -1715,12 +1733,21 @@ __device__ __forceinline__ int r_row0(int rh, int i) { return SKIP ? 32 * r_bloc
 
 template <int NB>
 __device__ __forceinline__ void r_load(const RSrc &q, int c, RData<NB> &d) {
+    if constexpr (NB == 2) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-        d.a[i] = __builtin_amdgcn_raw_buffer_load_b128(q.a, q.voffA, c * 256 * RCH + q.boffA[i], 0);
+        for (int i = 0; i < 4; ++i)
+            d.a[i] = __builtin_amdgcn_raw_buffer_load_b64(q.a, q.voffA, c * 256 * RCH + q.boffA[i], 0);
 #pragma unroll
-    for (int i = 0; i < NB; ++i)
-        d.b[i] = __builtin_amdgcn_raw_buffer_load_b128(q.b, q.voffB, c * 256 * RCH + i * 32 * RCH, 0);
+        for (int i = 0; i < NB; ++i)
+            d.b[i] = __builtin_amdgcn_raw_buffer_load_b64(q.b, q.voffB, c * 256 * RCH + i * 32 * RCH, 0);
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            d.a[i] = __builtin_amdgcn_raw_buffer_load_b128(q.a, q.voffA, c * 256 * RCH + q.boffA[i], 0);
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+            d.b[i] = __builtin_amdgcn_raw_buffer_load_b128(q.b, q.voffB, c * 256 * RCH + i * 32 * RCH, 0);
+    }
 }
 
 // rows that have ended before this cycle group read the padding byte, whose table row is zero
@@ -1728,18 +1755,18 @@ template <int NB>
 __device__ __forceinline__ void r_finish(RData<NB> &d, const bool (&fin)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        if (fin[i]) d.a[i] = u4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
+        if (fin[i]) d.a[i] = 0x80808080u;
 }
 
-// the table row of element E (0..15) of a lane's 16: address byte 1 = the element's byte,
-// bytes 0 and 2 = the copy and the region (from lo)
+// the table row of element E of the lane's elements (0..15, or 0..7 with NB = 2): address
+// byte 1 = the element's byte, bytes 0 and 2 = the copy and the region (from lo)
 template <int E>
 __device__ __forceinline__ u4 r_look(const RSrc &q, uint32_t word, uint32_t lo) {
     constexpr uint32_t sel = 0x0C020000u | ((4u + (E & 3)) << 8);
     return *reinterpret_cast<const u4 *>(q.lut + __builtin_amdgcn_perm(word, lo, sel));
 }
-template <int E>
-__device__ __forceinline__ uint32_t r_word(const u4 &v) {
+template <int E, typename V>
+__device__ __forceinline__ uint32_t r_word(const V &v) {
     return v[E >> 2];
 }
 
@@ -1780,6 +1807,7 @@ __device__ __forceinline__ void r_frags_h(const RSrc &q, const RData<NB> &d, con
 
 // Stage S (k-steps 2S, 2S+1) of a chunk: fragment set 0 holds k-step 2S on entry and the
 // next k-step (2S + 2, or the next chunk's first) on exit; stage 0 loads the next chunk.
+// A chunk has KS / 2 stages (RShape).
 // MASK: the A fragments are masked with the rows' lengths (some row of the pair ends
 // inside a cycle group); else rows that have ended read the padding byte (r_finish).
 template <int NB>
@@ -1825,7 +1853,7 @@ __device__ __forceinline__ void r_stage(const RSrc &q, int cnext, RData<NB> &cur
     if (MASK) r_mask(m, f[1]);
     q_mma_half(acc, f[0], 1);
     r_quarter_masks<MASK, NB>();
-    if (S < 7) {
+    if (S < RShape<NB>::KS / 2 - 1) {
         r_frags<2 * S + 2, false>(q, cur, m, f[0]);
     } else {
         if (!MASK) r_finish(nxt, fin);
@@ -1847,7 +1875,7 @@ __device__ __forceinline__ void r_stage_h(const RSrc &q, int cnext, RData<NB> &c
     if (S == 0) r_load(q, cnext, nxt);
     r_frags_h<2 * S + 1, MASK>(q, cur, m, f[1]);
     q_mma_half(acc, f[0], 0);
-    if (S < 7) {
+    if (S < RShape<NB>::KS / 2 - 1) {
         r_frags_h<2 * S + 2, MASK>(q, cur, m, f[0]);
     } else {
         if (!MASK) r_finish(nxt, fin);
@@ -1866,10 +1894,12 @@ __device__ __forceinline__ void r_chunks_h(const RSrc &q, int c, int ce, RData<N
         r_stage_h<1, MASK>(q, x, cur, nxt, m, fin, acc, f);
         r_stage_h<2, MASK>(q, x, cur, nxt, m, fin, acc, f);
         r_stage_h<3, MASK>(q, x, cur, nxt, m, fin, acc, f);
-        r_stage_h<4, MASK>(q, x, cur, nxt, m, fin, acc, f);
-        r_stage_h<5, MASK>(q, x, cur, nxt, m, fin, acc, f);
-        r_stage_h<6, MASK>(q, x, cur, nxt, m, fin, acc, f);
-        r_stage_h<7, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        if constexpr (RShape<NB>::KS == 16) {
+            r_stage_h<4, MASK>(q, x, cur, nxt, m, fin, acc, f);
+            r_stage_h<5, MASK>(q, x, cur, nxt, m, fin, acc, f);
+            r_stage_h<6, MASK>(q, x, cur, nxt, m, fin, acc, f);
+            r_stage_h<7, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        }
         cur = nxt;
     }
 }
@@ -1886,10 +1916,12 @@ __device__ __forceinline__ void r_chunks(const RSrc &q, int c, int ce, RData<NB>
         r_stage<1, MASK>(q, x, cur, nxt, m, fin, acc, f);
         r_stage<2, MASK>(q, x, cur, nxt, m, fin, acc, f);
         r_stage<3, MASK>(q, x, cur, nxt, m, fin, acc, f);
-        r_stage<4, MASK>(q, x, cur, nxt, m, fin, acc, f);
-        r_stage<5, MASK>(q, x, cur, nxt, m, fin, acc, f);
-        r_stage<6, MASK>(q, x, cur, nxt, m, fin, acc, f);
-        r_stage<7, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        if constexpr (RShape<NB>::KS == 16) {
+            r_stage<4, MASK>(q, x, cur, nxt, m, fin, acc, f);
+            r_stage<5, MASK>(q, x, cur, nxt, m, fin, acc, f);
+            r_stage<6, MASK>(q, x, cur, nxt, m, fin, acc, f);
+            r_stage<7, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        }
         cur = nxt;
     }
 }
@@ -1900,13 +1932,13 @@ __device__ __forceinline__ void r_chunks(const RSrc &q, int c, int ce, RData<NB>
 // cycle group reads there the table masked to its length.  Both variants are launched and
 // one returns at once: MASK runs when some row pair holds more lengths inside a group than
 // there are masked tables (then every A fragment is masked with its row's length instead).
-// NARROW (N <= 64): a block of 2 waves takes the pair's 256 rows x the first 64 columns of
-// the B pair, two blocks per CU; it has no masked tables (every length inside a group makes
-// the call take the MASK variant).
+// NARROW (N <= 64): a block takes the pair's 256 rows x the first 64 columns of the B pair,
+// two blocks per CU: wave (rh, kh) the rows of half rh and k-steps kh of every chunk, so that
+// each SIMD runs two waves; the two k-halves are summed through the LDS at the end.  It has no
+// masked tables (every length inside a group makes the call take the MASK variant).
 template <bool BIP, bool MASK, bool NARROW>
-__global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MGemmArgs g, Layout lay,
-                                                                          uint8_t *ws) {
-    constexpr int NT = NARROW ? 128 : 256;            // threads
+__global__ __launch_bounds__(256, NARROW ? 2 : 1) void k_rgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
+    constexpr int NT = 256;                           // threads
     constexpr int NB = NARROW ? 2 : 4;                // B blocks of 32 columns per wave
     constexpr bool TABLES = !MASK && !NARROW;         // tables masked to row lengths
     constexpr bool SKIP = NARROW;                     // skip the MFMAs of blocks whose rows ended
@@ -1948,7 +1980,8 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     asm volatile("" : "+v"(tid));
     const int lane = tid & 63, w = tid >> 6;
     const int grp = lane >> 5, i32 = lane & 31;
-    const int rh = NARROW ? w : (w >> 1), wc = NARROW ? 0 : (w & 1) * 128;   // row half, columns
+    const int rh = NARROW ? (w & 1) : (w >> 1), wc = NARROW ? 0 : (w & 1) * 128;   // row half, columns
+    const int kh = NARROW ? (w >> 1) : 0;                                          // k-half (NARROW)
     uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
     uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
     const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm) + tp * 256;
@@ -1959,10 +1992,10 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
                                             0x00020000);
     q.b = __builtin_amdgcn_make_buffer_rsrc(ws_ptr<uint8_t>(wsbB, lay.off_Bp) + (size_t)tw * pairb, 0, (int)pairb,
                                             0x00020000);
-    q.voffA = ((SKIP ? 0 : 128 * rh) + i32) * RCH + grp * 16;
+    q.voffA = ((SKIP ? 0 : 128 * rh) + i32) * RCH + grp * 16 + kh * 8;
 #pragma unroll
     for (int i = 0; i < 4; ++i) q.boffA[i] = (SKIP ? 32 * r_block(rh, i) : 32 * i) * RCH;
-    q.voffB = (wc + i32) * RCH + grp * 16;
+    q.voffB = (wc + i32) * RCH + grp * 16 + kh * 8;
     q.KC = g.KC > 0 ? g.KC : 1;
     // A unit of the 256 x 256 blocks that knows its first chunk step before its tile's length
     // (whole tiles, and the units of the ranges division) loads that step's table entries and
@@ -2080,8 +2113,40 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
         x = xe;
     }
 
+    if (NARROW) {
+        // the k-half 1 waves hand their sums to the k-half 0 waves of the same rows
+        __syncthreads();   // (every read of the table is done)
+        float4 *F = reinterpret_cast<float4 *>(lut) + rh * (4 * NB * 4 * 64);
+        if (kh == 1) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int c = 0; c < NB; ++c)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        F[((i * NB + c) * 4 + e) * 64 + lane] =
+                            float4{acc[i][c][4 * e], acc[i][c][4 * e + 1], acc[i][c][4 * e + 2], acc[i][c][4 * e + 3]};
+        }
+        __syncthreads();
+        if (kh == 0) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int c = 0; c < NB; ++c)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float4 t = F[((i * NB + c) * 4 + e) * 64 + lane];
+                        acc[i][c][4 * e] += t.x;
+                        acc[i][c][4 * e + 1] += t.y;
+                        acc[i][c][4 * e + 2] += t.z;
+                        acc[i][c][4 * e + 3] += t.w;
+                    }
+        }
+    }
     if (split) {
-        store_part_r<SKIP, NB>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * lay.pcols, rh, wc, lane);
+        if (kh == 0)
+            store_part_r<SKIP, NB>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * lay.pcols, rh, wc,
+                                   lane);
         continue;
     }
     d_stage<NT>(dl, perm, Ls, b, tw, g, tid);
@@ -2092,10 +2157,11 @@ __global__ __launch_bounds__(NARROW ? 128 : 256, NARROW ? 2 : 1) void k_rgemm(MG
     for (int h = 0; h < 256 / TR; ++h) {
         __syncthreads();
         // rows TR h .. TR h + TR - 1: the blocks i of each wave with r_row0(rh, i) among them
+        // (NARROW: the k-half 0 waves, which hold the sums)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int rr = r_row0<SKIP>(rh, i) - TR * h;
-            if (rr < 0 || rr >= TR) continue;
+            if (rr < 0 || rr >= TR || kh != 0) continue;
 #pragma unroll
             for (int c = 0; c < NB; ++c)
 #pragma unroll
@@ -2113,7 +2179,7 @@ static hipError_t launch_rgemm_w(const MGemmArgs &g, const Layout &lay, uint8_t 
     const unsigned tiles = (unsigned)(g.batch * (lay.MT / 2) * (lay.NT / 2));
     const unsigned tail = tiles - (unsigned)g.F;
     const dim3 grid(lay.vsplit ? (unsigned)lay.sk_slots : (unsigned)g.F + tail * (unsigned)g.S),
-        block(NARROW ? 128 : 256);
+        block(256);
     hipLaunchKernelGGL((k_rgemm<BIP, false, NARROW>), grid, block, 0, st, g, lay, ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
