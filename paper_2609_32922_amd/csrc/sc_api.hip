@@ -230,11 +230,14 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
     l.off_units = off;
     int64_t pieces = quad ? (tiles - l.F) * (int64_t)l.S : tiles * (int64_t)l.S;
     if (l.vsplit) {
-        // (k_units adds at most 7 steps' cost per tile for its decode and a minimum step, and
-        // a range of T = ceil(W / sl) <= RSTEP_EXACT steps sums exactly)
+        // (k_units weighs a step w1 or w2 and adds at most 7 w1 per tile for its decode and a
+        // minimum step: W <= w1 wmax.  A range of cost T = ceil(W / sl) <= w1 wmax / sl + 1
+        // holds at most T / w2 + 1 steps, which must stay below RSTEP_EXACT to sum exactly.)
+        const int64_t w1 = l.narrow ? RW1_NARROW : 1, w2 = l.narrow ? RW2_NARROW : 1;
         const int64_t wmax = tiles * ((int64_t)l.KC * (l.LBS / 32) + 7);
+        const int64_t den = w2 * (RSTEP_EXACT - 2) - 1;
         int64_t sl = l.q_slots;
-        if (wmax > sl * (RSTEP_EXACT - 1)) sl = (wmax + RSTEP_EXACT - 2) / (RSTEP_EXACT - 1);
+        if (w1 * wmax > sl * den) sl = (w1 * wmax + den - 1) / den;
         if (sl > (1 << 20)) return false;
         l.sk_slots = (int)sl;
         l.F = 0;

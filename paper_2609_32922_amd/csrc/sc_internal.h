@@ -89,6 +89,10 @@ constexpr int RSLOTS = 4;        // int8-chunk GEMM: tables masked to a row leng
 constexpr int64_t MFMA_EXACT = 1ll << 24;   // products one fp32 accumulator sums exactly
 constexpr int64_t RSTEP_EXACT = MFMA_EXACT / (32 * 32);   // int8-chunk GEMM chunk steps (32 cycles x
                                                           // 32 elements) one accumulator sums exactly
+// Cost of a chunk step of the 256 x 64 int8-chunk GEMM in the work division, while all of a
+// wave's row blocks run (RW1) and once only the first two do (RW2): half the MFMAs and two
+// thirds of the table reads; the 256 x 256 blocks weigh every step 1
+constexpr int64_t RW1_NARROW = 8, RW2_NARROW = 5;
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 

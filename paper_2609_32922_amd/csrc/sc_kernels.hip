@@ -380,34 +380,57 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 }
 
 // Work division of the int8-chunk GEMM when row lengths vary (Layout::vsplit).  Tile t (pair
-// tp of batch entry b x B pair tw, in the GEMM's tile order: longest pairs first) runs w_t =
-// ceil(tileL / 32) x KC chunk steps (32-cycle groups x 32-element chunks; at least 1, so that
-// a tile of rows of length 0 still writes its zeros) and then decodes, which costs about E
-// steps with its prologue (measured: 13.6 + 3.7 us against 3.6 us per step for 256 x 256
-// blocks, E = 5; 6 + 3.6 against 2.7 for 256 x 64, E = 3).  Tile t's cost w_t + E is laid end
-// to end with the others' and the total cut into sk_slots ranges of T = ceil(W / sk_slots),
-// range s for GEMM block s: every block gets the same share of the sum of the row lengths
-// (Sec. 4.1: the cost follows the sum of the l_i) and of the decodes.  A tile inside one range runs whole and is decoded by its block; a
-// tile that c cuts cross through its steps runs as c + 1 pieces, whose partial sums the
-// split-sum pass adds (a cut through the decode's share leaves the steps to one piece).
-// Written: units {tile, first step, end step, partial index or -1} in tile order, which is
-// range order; slot[s] = the first unit of range s (slot[sk_slots] = the unit count);
-// tinfo[t] = {pieces, partial index of piece 0}.  One block.
+// tp of batch entry b x B pair tw, in the GEMM's tile order: longest pairs first) runs
+// ceil(tileL / 32) x KC chunk steps (32-cycle groups x 32-element chunks) and then decodes.
+// Its cost, in units of the time of one step: W1 per step while every row block of the
+// block runs, W2 per step once the 256 x 64 blocks run only the first half of each wave's
+// row blocks (from the group where sorted row 128 of the pair has ended: rows are sorted by
+// length, and the blocks {2, 3} and {6, 7} of the waves' row halves hold rows 128 .. 255),
+// at least 1 (a tile of rows of length 0 still writes its zeros), plus E for its decode and
+// prologue (measured: 13.6 + 3.7 us against 3.6 us per step for 256 x 256 blocks, E = 5
+// steps; about 3 steps for 256 x 64).  The tiles' costs are laid end to end and the total
+// cut into sk_slots ranges of T = ceil(W / sk_slots), range s for GEMM block s: every block
+// gets the same share of the MFMA work, which follows the sum of the row lengths (Sec. 4.1),
+// and of the decodes.  A tile inside one range runs whole and is decoded by its block; a
+// tile that c cuts cross through its steps runs as c + 1 pieces (a cut maps to the first
+// step whose cost ends after it), whose partial sums the split-sum pass adds (a cut through
+// the decode's share leaves the steps to one piece).  Written: units {tile, first step, end
+// step, partial index or -1} in tile order, which is range order; slot[s] = the first unit
+// of range s (slot[sk_slots] = the unit count); tinfo[t] = {pieces, partial index of piece
+// 0}.  One block.
 __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *ws) {
     const int tid = threadIdx.x;
     const int NTW = lay.NT / 2, npairs = lay.MT / 2, slots = lay.sk_slots;
     const int tiles = batch * npairs * NTW;
-    const int64_t E = lay.narrow ? 3 : 5;
-    auto work = [&](int t) -> int64_t {
+    const int64_t W1 = lay.narrow ? RW1_NARROW : 1, W2 = lay.narrow ? RW2_NARROW : 1;
+    const int64_t E = lay.narrow ? 3 * W1 : 5 * W1;
+    // tile t's steps at weight W1 and at weight W2
+    auto steps = [&](int t) -> int2 {
         const int tb = t / NTW, b = tb % batch, tp = tb / batch;
-        const int L = ws_ptr<int32_t>(ws + (size_t)b * lay.stride_batchA, lay.off_tileL)[2 * tp];
-        const int64_t w = (int64_t)((L + 31) / 32) * lay.KC;
-        return w > 0 ? w : 1;
+        uint8_t *wsb = ws + (size_t)b * lay.stride_batchA;
+        const int g0 = (ws_ptr<int32_t>(wsb, lay.off_tileL)[2 * tp] + 31) / 32;
+        int g1 = g0;
+        if (lay.narrow) {
+            const int r = tp * 256 + 128;
+            const int L1 = ws_ptr<int32_t>(wsb, lay.off_perm)[r] >= 0
+                               ? ws_ptr<int32_t>(wsb, lay.off_Ls)[r]
+                               : 0;
+            g1 = min((L1 + 31) / 32, g0);
+        }
+        return make_int2(g1 * lay.KC, (g0 - g1) * lay.KC);
+    };
+    auto cost = [&](int2 n) -> int64_t {
+        const int64_t c = (int64_t)n.x * W1 + (int64_t)n.y * W2;
+        return c > 0 ? c : 1;
+    };
+    // the steps whose cost ends at or before c (0 <= c <= cost(n); c = cost(n): every step)
+    auto step_at = [&](int2 n, int64_t c) -> int64_t {
+        return c < (int64_t)n.x * W1 ? c / W1 : n.x + (c - (int64_t)n.x * W1) / W2;
     };
     int64_t W = 0;
     for (int c = 0; c < tiles; c += 1024) {
         int64_t tot;
-        block_excl_scan_1024(c + tid < tiles ? work(c + tid) + E : 0, &tot);
+        block_excl_scan_1024(c + tid < tiles ? cost(steps(c + tid)) + E : 0, &tot);
         W += tot;
     }
     const int64_t T = (W + slots - 1) / slots;
@@ -417,7 +440,8 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *
     int64_t ccarry = 0, ucarry = 0, pcarry = 0;
     for (int c = 0; c < tiles; c += 1024) {
         const int t = c + tid;
-        const int64_t w = t < tiles ? work(t) : 0, cw = t < tiles ? w + E : 0;
+        const int2 n = t < tiles ? steps(t) : make_int2(0, 0);
+        const int64_t w = t < tiles ? cost(n) : 0, cw = t < tiles ? w + E : 0;
         int64_t ctot, utot, ptot;
         const int64_t C = ccarry + block_excl_scan_1024(cw, &ctot);
         // ranges meeting the tile's cost; the last one starts inside the decode's share when
@@ -431,7 +455,9 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *
             for (int p = 0; p < nr; ++p) {
                 const int64_t s0 = C / T + p;
                 const int64_t a = p == 0 ? C : s0 * T, e = p == np - 1 ? C + w : (s0 + 1) * T;
-                if (p < np) units[U + p] = make_int4(t, (int)(a - C), (int)(e - C), np > 1 ? (int)(P + p) : -1);
+                if (p < np)
+                    units[U + p] = make_int4(t, (int)step_at(n, a - C), (int)step_at(n, e - C),
+                                             np > 1 ? (int)(P + p) : -1);
                 // (a range starting inside the decode's share starts with the next tile's first unit)
                 if (a % T == 0) slot[a / T] = (uint32_t)(U + p);
             }

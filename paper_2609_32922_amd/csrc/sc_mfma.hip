@@ -1867,21 +1867,31 @@ __device__ __forceinline__ void r_stage(const RSrc &q, int cnext, RData<NB> &cur
 }
 
 // Stage S when only the first two A blocks of the wave run: half the MFMAs, two A table
-// reads per k-step instead of four
+// reads per k-step instead of four.  The reads of the next fragments go with the k-step's
+// MFMAs and their length masks (MASK) after them, right before the MFMAs that use them.
+template <int NB>
+__device__ __forceinline__ void r_mask_h(const u4 (&m)[4], RFrags<NB> &f) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) f.a[i] &= m[i];
+}
 template <int S, bool MASK, int NB>
 __device__ __forceinline__ void r_stage_h(const RSrc &q, int cnext, RData<NB> &cur, RData<NB> &nxt,
                                           const u4 (&m)[4], const bool (&fin)[4], v16f (&acc)[4][NB],
                                           RFrags<NB> (&f)[2]) {
     if (S == 0) r_load(q, cnext, nxt);
-    r_frags_h<2 * S + 1, MASK>(q, cur, m, f[1]);
+    r_frags_h<2 * S + 1, false>(q, cur, m, f[1]);
     q_mma_half(acc, f[0], 0);
+    r_quarter_reads<S == 0, NB>();
+    if (MASK) r_mask_h(m, f[1]);
     if (S < RShape<NB>::KS / 2 - 1) {
-        r_frags_h<2 * S + 2, MASK>(q, cur, m, f[0]);
+        r_frags_h<2 * S + 2, false>(q, cur, m, f[0]);
     } else {
         if (!MASK) r_finish(nxt, fin);
-        r_frags_h<0, MASK>(q, nxt, m, f[0]);
+        r_frags_h<0, false>(q, nxt, m, f[0]);
     }
     q_mma_half(acc, f[1], 0);
+    r_quarter_reads<false, NB>();
+    if (MASK) r_mask_h(m, f[0]);
 }
 
 template <bool MASK, int NB>
@@ -1994,7 +2004,7 @@ __global__ __launch_bounds__(256, NARROW ? 2 : 1) void k_rgemm(MGemmArgs g, Layo
                                             0x00020000);
     q.voffA = ((SKIP ? 0 : 128 * rh) + i32) * RCH + grp * 16 + kh * 8;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) q.boffA[i] = (SKIP ? 32 * r_block(rh, i) : 32 * i) * RCH;
+    for (int i = 0; i < 4; ++i) q.boffA[i] = wave_uniform((SKIP ? 32 * r_block(rh, i) : 32 * i) * RCH);
     q.voffB = (wc + i32) * RCH + grp * 16 + kh * 8;
     q.KC = g.KC > 0 ? g.KC : 1;
     // A unit of the 256 x 256 blocks that knows its first chunk step before its tile's length
