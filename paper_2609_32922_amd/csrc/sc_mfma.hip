@@ -1939,23 +1939,33 @@ __device__ __forceinline__ void r_chunks(const RSrc &q, int c, int ce, RData<NB>
 // One work unit, as in k_qgemm: tile `tile` over chunk steps [s, s + 1) / S of the pair's
 // (group, chunk) steps, whole tiles decoded here, parts stored as partial sums.  Rows that
 // have ended read the padding byte, whose table row is zero; a row that ends inside a
-// cycle group reads there the table masked to its length.  Both variants are launched and
-// one returns at once: MASK runs when some row pair holds more lengths inside a group than
-// there are masked tables (then every A fragment is masked with its row's length instead).
+// cycle group reads there the table masked to its length.  MASK runs when some row pair
+// holds more lengths inside a group than there are masked tables (then every A fragment is
+// masked with its row's length instead): the 256 x 256 blocks launch both variants and one
+// returns at once, the 256 x 64 blocks take the variant per block in one launch.
 // NARROW (N <= 64): a block takes the pair's 256 rows x the first 64 columns of the B pair,
 // two blocks per CU: wave (rh, kh) the rows of half rh and k-steps kh of every chunk, so that
 // each SIMD runs two waves; the two k-halves are summed through the LDS at the end.  It has no
 // masked tables (every length inside a group makes the call take the MASK variant).
-template <bool BIP, bool MASK, bool NARROW>
-__global__ __launch_bounds__(256, NARROW ? 2 : 1) void k_rgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
+// The LDS of a GEMM block: the group's table (64 KB, or 128 KB with the masked tables; the
+// epilogue's transpose reuses it), bit r of rems[G]: a row ends r cycles into group G, and
+// what the decode needs (filled after the chunk loop)
+template <bool TABLES>
+struct RLds {
+    u4 lut[(TABLES ? 2 : 1) * 256 * 16];
+    uint32_t rems[TABLES ? RGROUPS : 1];
+    DecodeLds dl;
+};
+
+template <bool BIP, bool MASK, bool NARROW, bool TABLES>
+__device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay, uint8_t *ws, RLds<TABLES> &sh) {
     constexpr int NT = 256;                           // threads
     constexpr int NB = NARROW ? 2 : 4;                // B blocks of 32 columns per wave
-    constexpr bool TABLES = !MASK && !NARROW;         // tables masked to row lengths
     constexpr bool SKIP = NARROW;                     // skip the MFMAs of blocks whose rows ended
-    __shared__ u4 lut[(TABLES ? 2 : 1) * 256 * 16];   // 64 or 128 KB; the epilogue's transpose reuses it
-    __shared__ uint32_t rems[TABLES ? RGROUPS : 1];   // bit r of rems[G]: a row ends r cycles into group G
-    __shared__ DecodeLds dl;                          // filled after the chunk loop
-    if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
+    static_assert(TABLES == (!MASK && !NARROW), "masked tables: the 256 x 256 variant without MASK");
+    u4 *lut = sh.lut;
+    uint32_t *rems = sh.rems;
+    DecodeLds &dl = sh.dl;
     const int NTW = lay.NT / 2;
     // the block's units: one, or with vsplit its range of the work (k_units)
     int ub = blockIdx.x, ue = blockIdx.x + 1;
@@ -2184,16 +2194,37 @@ __global__ __launch_bounds__(256, NARROW ? 2 : 1) void k_rgemm(MGemmArgs g, Layo
     }
 }
 
+// 256 x 256 blocks: both variants are launched and one returns at once
+template <bool BIP, bool MASK>
+__global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
+    __shared__ RLds<!MASK> sh;
+    if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
+    rgemm_body<BIP, MASK, false, !MASK>(g, lay, ws, sh);
+}
+
+// 256 x 64 blocks: one launch, each block takes the variant the status word names
+template <bool BIP>
+__global__ __launch_bounds__(256, 2) void k_rgemm_n(MGemmArgs g, Layout lay, uint8_t *ws) {
+    __shared__ RLds<false> sh;
+    if (ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) rgemm_body<BIP, true, true, false>(g, lay, ws, sh);
+    else rgemm_body<BIP, false, true, false>(g, lay, ws, sh);
+}
+
 template <bool BIP, bool NARROW>
 static hipError_t launch_rgemm_w(const MGemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
     const unsigned tiles = (unsigned)(g.batch * (lay.MT / 2) * (lay.NT / 2));
     const unsigned tail = tiles - (unsigned)g.F;
     const dim3 grid(lay.vsplit ? (unsigned)lay.sk_slots : (unsigned)g.F + tail * (unsigned)g.S),
         block(256);
-    hipLaunchKernelGGL((k_rgemm<BIP, false, NARROW>), grid, block, 0, st, g, lay, ws);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_rgemm<BIP, true, NARROW>), grid, block, 0, st, g, lay, ws);
+    hipError_t e;
+    if (NARROW) {
+        hipLaunchKernelGGL((k_rgemm_n<BIP>), grid, block, 0, st, g, lay, ws);
+    } else {
+        hipLaunchKernelGGL((k_rgemm<BIP, false>), grid, block, 0, st, g, lay, ws);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_rgemm<BIP, true>), grid, block, 0, st, g, lay, ws);
+    }
     e = hipGetLastError();
     if (e != hipSuccess || tail == 0) return e;
     return launch_qreduce<BIP>(g, lay, ws, tail, st);
