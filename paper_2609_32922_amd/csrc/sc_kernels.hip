@@ -207,6 +207,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     __shared__ int hist[SC_L_MAX_LIMIT + 1];
     __shared__ int hstart[SC_L_MAX_LIMIT + 1];
     __shared__ int dpair[2048 + 1];
+    __shared__ int lmin, lmax;
     const int b = blockIdx.x, tid = threadIdx.x;
     uint8_t *wsb = ws + (size_t)b * lay.stride_batchA;
     int32_t *perm = ws_ptr<int32_t>(wsb, lay.off_perm);
@@ -244,16 +245,61 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         }
     }
     for (int v = tid; v <= L_max; v += 1024) hist[v] = 0;
+    if (tid == 0) {
+        lmin = INT_MAX;
+        lmax = INT_MIN;
+    }
     __syncthreads();
+    // the lengths held in registers: validated, and their range over the batch entry
     if (cached) {
+        int lo = INT_MAX, hi = INT_MIN;
 #pragma unroll
         for (int k = 0; k < SREG; ++k) {
             if (lv[k] < 0 || lv[k] > L_max) {
                 atomicOr(status, STATUS_BAD_LENGTH);
                 lv[k] = 0;
             }
-            if (k * 1024 < M) wave_bucket_add(hist, lv[k], k * 1024 + tid < M);
+            if (k * 1024 + tid < M) {
+                lo = min(lo, lv[k]);
+                hi = max(hi, lv[k]);
+            }
         }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            lo = min(lo, __shfl_xor(lo, o, 64));
+            hi = max(hi, __shfl_xor(hi, o, 64));
+        }
+        if ((tid & 63) == 0) {
+            atomicMin(&lmin, lo);
+            atomicMax(&lmax, hi);
+        }
+        __syncthreads();
+    }
+    // One length for every row (M > 0): the sort keeps the row order, and the counts below
+    // are set directly.
+    const bool one = cached && M > 0 && lmin == lmax;
+    if (one) {
+        const int l = lmin;
+        // as after the scatter of the general path: hist[v] = end and hstart[v] = start of
+        // length v's run of sorted positions (lengths above l: empty runs at 0, below: at M)
+        for (int v = tid; v <= L_max; v += 1024) {
+            hist[v] = v <= l ? M : 0;
+            hstart[v] = v < l ? M : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < SREG; ++k) {
+            const int i = k * 1024 + tid;
+            if (i < M) {
+                perm[i] = i;
+                Ls[i] = l;
+            }
+        }
+        // every pair meets one length; it is not a multiple of 32 only when l is not
+        if (tid == 0 && lay.rgen && l % 32 != 0 && lay.rslots < 1) atomicOr(status + 2, 1u);
+    } else if (cached) {
+#pragma unroll
+        for (int k = 0; k < SREG; ++k)
+            if (k * 1024 < M) wave_bucket_add(hist, lv[k], k * 1024 + tid < M);
     } else {
         for (int i0 = 0; i0 < M; i0 += 1024) {
             const int i = i0 + tid;
@@ -269,7 +315,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     // start position of each length bucket, longest lengths first (also kept in hstart: the
     // scatter below moves hist[l] on to the end of l's run)
     int64_t carry = 0;
-    for (int c = 0; c <= L_max; c += 1024) {
+    for (int c = 0; !one && c <= L_max; c += 1024) {
         const int idx = L_max - (c + tid);
         const int64_t v = idx >= 0 ? hist[idx] : 0;
         int64_t tot;
@@ -281,7 +327,9 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
         carry += tot;
         __syncthreads();
     }
-    if (cached) {
+    if (one) {
+        // (done above)
+    } else if (cached) {
 #pragma unroll
         for (int k = 0; k < SREG; ++k) {
             const int i = k * 1024 + tid;
@@ -315,7 +363,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
     // Each such length adds one to every pair its run [hstart[l], end) meets (a difference
     // array over pairs, then a scan); end = hstart[l - 1] (runs in order of decreasing
     // length), or M.  (Up to 2048 pairs per pass; the first pass runs beside the scatter.)
-    const int npairs = lay.rgen ? lay.MT / 2 : 0;
+    const int npairs = lay.rgen && !one ? lay.MT / 2 : 0;
     for (int q0 = 0; q0 < npairs; q0 += 2048) {
         const int nq = min(npairs - q0, 2048);
         if (q0 > 0) __syncthreads();

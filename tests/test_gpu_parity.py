@@ -213,6 +213,11 @@ RGEN = [
     (2, 300, 64, 64, 256, "uniform", 0, True, 73),     # the compensator's shape class
     (3, 577, 17, 200, 130, "random", 1, False, 75),    # attention-like, ragged N
     (1, 129, 1, 5, 96, "mult32", 0, False, 77),        # one column, K < 32, rows ending at bounds
+    # one length per batch entry (the scheduler keeps the row order): inside a group with
+    # 64-column blocks (every fragment masked), all rows of length 0, and per-entry lengths
+    (2, 400, 48, 70, 90, "uniform", 1, False, 79),
+    (1, 300, 300, 40, 64, "zero", 0, False, 81),
+    (3, 600, 260, 96, 160, "per_entry", 0, True, 83),
 ]
 
 
@@ -224,6 +229,10 @@ def _rgen_gemm(case):
         g.L = (rng.integers(0, L_max // 32 + 1, g.L.shape) * 32).astype(np.int32)
     elif kind == "uniform":
         g.L = np.full(g.L.shape, L_max, np.int32)
+    elif kind == "zero":
+        g.L = np.zeros(g.L.shape, np.int32)
+    elif kind == "per_entry":
+        g.L = np.repeat(rng.integers(1, L_max + 1, (g.L.shape[0], 1)), g.L.shape[1], axis=1).astype(np.int32)
     return g
 
 
