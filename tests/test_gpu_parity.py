@@ -218,6 +218,10 @@ RGEN = [
     (2, 400, 48, 70, 90, "uniform", 1, False, 79),
     (1, 300, 300, 40, 64, "zero", 0, False, 81),
     (3, 600, 260, 96, 160, "per_entry", 0, True, 83),
+    # 64-column blocks whose last chunk of K holds few elements (the waves run only the
+    # k-steps that reach them)
+    (1, 700, 64, 108, 200, "random", 0, False, 85),
+    (2, 333, 20, 99, 64, "random", 1, False, 87),
 ]
 
 
