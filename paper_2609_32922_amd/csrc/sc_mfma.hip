@@ -1366,6 +1366,11 @@ template <bool BIP, int NK, int PC>
 __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, uint8_t *ws) {
     constexpr int QPT = 256 * PC / 4;         // quads per tile
     constexpr int BPT = QPT / (256 * NK);     // blocks per tile
+    constexpr int CB = PC / 32;               // 32-column blocks of a piece
+    constexpr int RPB = 32 * ((NK + CB - 1) / CB);   // rows a block's NK MFMA blocks span
+    static_assert(RPB <= 256, "rows of a block");
+    __shared__ int32_t srow[RPB], slen[RPB];
+    __shared__ float sfac[RPB];
     const int NTW = lay.NT / 2;
     int F, SS;
     q_division(g, lay, ws, F, SS);
@@ -1383,18 +1388,37 @@ __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, u
     const int b = tb % g.batch, tp = tb / g.batch;
     const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part)) + pbase * QPT +
                        (size_t)part * 256 * NK + threadIdx.x;
-    // (NK <= 2: every piece's loads in flight at once; else one piece at a time)
-    constexpr int SB = NK <= 2 ? MAX_SPLIT : 1;
+    // the first pieces' loads go out before the block stages its rows' decode data
+    constexpr int SB = NK <= 2 ? MAX_SPLIT : (NK <= 4 ? 2 : 1);
+    int4 q[SB][NK];
+#pragma unroll
+    for (int s = 0; s < SB; ++s)
+#pragma unroll
+        for (int k = 0; k < NK; ++k)
+            q[s][k] = s < SS ? base[(size_t)s * QPT + 256 * k] : make_int4(0, 0, 0, 0);
+    // the block's rows rbase .. rbase + RPB - 1 of the pair: original row (-1: padding),
+    // length, decode factor
+    const int rbase = (part * NK / CB) * 32;
+    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
+    if ((int)threadIdx.x < RPB) {
+        const int r = rbase + (int)threadIdx.x;
+        const int i = ws_ptr<int32_t>(wsa, lay.off_perm)[tp * 256 + r];
+        const int Li = i >= 0 ? ws_ptr<int32_t>(wsa, lay.off_Ls)[tp * 256 + r] : 0;
+        srow[threadIdx.x] = i;
+        slen[threadIdx.x] = Li;
+        sfac[threadIdx.x] = i >= 0 ? decode_factor(g.sA[(size_t)b * g.strideSA + i], Li) : 0.0f;
+    }
     int4 sum[NK];
 #pragma unroll
     for (int k = 0; k < NK; ++k) sum[k] = make_int4(0, 0, 0, 0);
     for (int s0 = 0; s0 < SS; s0 += SB) {
-        int4 q[SB][NK];
+        if (s0 > 0) {
 #pragma unroll
-        for (int s = 0; s < SB; ++s)
+            for (int s = 0; s < SB; ++s)
 #pragma unroll
-            for (int k = 0; k < NK; ++k)
-                q[s][k] = s0 + s < SS ? base[(size_t)(s0 + s) * QPT + 256 * k] : make_int4(0, 0, 0, 0);
+                for (int k = 0; k < NK; ++k)
+                    q[s][k] = s0 + s < SS ? base[(size_t)(s0 + s) * QPT + 256 * k] : make_int4(0, 0, 0, 0);
+        }
 #pragma unroll
         for (int s = 0; s < SB; ++s)
 #pragma unroll
@@ -1405,28 +1429,25 @@ __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, u
                 sum[k].w += q[s][k].w;
             }
     }
-    uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
-    const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm) + tp * 256;
-    const int32_t *Ls = ws_ptr<int32_t>(wsa, lay.off_Ls) + tp * 256;
+    __syncthreads();
     const float *sBb = g.sB + (size_t)b * g.strideSB;
     const int lane = threadIdx.x & 63, grp = lane >> 5, i32 = lane & 31;
 #pragma unroll
     for (int k = 0; k < NK; ++k) {
         const int qd = (part * 256 * NK + 256 * k + (int)threadIdx.x) >> 6;   // quad index of the wave
-        const int blk = qd >> 2, q = qd & 3;
-        const int r0 = (blk / (PC / 32)) * 32 + 8 * q + 4 * grp;
-        const int j = tw * 256 + (blk % (PC / 32)) * 32 + i32;
+        const int blk = qd >> 2, qq = qd & 3;
+        const int rl = (blk / CB) * 32 + 8 * qq + 4 * grp - rbase;   // first of its 4 rows, in the block
+        const int j = tw * 256 + (blk % CB) * 32 + i32;
         if (j >= g.N) continue;
         const float sBj = sBb[j];
         const int32_t P[4] = {sum[k].x, sum[k].y, sum[k].z, sum[k].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int i = perm[r0 + e];
+            const int i = srow[rl + e];
             if (i < 0) continue;
-            const int Li = Ls[r0 + e];
-            const float f = decode_factor(g.sA[(size_t)b * g.strideSA + i], Li);
+            const int Li = slen[rl + e];
             const size_t off = (size_t)b * g.strideO + (size_t)i * g.ldo + j;
-            g.out[off] = ((float)P[e] * f) * sBj;
+            g.out[off] = ((float)P[e] * sfac[rl + e]) * sBj;
             if (g.counts) g.counts[off] = Li > 0 ? (BIP ? (g.K * Li + P[e]) / 2 : P[e]) : 0;
         }
     }
