@@ -1962,8 +1962,8 @@ __device__ __forceinline__ void r_chunks(const RSrc &q, int c, int ce, RData<NB>
 // have ended read the padding byte, whose table row is zero; a row that ends inside a
 // cycle group reads there the table masked to its length.  MASK runs when some row pair
 // holds more lengths inside a group than there are masked tables (then every A fragment is
-// masked with its row's length instead): the 256 x 256 blocks launch both variants and one
-// returns at once, the 256 x 64 blocks take the variant per block in one launch.
+// masked with its row's length instead): one launch, each block takes the variant the
+// scheduler's flag names.
 // NARROW (N <= 64): a block takes the pair's 256 rows x the first 64 columns of the B pair,
 // two blocks per CU: wave (rh, kh) the rows of half rh and k-steps kh of every chunk, so that
 // each SIMD runs two waves; the two k-halves are summed through the LDS at the end.  It has no
@@ -2222,12 +2222,16 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
     }
 }
 
-// 256 x 256 blocks: both variants are launched and one returns at once
-template <bool BIP, bool MASK>
+// 256 x 256 blocks: one launch, each block takes the variant the status word names
+union RLdsW {
+    RLds<true> t;
+    RLds<false> m;
+};
+template <bool BIP>
 __global__ __launch_bounds__(256, 1) void k_rgemm(MGemmArgs g, Layout lay, uint8_t *ws) {
-    __shared__ RLds<!MASK> sh;
-    if ((ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) != MASK) return;
-    rgemm_body<BIP, MASK, false, !MASK>(g, lay, ws, sh);
+    __shared__ RLdsW sh;
+    if (ws_ptr<uint32_t>(ws, lay.off_status)[2] != 0u) rgemm_body<BIP, true, false, false>(g, lay, ws, sh.m);
+    else rgemm_body<BIP, false, false, true>(g, lay, ws, sh.t);
 }
 
 // 256 x 64 blocks: one launch, each block takes the variant the status word names
@@ -2248,10 +2252,7 @@ static hipError_t launch_rgemm_w(const MGemmArgs &g, const Layout &lay, uint8_t 
     if (NARROW) {
         hipLaunchKernelGGL((k_rgemm_n<BIP>), grid, block, 0, st, g, lay, ws);
     } else {
-        hipLaunchKernelGGL((k_rgemm<BIP, false>), grid, block, 0, st, g, lay, ws);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL((k_rgemm<BIP, true>), grid, block, 0, st, g, lay, ws);
+        hipLaunchKernelGGL((k_rgemm<BIP>), grid, block, 0, st, g, lay, ws);
     }
     e = hipGetLastError();
     if (e != hipSuccess || tail == 0) return e;
