@@ -249,6 +249,28 @@ def test_rgen_full_compare(dev, oracle_mod, case):
         _compare(g, b, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "rgen%s b%d" % (case, b))
 
 
+# One row length and more 256 x 256 tiles than CUs with a partial last round: on a 256-CU
+# device the full rounds run whole tiles and the last round's tiles run in k-range parts whose
+# partial counts the split sum adds.  Last rounds of 32 tiles, of 44 (ragged M
+# and N), inside a group (L = 100: masked tables) and after two full rounds (544 tiles).
+LAST_ROUND = [
+    # batch, M, N, K, L_max, lengths, polarity, broadcast_B, seed
+    (4, 2304, 2048, 40, 64, "uniform", 0, False, 501),
+    (3, 2500, 2500, 33, 96, "uniform", 1, False, 503),
+    (2, 3577, 2716, 20, 100, "uniform", 0, True, 505),
+    (2, 4352, 4096, 16, 32, "uniform", 1, False, 507),
+]
+
+
+@pytest.mark.parametrize("case", LAST_ROUND, ids=[str(c) for c in LAST_ROUND])
+def test_rgen_partial_last_round(dev, oracle_mod, case):
+    g = _rgen_gemm(case)
+    _note("int8-chunk GEMM, one length, partial last round %s" % (case,))
+    out, cnt = _run(g, dev)
+    for b in range(g.batch):
+        _compare(g, b, np.arange(g.M), np.arange(g.N), out, cnt, oracle_mod, "last_round%s b%d" % (case, b))
+
+
 # With an expected mean length (L_hint) below L_max the 256-row GEMM takes its split count
 # from the scheduled lengths, and the 256 x 64 blocks (N <= 64) divide their tiles by length:
 # long tiles in 2, 4 or 8 parts, short ones whole.  Shapes with few tiles (so that splitting
