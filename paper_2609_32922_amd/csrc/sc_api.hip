@@ -251,11 +251,19 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
         // pieces per cut
         pieces = 2 * sl;
     }
+    // Parts of the int8-chunk GEMM's split tiles of at most P16_STEPS chunk steps store int16
+    // partial counts (half the partial-sum traffic).  A part of S has at most ceil(steps / S)
+    // of a tile's steps; with F = 0 the GEMM may lower S to Smin.
+    if (l.rgen && !l.vsplit && l.S > 1) {
+        const int64_t smin = l.F > 0 ? l.S : l.Smin;
+        const int64_t steps = (int64_t)l.KC * (l.LBS / 32);
+        l.p16 = (steps + smin - 1) / smin <= P16_STEPS;
+    }
     l.off_part = off;
     if (pieces > 0 && (l.S > 1 || l.vsplit)) {
         size_t partb;
-        // every piece is [mbm rows][pcols columns] of int32
-        if (!mul_ok((size_t)pieces, (size_t)l.mbm * (size_t)l.pcols * 4, &partb)) return false;
+        // every piece is [mbm rows][pcols columns] of int32 (int16 with p16)
+        if (!mul_ok((size_t)pieces, (size_t)l.mbm * (size_t)l.pcols * (l.p16 ? 2 : 4), &partb)) return false;
         off = align256(off + partb);
     }
 

@@ -87,6 +87,8 @@ __host__ __device__ inline double quad_split_time(int64_t tiles, int s, double p
 constexpr int OCH = 8;           // octets per block of the nibble-plane generator
 constexpr int RSLOTS = 4;        // int8-chunk GEMM: tables masked to a row length, per cycle group
 constexpr int64_t MFMA_EXACT = 1ll << 24;   // products one fp32 accumulator sums exactly
+// chunk steps whose counts fit int16: a step adds at most 32 x 32 products of magnitude 1 to a count
+constexpr int64_t P16_STEPS = 32767 / (32 * 32);
 constexpr int64_t RSTEP_EXACT = MFMA_EXACT / (32 * 32);   // int8-chunk GEMM chunk steps (32 cycles x
                                                           // 32 elements) one accumulator sums exactly
 // Cost of a chunk step of the 256 x 64 int8-chunk GEMM in the work division, while all of a
@@ -146,6 +148,8 @@ struct Layout {
                               // columns a block computes: 256, or 64 with N <= 64)
     size_t off_part;   // partial counts of split tiles: [pieces][256 rows][pcols columns] int32
     int pcols;         // columns of a piece of partial counts: 256, or 64 for the 256 x 64 blocks
+    int p16;           // int8-chunk GEMM split into parts of at most P16_STEPS chunk steps: the
+                       // partial counts are int16 ([pieces][256 rows][pcols columns])
     int vsplit;        // int8-chunk GEMM with varying lengths: the tiles' chunk steps, end to
                        // end, are cut into sk_slots equal ranges, one per GEMM block (k_units)
     int sk_slots;      // vsplit: GEMM blocks, each running one range of the work

@@ -59,6 +59,7 @@
 namespace scg {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));   // one slot row: 32 nibbles
@@ -429,6 +430,30 @@ __device__ __forceinline__ void d_stage(DecodeLds &d, const int32_t *perm, const
     }
 }
 
+// The same data for one row per thread (256 threads), in two steps: the loads (every row's
+// length is in the layout, padding rows' too, so only the decode factor's scale waits for the
+// row's original index), then the LDS stores
+struct DRow {
+    int32_t i, L;
+    float sa, sb;
+};
+__device__ __forceinline__ DRow d_fetch(const int32_t *perm, const int32_t *Ls, int b, int tw, const MGemmArgs &g,
+                                        int r) {
+    DRow x;
+    x.i = perm[r];
+    x.L = Ls[r];
+    const int j = tw * 256 + r;
+    x.sb = j < g.N ? g.sB[(size_t)b * g.strideSB + j] : 0.0f;
+    x.sa = x.i >= 0 ? g.sA[(size_t)b * g.strideSA + x.i] : 0.0f;
+    return x;
+}
+__device__ __forceinline__ void d_put(DecodeLds &d, const DRow &x, int r) {
+    d.row[r] = x.i;
+    d.len[r] = x.i >= 0 ? x.L : 0;
+    d.f[r] = x.i >= 0 ? decode_factor(x.sa, x.L) : 0.0f;
+    d.sB[r] = x.sb;
+}
+
 // Decode of TR rows of a whole tile from their sums T (fp32, row-major, row stride TS, the
 // tile's columns from 0): thread tid takes column quad tid % NQ of rows tid / NQ + k NT / NQ.
 // All of a thread's LDS reads are issued before its stores.
@@ -480,6 +505,17 @@ __device__ __forceinline__ void store_block(const v16f &a, __amdgpu_buffer_rsrc_
     }
 }
 
+// The same layout with int16 counts (8 bytes per lane and quad; the counts fit, see P16_STEPS)
+template <int PC>
+__device__ __forceinline__ void store_block16(const v16f &a, __amdgpu_buffer_rsrc_t pr, int lane, int rb, int cb) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const v2i v = {(int)(((uint32_t)(int)a[4 * q] & 0xFFFFu) | ((uint32_t)(int)a[4 * q + 1] << 16)),
+                       (int)(((uint32_t)(int)a[4 * q + 2] & 0xFFFFu) | ((uint32_t)(int)a[4 * q + 3] << 16))};
+        __builtin_amdgcn_raw_buffer_store_b64(v, pr, lane * 8, (((rb * (PC / 32) + cb) * 4 + q) * 64) * 8, 0);
+    }
+}
+
 // A wave's 4 x NB blocks of 32 x 32 at rows wr + 32 i, columns wc + 32 c (256-column pieces)
 template <int NB>
 __device__ __forceinline__ void store_part(const v16f (&acc)[4][NB], int32_t *part, int wr, int wc, int lane) {
@@ -496,13 +532,21 @@ __device__ __forceinline__ void store_part(const v16f (&acc)[4][NB], int32_t *pa
 template <bool SKIP>
 __device__ __forceinline__ int r_row0(int rh, int i);
 template <bool SKIP, int NB>
-__device__ __forceinline__ void store_part_r(const v16f (&acc)[4][NB], int32_t *part, int rh, int wc, int lane) {
+__device__ __forceinline__ void store_part_r(const v16f (&acc)[4][NB], uint8_t *part, bool p16, int rh, int wc,
+                                             int lane) {
     constexpr int PC = NB == 2 ? 64 : 256;
-    const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(part, 0, 256 * PC * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(part, 0, 256 * PC * (p16 ? 2 : 4), 0x00020000);
+    if (p16) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int c = 0; c < NB; ++c) store_block<PC>(acc[i][c], pr, lane, r_row0<SKIP>(rh, i) / 32, wc / 32 + c);
+            for (int c = 0; c < NB; ++c) store_block16<PC>(acc[i][c], pr, lane, r_row0<SKIP>(rh, i) / 32, wc / 32 + c);
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int c = 0; c < NB; ++c) store_block<PC>(acc[i][c], pr, lane, r_row0<SKIP>(rh, i) / 32, wc / 32 + c);
+    }
 }
 
 // Block tile: BM = 128 rows of A x WB columns of B, WB = 256 (two 128-column B plane
@@ -1361,8 +1405,22 @@ __global__ __launch_bounds__(256, 1) void k_qgemm(MGemmArgs g, Layout lay, uint8
 // rows of one column, and a block of 256 threads 256 NK quads (BPT blocks per tile).  Few
 // quads per thread when few tiles are split, so that enough waves keep loads in flight; more
 // when many are (less per-block overhead).  With vsplit, tinfo gives each tile's pieces
-// (tiles that ran whole have none).
-template <bool BIP, int NK, int PC>
+// (tiles that ran whole have none).  P16: the pieces hold int16 counts (Layout::p16).
+template <bool P16>
+struct PQuad;
+template <>
+struct PQuad<false> {
+    typedef int4 T;
+    static __device__ __forceinline__ int4 get(const int4 &x) { return x; }
+};
+template <>
+struct PQuad<true> {
+    typedef int2 T;
+    static __device__ __forceinline__ int4 get(const int2 &x) {
+        return make_int4((int)(int16_t)(x.x & 0xFFFF), x.x >> 16, (int)(int16_t)(x.y & 0xFFFF), x.y >> 16);
+    }
+};
+template <bool BIP, int NK, int PC, bool P16>
 __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, uint8_t *ws) {
     constexpr int QPT = 256 * PC / 4;         // quads per tile
     constexpr int BPT = QPT / (256 * NK);     // blocks per tile
@@ -1386,16 +1444,17 @@ __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, u
     const int tw = tile % NTW;
     const int tb = tile / NTW;
     const int b = tb % g.batch, tp = tb / g.batch;
-    const int4 *base = reinterpret_cast<const int4 *>(ws_ptr<int32_t>(ws, lay.off_part)) + pbase * QPT +
-                       (size_t)part * 256 * NK + threadIdx.x;
+    typedef typename PQuad<P16>::T Q;
+    const Q *base = reinterpret_cast<const Q *>(ws_ptr<uint8_t>(ws, lay.off_part)) + pbase * QPT +
+                    (size_t)part * 256 * NK + threadIdx.x;
     // the first pieces' loads go out before the block stages its rows' decode data
     constexpr int SB = NK <= 2 ? MAX_SPLIT : (NK <= 4 ? 2 : 1);
-    int4 q[SB][NK];
+    Q q[SB][NK];
 #pragma unroll
     for (int s = 0; s < SB; ++s)
 #pragma unroll
         for (int k = 0; k < NK; ++k)
-            q[s][k] = s < SS ? base[(size_t)s * QPT + 256 * k] : make_int4(0, 0, 0, 0);
+            q[s][k] = s < SS ? base[(size_t)s * QPT + 256 * k] : Q{};
     // the block's rows rbase .. rbase + RPB - 1 of the pair: original row (-1: padding),
     // length, decode factor
     const int rbase = (part * NK / CB) * 32;
@@ -1417,16 +1476,17 @@ __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, u
             for (int s = 0; s < SB; ++s)
 #pragma unroll
                 for (int k = 0; k < NK; ++k)
-                    q[s][k] = s0 + s < SS ? base[(size_t)(s0 + s) * QPT + 256 * k] : make_int4(0, 0, 0, 0);
+                    q[s][k] = s0 + s < SS ? base[(size_t)(s0 + s) * QPT + 256 * k] : Q{};
         }
 #pragma unroll
         for (int s = 0; s < SB; ++s)
 #pragma unroll
             for (int k = 0; k < NK; ++k) {
-                sum[k].x += q[s][k].x;
-                sum[k].y += q[s][k].y;
-                sum[k].z += q[s][k].z;
-                sum[k].w += q[s][k].w;
+                const int4 t = PQuad<P16>::get(q[s][k]);
+                sum[k].x += t.x;
+                sum[k].y += t.y;
+                sum[k].z += t.z;
+                sum[k].w += t.w;
             }
     }
     __syncthreads();
@@ -1453,19 +1513,24 @@ __global__ __launch_bounds__(256) void k_qgemm_reduce(MGemmArgs g, Layout lay, u
     }
 }
 
-template <bool BIP>
-static hipError_t launch_qreduce(const MGemmArgs &g, const Layout &lay, uint8_t *ws, unsigned tail, hipStream_t st) {
+template <bool BIP, bool P16>
+static void launch_qreduce_p(const MGemmArgs &g, const Layout &lay, uint8_t *ws, unsigned tail, hipStream_t st) {
     if (lay.pcols == 64) {
         if (tail * 16u < 1024u)
-            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 1, 64>), dim3(tail * 16u), dim3(256), 0, st, g, lay, ws);
+            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 1, 64, P16>), dim3(tail * 16u), dim3(256), 0, st, g, lay, ws);
         else
-            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 4, 64>), dim3(tail * 4u), dim3(256), 0, st, g, lay, ws);
+            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 4, 64, P16>), dim3(tail * 4u), dim3(256), 0, st, g, lay, ws);
     } else {
         if (tail * 8u < 1024u)
-            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 2, 256>), dim3(tail * 32u), dim3(256), 0, st, g, lay, ws);
+            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 2, 256, P16>), dim3(tail * 32u), dim3(256), 0, st, g, lay, ws);
         else
-            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 8, 256>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
+            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 8, 256, P16>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
     }
+}
+template <bool BIP>
+static hipError_t launch_qreduce(const MGemmArgs &g, const Layout &lay, uint8_t *ws, unsigned tail, hipStream_t st) {
+    if (lay.p16) launch_qreduce_p<BIP, true>(g, lay, ws, tail, st);
+    else launch_qreduce_p<BIP, false>(g, lay, ws, tail, st);
     return hipGetLastError();
 }
 
@@ -2034,6 +2099,13 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
     uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
     const int32_t *perm = ws_ptr<int32_t>(wsa, lay.off_perm) + tp * 256;
     const int32_t *Ls = ws_ptr<int32_t>(wsa, lay.off_Ls) + tp * 256;
+    // (NARROW) a whole tile's decode data: loaded here, so that their latency overlaps the
+    // unit's first loads instead of following its last chunk step, and staged in LDS before
+    // the steps (compensator 3 % faster; the 256 x 256 blocks stage them after the steps, as
+    // loading them here made them slower on per-row lengths)
+    static_assert(NT == 256, "one row of decode data per thread");
+    DRow drow{};
+    if (NARROW && !split) drow = d_fetch(perm, Ls, b, tw, g, threadIdx.x);
     const size_t pairb = (size_t)g.KC * 256 * RCH;
     RSrc q;
     q.a = __builtin_amdgcn_make_buffer_rsrc(ws_ptr<uint8_t>(wsa, lay.off_Ap) + (size_t)tp * pairb, 0, (int)pairb,
@@ -2105,6 +2177,7 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
     // wave's chunks.  Three phases in turn, as the wave's rows end: all four blocks run, only
     // the first two run, none runs (the wave still takes part in the table fills).  Separate
     // loops, so that a later phase holds none of an earlier one's registers.
+    if (NARROW && !split) d_put(dl, drow, tid);   // (read after the epilogue's first barrier)
     int64_t x = x0;
     auto group_start = [&](int G, int64_t xe, bool (&fin)[4]) {
         const uint32_t rm = TABLES ? rems[G] : 0u;
@@ -2193,11 +2266,11 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
     }
     if (split) {
         if (kh == 0)
-            store_part_r<SKIP, NB>(acc, ws_ptr<int32_t>(ws, lay.off_part) + (size_t)v * 256 * lay.pcols, rh, wc,
-                                   lane);
+            store_part_r<SKIP, NB>(acc, ws_ptr<uint8_t>(ws, lay.off_part) + (size_t)v * 256 * lay.pcols * (lay.p16 ? 2 : 4),
+                                   lay.p16 != 0, rh, wc, lane);
         continue;
     }
-    d_stage<NT>(dl, perm, Ls, b, tw, g, tid);
+    if (!NARROW) d_stage<NT>(dl, perm, Ls, b, tw, g, tid);
     // TR rows per pass: all that fit the table's LDS (64 KB, or 128 KB with the masked tables)
     constexpr int TS = NARROW ? 64 + 4 : 256 + 4, TR = NARROW ? 128 : (TABLES ? 64 : 32);
     static_assert(TR * TS * 4 <= (TABLES ? 2 : 1) * 256 * 16 * 16, "the epilogue transpose must fit the table");
