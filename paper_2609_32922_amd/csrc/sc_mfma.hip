@@ -2136,11 +2136,21 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
     // the unit's chunk steps (a tile of rows of length 0 has none)
     const int64_t x1 = lay.vsplit ? min(ux1, nch) : (int64_t)(s + 1) * nch / S;
     const int64_t x0 = lay.vsplit ? min(ux0, x1) : (int64_t)s * nch / S;
+    // this thread's entries of the group tables (the next group's loaded while the current
+    // group runs) and the first chunk, unless loaded above: issued before the row lengths
+    // below are waited for
+    if (xs < 0 && x0 < x1) {
+        r_load_ent<NT>(ent, rtab + (size_t)(x0 / g.KC) * 512, tid);
+        r_load(q, (int)(x0 % q.KC), cur);
+    }
 
+    // (the layout holds a length for every row, padding rows too, so a row's length is
+    // loaded beside its original index rather than after it)
     if (TABLES) {
         if (tid < ngroups) rems[tid] = 0u;
         __syncthreads();
-        const int Lt = perm[tid] >= 0 ? Ls[tid] : 0;
+        const int pt = perm[tid], lt = Ls[tid];
+        const int Lt = pt >= 0 ? lt : 0;
         if (Lt % RCH != 0) atomicOr(&rems[Lt / RCH], 1u << (Lt % RCH));
         __syncthreads();
     }
@@ -2150,20 +2160,16 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int row = r_row0<SKIP>(rh, i) + i32;
-        Lr[i] = perm[row] >= 0 ? Ls[row] : INT_MAX;
+        const int pr = perm[row], lr = Ls[row];
+        Lr[i] = pr >= 0 ? lr : INT_MAX;
     }
     const int h0 = r_row0<SKIP>(rh, 0), h1 = r_row0<SKIP>(rh, 2);
-    const int Lh0 = wave_uniform(perm[h0] >= 0 ? Ls[h0] : 0), Lh1 = wave_uniform(perm[h1] >= 0 ? Ls[h1] : 0);
+    const int p0 = perm[h0], l0 = Ls[h0], p1 = perm[h1], l1 = Ls[h1];
+    const int Lh0 = wave_uniform(p0 >= 0 ? l0 : 0), Lh1 = wave_uniform(p1 >= 0 ? l1 : 0);
 
     const uint32_t lrep = 16u * (uint32_t)(lane & (RREP - 1));
     q.loB = lrep + 16u * RREP;
     q.lut = reinterpret_cast<const char *>(lut);
-    // this thread's entries of the group tables (the next group's loaded while the current
-    // group runs) and the first chunk, unless loaded above
-    if (xs < 0 && x0 < x1) {
-        r_load_ent<NT>(ent, rtab + (size_t)(x0 / g.KC) * 512, tid);
-        r_load(q, (int)(x0 % q.KC), cur);
-    }
 
     v16f acc[4][NB];
 #pragma unroll
