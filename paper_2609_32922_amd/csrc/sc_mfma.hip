@@ -2093,7 +2093,10 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
     asm volatile("" : "+v"(tid));
     const int lane = tid & 63, w = tid >> 6;
     const int grp = lane >> 5, i32 = lane & 31;
-    const int rh = NARROW ? (w & 1) : (w >> 1), wc = NARROW ? 0 : (w & 1) * 128;   // row half, columns
+    // (NARROW: the second block of a CU, block index cus.., swaps its waves' row halves, so
+    // that when only row half 0 runs the two blocks' busy waves sit on different SIMDs)
+    const int rswap = NARROW ? ((int)blockIdx.x / max(lay.cus, 1)) & 1 : 0;
+    const int rh = NARROW ? (w & 1) ^ rswap : (w >> 1), wc = NARROW ? 0 : (w & 1) * 128;   // row half, columns
     const int kh = NARROW ? (w >> 1) : 0;                                          // k-half (NARROW)
     uint8_t *wsa = ws + (size_t)b * lay.stride_batchA;
     uint8_t *wsbB = ws + (size_t)bB * lay.stride_batchB;
