@@ -113,8 +113,9 @@ typedef struct sc_gemm_desc {
                                    compute units, never changes a result; 0..L_max */
     int32_t reserved;           /* must be 0 */
     uint64_t seed;              /* comparator seed; same seed => bit-identical results */
-    void *prof_event_begin;     /* optional hipEvent_t recorded just before the main */
-    void *prof_event_end;       /*   GEMM kernel and just after it (profiling); NULL = off */
+    void *prof_event_begin;     /* optional hipEvent_t recorded when the counting GEMM's */
+    void *prof_event_end;       /*   first kernel starts and when its last kernel ends (the
+                                     events ride on the kernels' dispatches); NULL = off */
 } sc_gemm_desc;
 
 /* Bytes of device workspace sc_gemm needs for `desc` on the current HIP device (the size

@@ -349,15 +349,19 @@ static int enqueue(const sc_gemm_desc &d, const Layout &lay, const int8_t *A, co
     } else if (!lay.fused) {
         if ((e = launch_mplanes(d, lay, A, B, ws, st)) != hipSuccess) return SC_ERR_HIP;
     }
-    if (d.prof_event_begin != nullptr &&
-        hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_begin), st) != hipSuccess)
-        return SC_ERR_HIP;
+    // the profiling events ride on the GEMM kernels' own dispatches (a marker of their own
+    // in the stream left an idle gap of several microseconds after it); recorded as markers
+    // only if no GEMM kernel was launched
+    hipEvent_t ev0 = reinterpret_cast<hipEvent_t>(d.prof_event_begin);
+    hipEvent_t ev1 = reinterpret_cast<hipEvent_t>(d.prof_event_end);
+    set_gemm_events(ev0, ev1);
     e = lay.fused ? launch_fgemm(d, lay, A, B, sA, sB, out, counts, ws, st)
                   : launch_mgemm(d, lay, sA, sB, out, counts, ws, st);
+    const bool taken = gemm_events_taken();
+    set_gemm_events(nullptr, nullptr);
     if (e != hipSuccess) return SC_ERR_HIP;
-    if (d.prof_event_end != nullptr &&
-        hipEventRecord(reinterpret_cast<hipEvent_t>(d.prof_event_end), st) != hipSuccess)
-        return SC_ERR_HIP;
+    if (!taken && ev0 != nullptr && hipEventRecord(ev0, st) != hipSuccess) return SC_ERR_HIP;
+    if (!taken && ev1 != nullptr && hipEventRecord(ev1, st) != hipSuccess) return SC_ERR_HIP;
     return SC_OK;
 }
 

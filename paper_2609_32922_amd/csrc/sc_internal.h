@@ -172,6 +172,13 @@ hipError_t launch_schedule(const sc_gemm_desc &d, const Layout &lay, const int32
 hipError_t launch_units(const sc_gemm_desc &d, const Layout &lay, uint8_t *ws, hipStream_t st);
 
 // counting GEMM (sc_mfma.hip)
+// Profiling events of the next launch_mgemm / launch_fgemm on this host thread (sc_gemm's
+// prof_event_begin / end, NULL = none): its first kernel records begin when it starts and
+// every kernel records end when it ends (the last one's stays), so the events time the GEMM
+// kernels themselves, with no marker of their own in the stream.  gemm_events_taken() tells
+// whether a kernel took them since set_gemm_events.
+void set_gemm_events(hipEvent_t begin, hipEvent_t end);
+bool gemm_events_taken();
 hipError_t launch_mplanes(const sc_gemm_desc &d, const Layout &lay, const int8_t *A,
                           const int8_t *B, uint8_t *ws, hipStream_t st);
 hipError_t launch_mgemm(const sc_gemm_desc &d, const Layout &lay, const float *sA, const float *sB,

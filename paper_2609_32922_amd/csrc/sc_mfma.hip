@@ -52,11 +52,38 @@
 //                 keeps the matrix cores fed where the 16x16x128 form loses several cycles
 //                 per instruction to issue.
 //   k_mgemm_reduce sums the partial counts of split tiles and decodes
+#include <hip/hip_ext.h>
 #include <limits.h>
 
 #include "sc_internal.h"
 
 namespace scg {
+
+namespace {
+thread_local hipEvent_t t_ev_begin = nullptr, t_ev_end = nullptr;
+thread_local bool t_ev_taken = false;
+}  // namespace
+
+void set_gemm_events(hipEvent_t begin, hipEvent_t end) {
+    t_ev_begin = begin;
+    t_ev_end = end;
+    t_ev_taken = false;
+}
+bool gemm_events_taken() { return t_ev_taken; }
+
+// Launch of a counting-GEMM kernel, `last` when no other kernel of the call follows it
+// (set_gemm_events: the events ride on the dispatches themselves)
+template <typename F, typename... Args>
+static void gemm_launch(F kernel, dim3 grid, dim3 block, hipStream_t st, bool last, Args... args) {
+    hipEvent_t e0 = t_ev_begin, e1 = last ? t_ev_end : nullptr;
+    if (e0 == nullptr && e1 == nullptr) {
+        hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+        return;
+    }
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, e0, e1, 0, args...);
+    t_ev_begin = nullptr;
+    t_ev_taken = true;
+}
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v2i __attribute__((ext_vector_type(2)));
@@ -816,14 +843,13 @@ static hipError_t launch_mgemm_tile(const MGemmArgs &g, const Layout &lay, uint8
                                     hipStream_t st) {
     const unsigned tiles = (unsigned)(g.batch * lay.MT * (lay.NT / (WB / BN)));
     if (g.S == 1) {
-        hipLaunchKernelGGL((k_mgemm<BIP, false, WB>), dim3(tiles), dim3(256), 0, st, g, lay, ws);
+        gemm_launch((k_mgemm<BIP, false, WB>), dim3(tiles), dim3(256), st, true, g, lay, ws);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((k_mgemm<BIP, true, WB>), dim3(tiles * (unsigned)g.S), dim3(256), 0, st, g, lay,
-                       ws);
+    gemm_launch((k_mgemm<BIP, true, WB>), dim3(tiles * (unsigned)g.S), dim3(256), st, false, g, lay, ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_mgemm_reduce<BIP, WB>), dim3(tiles * 4u), dim3(256), 0, st, g, lay, ws);
+    gemm_launch((k_mgemm_reduce<BIP, WB>), dim3(tiles * 4u), dim3(256), st, true, g, lay, ws);
     return hipGetLastError();
 }
 
@@ -1085,14 +1111,14 @@ static hipError_t launch_fgemm_pol(const MGemmArgs &g, const FArgs &f, const Lay
                                    hipStream_t st) {
     const unsigned tiles = (unsigned)(g.batch * lay.MT);
     if (g.S == 1) {
-        hipLaunchKernelGGL((k_fgemm<POL, false>), dim3(tiles), dim3(256), 0, st, g, f, lay, ws);
+        gemm_launch((k_fgemm<POL, false>), dim3(tiles), dim3(256), st, true, g, f, lay, ws);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((k_fgemm<POL, true>), dim3(tiles * (unsigned)g.S), dim3(256), 0, st, g, f, lay, ws);
+    gemm_launch((k_fgemm<POL, true>), dim3(tiles * (unsigned)g.S), dim3(256), st, false, g, f, lay, ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_mgemm_reduce<POL == SC_BIPOLAR_XNOR, FWB>), dim3(tiles * 4u), dim3(256), 0, st, g,
-                       lay, ws);
+    gemm_launch((k_mgemm_reduce<POL == SC_BIPOLAR_XNOR, FWB>), dim3(tiles * 4u), dim3(256), st, true, g, lay,
+                ws);
     return hipGetLastError();
 }
 
@@ -1517,14 +1543,14 @@ template <bool BIP, bool P16>
 static void launch_qreduce_p(const MGemmArgs &g, const Layout &lay, uint8_t *ws, unsigned tail, hipStream_t st) {
     if (lay.pcols == 64) {
         if (tail * 16u < 1024u)
-            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 1, 64, P16>), dim3(tail * 16u), dim3(256), 0, st, g, lay, ws);
+            gemm_launch((k_qgemm_reduce<BIP, 1, 64, P16>), dim3(tail * 16u), dim3(256), st, true, g, lay, ws);
         else
-            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 4, 64, P16>), dim3(tail * 4u), dim3(256), 0, st, g, lay, ws);
+            gemm_launch((k_qgemm_reduce<BIP, 4, 64, P16>), dim3(tail * 4u), dim3(256), st, true, g, lay, ws);
     } else {
         if (tail * 8u < 1024u)
-            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 2, 256, P16>), dim3(tail * 32u), dim3(256), 0, st, g, lay, ws);
+            gemm_launch((k_qgemm_reduce<BIP, 2, 256, P16>), dim3(tail * 32u), dim3(256), st, true, g, lay, ws);
         else
-            hipLaunchKernelGGL((k_qgemm_reduce<BIP, 8, 256, P16>), dim3(tail * 8u), dim3(256), 0, st, g, lay, ws);
+            gemm_launch((k_qgemm_reduce<BIP, 8, 256, P16>), dim3(tail * 8u), dim3(256), st, true, g, lay, ws);
     }
 }
 template <bool BIP>
@@ -1538,8 +1564,8 @@ template <bool BIP>
 static hipError_t launch_qgemm(const MGemmArgs &g, const Layout &lay, uint8_t *ws, hipStream_t st) {
     const unsigned tiles = (unsigned)(g.batch * (lay.MT / 2) * (lay.NT / 2));
     const unsigned tail = tiles - (unsigned)g.F;
-    hipLaunchKernelGGL((k_qgemm<BIP>), dim3((unsigned)g.F + tail * (unsigned)g.S), dim3(256), 0, st, g,
-                       lay, ws);
+    gemm_launch((k_qgemm<BIP>), dim3((unsigned)g.F + tail * (unsigned)g.S), dim3(256), st, tail == 0, g, lay,
+                ws);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || tail == 0) return e;
     return launch_qreduce<BIP>(g, lay, ws, tail, st);
@@ -2332,9 +2358,9 @@ static hipError_t launch_rgemm_w(const MGemmArgs &g, const Layout &lay, uint8_t 
         block(256);
     hipError_t e;
     if (NARROW) {
-        hipLaunchKernelGGL((k_rgemm_n<BIP>), grid, block, 0, st, g, lay, ws);
+        gemm_launch((k_rgemm_n<BIP>), grid, block, st, tail == 0, g, lay, ws);
     } else {
-        hipLaunchKernelGGL((k_rgemm<BIP>), grid, block, 0, st, g, lay, ws);
+        gemm_launch((k_rgemm<BIP>), grid, block, st, tail == 0, g, lay, ws);
     }
     e = hipGetLastError();
     if (e != hipSuccess || tail == 0) return e;
