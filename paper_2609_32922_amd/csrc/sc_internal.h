@@ -95,6 +95,10 @@ constexpr int64_t RSTEP_EXACT = MFMA_EXACT / (32 * 32);   // int8-chunk GEMM chu
 // wave's row blocks run (RW1) and once only the first two do (RW2): half the MFMAs and two
 // thirds of the table reads; the 256 x 256 blocks weigh every step 1
 constexpr int64_t RW1_NARROW = 8, RW2_NARROW = 5;
+// The 256 x 64 blocks run two per CU, and the one dispatched first issues first: of the two
+// ranges of a CU's pair of blocks, the first one's is RLEAD_NARROW / 16 longer than the
+// average and the second one's as much shorter, so that both end together
+constexpr int64_t RLEAD_NARROW = 4;
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 

@@ -482,6 +482,17 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *
         W += tot;
     }
     const int64_t T = (W + slots - 1) / slots;
+    // Range s covers the costs [cut(s), cut(s + 1)).  The 256 x 64 blocks take the ranges in
+    // pairs, 2p for the first block of a CU and 2p + 1 for the second, the first
+    // (16 + RLEAD_NARROW) / 16 T long (cut(slots) = slots T >= W either way).
+    const bool lead = lay.narrow && slots % 2 == 0;
+    const int64_t TL = lead ? T + T * RLEAD_NARROW / 16 : T;
+    auto cut = [&](int64_t s) -> int64_t { return lead ? (s >> 1) * 2 * T + (s & 1) * TL : s * T; };
+    auto range_of = [&](int64_t c) -> int64_t {
+        if (!lead) return c / T;
+        const int64_t p = c / (2 * T);
+        return 2 * p + (c - p * 2 * T >= TL ? 1 : 0);
+    };
     int4 *units = ws_ptr<int4>(ws, lay.off_units);
     int2 *tinfo = ws_ptr<int2>(ws, lay.off_tinfo);
     uint32_t *slot = ws_ptr<uint32_t>(ws, lay.off_slot);
@@ -494,20 +505,20 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *
         const int64_t C = ccarry + block_excl_scan_1024(cw, &ctot);
         // ranges meeting the tile's cost; the last one starts inside the decode's share when
         // the last cut lies past the steps: it gets no piece
-        const int nr = t < tiles ? (int)((C + cw - 1) / T - C / T + 1) : 0;
-        const int np = nr > 1 && ((C + cw - 1) / T) * T >= C + w ? nr - 1 : nr;
+        const int nr = t < tiles ? (int)(range_of(C + cw - 1) - range_of(C) + 1) : 0;
+        const int np = nr > 1 && cut(range_of(C + cw - 1)) >= C + w ? nr - 1 : nr;
         const int64_t U = ucarry + block_excl_scan_1024(np, &utot);
         const int64_t P = pcarry + block_excl_scan_1024(np > 1 ? np : 0, &ptot);
         if (t < tiles) {
             tinfo[t] = make_int2(np, np > 1 ? (int)P : -1);
             for (int p = 0; p < nr; ++p) {
-                const int64_t s0 = C / T + p;
-                const int64_t a = p == 0 ? C : s0 * T, e = p == np - 1 ? C + w : (s0 + 1) * T;
+                const int64_t s0 = range_of(C) + p;
+                const int64_t a = p == 0 ? C : cut(s0), e = p == np - 1 ? C + w : cut(s0 + 1);
                 if (p < np)
                     units[U + p] = make_int4(t, (int)step_at(n, a - C), (int)step_at(n, e - C),
                                              np > 1 ? (int)(P + p) : -1);
                 // (a range starting inside the decode's share starts with the next tile's first unit)
-                if (a % T == 0) slot[a / T] = (uint32_t)(U + p);
+                if (cut(s0) == a) slot[s0] = (uint32_t)(U + p);
             }
         }
         ccarry += ctot;
@@ -515,7 +526,7 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *
         pcarry += ptot;
     }
     // ranges past the end of the work hold no unit
-    for (int64_t s = (W + T - 1) / T + tid; s <= slots; s += 1024) slot[s] = (uint32_t)ucarry;
+    for (int64_t s = (W > 0 ? range_of(W - 1) + 1 : 0) + tid; s <= slots; s += 1024) slot[s] = (uint32_t)ucarry;
 }
 
 hipError_t launch_units(const sc_gemm_desc &d, const Layout &lay, uint8_t *ws, hipStream_t st) {
