@@ -435,9 +435,10 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 // row blocks (from the group where sorted row 128 of the pair has ended: rows are sorted by
 // length, and the blocks {2, 3} and {6, 7} of the waves' row halves hold rows 128 .. 255),
 // at least 1 (a tile of rows of length 0 still writes its zeros), plus E for its decode and
-// prologue (measured: 13.6 + 3.7 us against 3.6 us per step for 256 x 256 blocks, E = 5
-// steps; about 3 steps for 256 x 64).  The tiles' costs are laid end to end and the total
-// cut into sk_slots ranges of T = ceil(W / sk_slots), range s for GEMM block s: every block
+// prologue (measured: 13.6 + 3.7 us against 3.6 us per step for 256 x 256 blocks; 13.4 us
+// against 1.65 us per step for 256 x 64 blocks, whose best E measured 5 steps of 3, 5 and 8).
+// The tiles' costs are laid end to end and the total cut into sk_slots ranges of about
+// T = ceil(W / sk_slots) (see cut() below), range s for GEMM block s: every block
 // gets the same share of the MFMA work, which follows the sum of the row lengths (Sec. 4.1),
 // and of the decodes.  A tile inside one range runs whole and is decoded by its block; a
 // tile that c cuts cross through its steps runs as c + 1 pieces (a cut maps to the first
@@ -451,7 +452,7 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *
     const int NTW = lay.NT / 2, npairs = lay.MT / 2, slots = lay.sk_slots;
     const int tiles = batch * npairs * NTW;
     const int64_t W1 = lay.narrow ? RW1_NARROW : 1, W2 = lay.narrow ? RW2_NARROW : 1;
-    const int64_t E = lay.narrow ? 3 * W1 : 5 * W1;
+    const int64_t E = 5 * W1;
     // tile t's steps at weight W1 and at weight W2
     auto steps = [&](int t) -> int2 {
         const int tb = t / NTW, b = tb % batch, tp = tb / batch;
