@@ -1639,17 +1639,22 @@ __device__ __forceinline__ u4 r_half(const int8_t *xrow, int d0, int K, bool vec
     if (vec && d0 + 16 <= K) {
         v = *reinterpret_cast<const u4 *>(xrow + d0);
     } else {
-        // any byte alignment: the five aligned dwords that cover the 16 bytes, each loaded
-        // only when it holds a byte of the row before K (an aligned dword never crosses a
-        // page, so it is readable when one of its bytes is), then shifted into place; bytes
-        // at or past K are replaced below
+        // any byte alignment: the two aligned 16-byte blocks that cover the 16 bytes, each
+        // loaded only when it holds a byte of the row before K (an aligned block never crosses
+        // a page, so it is readable when one of its bytes is; the first always holds byte d0),
+        // then shifted into place; bytes at or past K are replaced below
         const uintptr_t p = reinterpret_cast<uintptr_t>(xrow + d0);
         const uintptr_t end = reinterpret_cast<uintptr_t>(xrow + K);
-        const uint32_t *w = reinterpret_cast<const uint32_t *>(p & ~(uintptr_t)3);
+        const u4 *w = reinterpret_cast<const u4 *>(p & ~(uintptr_t)15);
+        const u4 lo = w[0];
+        const u4 hi = reinterpret_cast<uintptr_t>(w + 1) < end ? w[1] : u4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
+        const uint32_t t[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const uint32_t q = (uint32_t)(p >> 2) & 3u, sh = (uint32_t)(p & 3);
+        // dwords q .. q + 4 of t, picked with selects (q differs between the rows of a wave)
         uint32_t wv[5];
 #pragma unroll
-        for (int k = 0; k < 5; ++k) wv[k] = reinterpret_cast<uintptr_t>(w + k) < end ? w[k] : 0x80808080u;
-        const uint32_t sh = (uint32_t)(p & 3);
+        for (int k = 0; k < 5; ++k)
+            wv[k] = q == 0 ? t[k] : q == 1 ? t[k + 1] : q == 2 ? t[k + 2] : t[k + 3];
 #pragma unroll
         for (int k = 0; k < 4; ++k) v[k] = __builtin_amdgcn_alignbyte(wv[k + 1], wv[k], sh);
     }
