@@ -93,8 +93,9 @@ constexpr int64_t RSTEP_EXACT = MFMA_EXACT / (32 * 32);   // int8-chunk GEMM chu
                                                           // 32 elements) one accumulator sums exactly
 // Cost of a chunk step of the 256 x 64 int8-chunk GEMM in the work division, while all of a
 // wave's row blocks run (RW1) and once only the first two do (RW2): half the MFMAs and two
-// thirds of the table reads; the 256 x 256 blocks weigh every step 1
-constexpr int64_t RW1_NARROW = 8, RW2_NARROW = 5;
+// thirds of the table reads (measured on attention-V: 9/16 of a full step's time, against
+// 8/16, 10/16 and 11/16); the 256 x 256 blocks weigh every step 1
+constexpr int64_t RW1_NARROW = 16, RW2_NARROW = 9;
 // The 256 x 64 blocks run two per CU, and the one dispatched first issues first: of the two
 // ranges of a CU's pair of blocks, the first one's is RLEAD_NARROW / 16 longer than the
 // average and the second one's as much shorter, so that both end together
