@@ -1898,6 +1898,15 @@ __device__ __forceinline__ void q_mma_half(v16f (&acc)[4][NB], const RFrags<NB> 
                                                                         acc[i][c], 4, 4, 0, 127, 0, 127);
 }
 
+// the MFMAs of the first A block only (its B blocks)
+template <int NB>
+__device__ __forceinline__ void q_mma_one(v16f (&acc)[4][NB], const RFrags<NB> &f) {
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+        acc[0][c] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(frag(f.a[0]), frag(f.b[c]), acc[0][c], 4, 4, 0,
+                                                                    127, 0, 127);
+}
+
 // fragments of k-step E (element E of the lane's 16) from chunk data d
 template <int E, bool MASK, int NB>
 __device__ __forceinline__ void r_frags(const RSrc &q, const RData<NB> &d, const u4 (&m)[4], RFrags<NB> &f) {
@@ -1920,6 +1929,15 @@ __device__ __forceinline__ void r_frags_h(const RSrc &q, const RData<NB> &d, con
         f.a[i] = r_look<E>(q, r_word<E>(d.a[i]), q.loA[i]);
         if (MASK) f.a[i] &= m[i];
     }
+}
+
+// fragments of k-step E for the first A block only (the wave's other three have ended)
+template <int E, bool MASK, int NB>
+__device__ __forceinline__ void r_frags_q(const RSrc &q, const RData<NB> &d, const u4 (&m)[4], RFrags<NB> &f) {
+#pragma unroll
+    for (int c = 0; c < NB; ++c) f.b[c] = r_look<E>(q, r_word<E>(d.b[c]), q.loB);
+    f.a[0] = r_look<E>(q, r_word<E>(d.a[0]), q.loA[0]);
+    if (MASK) f.a[0] &= m[0];
 }
 
 // Stage S (k-steps 2S, 2S+1) of a chunk: fragment set 0 holds k-step 2S on entry and the
@@ -2009,6 +2027,42 @@ __device__ __forceinline__ void r_stage_h(const RSrc &q, int cnext, RData<NB> &c
     q_mma_half(acc, f[1], 0);
     r_quarter_reads<false, NB>();
     if (MASK) r_mask_h(m, f[0]);
+}
+
+// Stage S when only the wave's first A block runs: NB MFMAs and 1 + NB table reads per k-step
+template <int S, bool MASK, int NB>
+__device__ __forceinline__ void r_stage_q(const RSrc &q, int cnext, RData<NB> &cur, RData<NB> &nxt,
+                                          const u4 (&m)[4], const bool (&fin)[4], v16f (&acc)[4][NB],
+                                          RFrags<NB> (&f)[2]) {
+    if (S == 0) r_load(q, cnext, nxt);
+    r_frags_q<2 * S + 1, MASK>(q, cur, m, f[1]);
+    q_mma_one(acc, f[0]);
+    if (S < RShape<NB>::KS / 2 - 1) {
+        r_frags_q<2 * S + 2, MASK>(q, cur, m, f[0]);
+    } else {
+        if (!MASK) r_finish(nxt, fin);
+        r_frags_q<0, MASK>(q, nxt, m, f[0]);
+    }
+    q_mma_one(acc, f[1]);
+}
+template <bool MASK, int NB>
+__device__ __forceinline__ void r_chunks_q(const RSrc &q, int c, int ce, RData<NB> &cur, RData<NB> &nxt,
+                                           const u4 (&m)[4], const bool (&fin)[4], v16f (&acc)[4][NB],
+                                           RFrags<NB> (&f)[2]) {
+    for (; c < ce; ++c) {
+        const int x = c + 1 < q.KC ? c + 1 : 0;
+        r_stage_q<0, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_q<1, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_q<2, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        r_stage_q<3, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        if constexpr (RShape<NB>::KS == 16) {
+            r_stage_q<4, MASK>(q, x, cur, nxt, m, fin, acc, f);
+            r_stage_q<5, MASK>(q, x, cur, nxt, m, fin, acc, f);
+            r_stage_q<6, MASK>(q, x, cur, nxt, m, fin, acc, f);
+            r_stage_q<7, MASK>(q, x, cur, nxt, m, fin, acc, f);
+        }
+        cur = nxt;
+    }
 }
 
 template <bool MASK, int NB>
@@ -2197,9 +2251,10 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
         const int pr = perm[row], lr = Ls[row];
         Lr[i] = pr >= 0 ? lr : INT_MAX;
     }
-    const int h0 = r_row0<SKIP>(rh, 0), h1 = r_row0<SKIP>(rh, 2);
-    const int p0 = perm[h0], l0 = Ls[h0], p1 = perm[h1], l1 = Ls[h1];
+    const int h0 = r_row0<SKIP>(rh, 0), h1 = r_row0<SKIP>(rh, 2), h01 = r_row0<SKIP>(rh, 1);
+    const int p0 = perm[h0], l0 = Ls[h0], p1 = perm[h1], l1 = Ls[h1], p01 = perm[h01], l01 = Ls[h01];
     const int Lh0 = wave_uniform(p0 >= 0 ? l0 : 0), Lh1 = wave_uniform(p1 >= 0 ? l1 : 0);
+    const int Lh01 = wave_uniform(p01 >= 0 ? l01 : 0);
 
     const uint32_t lrep = 16u * (uint32_t)(lane & (RREP - 1));
     q.loB = lrep + 16u * RREP;
@@ -2256,12 +2311,22 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
     }
     for (; SKIP && x < x1;) {
         const int G = (int)(x / g.KC);
-        if (Lh0 <= RCH * G) break;
+        if (Lh01 <= RCH * G) break;
         const int64_t xe = min(x1, (int64_t)(G + 1) * g.KC);
         bool fin[4];
         group_start(G, xe, fin);
         r_frags_h<0, MASK>(q, cur, m, f[0]);
         r_chunks_h<MASK>(q, (int)(x - (int64_t)G * g.KC), (int)(xe - (int64_t)G * g.KC), cur, nxt, m, fin, acc, f);
+        x = xe;
+    }
+    for (; SKIP && x < x1;) {
+        const int G = (int)(x / g.KC);
+        if (Lh0 <= RCH * G) break;
+        const int64_t xe = min(x1, (int64_t)(G + 1) * g.KC);
+        bool fin[4];
+        group_start(G, xe, fin);
+        r_frags_q<0, MASK>(q, cur, m, f[0]);
+        r_chunks_q<MASK>(q, (int)(x - (int64_t)G * g.KC), (int)(xe - (int64_t)G * g.KC), cur, nxt, m, fin, acc, f);
         x = xe;
     }
     for (; SKIP && x < x1;) {
