@@ -230,11 +230,11 @@ bool make_layout(const sc_gemm_desc &d, int cus, Layout *lay) {
     l.off_units = off;
     int64_t pieces = quad ? (tiles - l.F) * (int64_t)l.S : tiles * (int64_t)l.S;
     if (l.vsplit) {
-        // (k_units weighs a step w1 or w2 and adds at most 7 w1 per tile for its decode and a
-        // minimum step: W <= w1 wmax.  A range of cost T = ceil(W / sl) <= w1 wmax / sl + 1
-        // holds at most T / w2 + 1 steps, which must stay below RSTEP_EXACT to sum exactly;
+        // (k_units weighs a step at most w1 and at least w2 and adds at most 7 w1 per tile for
+        // its decode and a minimum step: W <= w1 wmax.  A range of cost T = ceil(W / sl) <=
+        // w1 wmax / sl + 1 holds at most T / w2 + 1 steps, which must stay below RSTEP_EXACT;
         // the 256 x 64 blocks' ranges hold up to twice T.)
-        const int64_t w1 = l.narrow ? RW1_NARROW : 1, w2 = l.narrow ? RW2_NARROW : 1;
+        const int64_t w1 = l.narrow ? RW1_NARROW : 1, w2 = l.narrow ? RW3_NARROW : 1;   // (w2: the lightest step)
         const int64_t wmax = tiles * ((int64_t)l.KC * (l.LBS / 32) + 7);
         const int64_t den = (w2 * (RSTEP_EXACT - 2) - 1) / (l.narrow ? 2 : 1);
         int64_t sl = l.q_slots;

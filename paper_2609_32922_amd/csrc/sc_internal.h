@@ -96,6 +96,9 @@ constexpr int64_t RSTEP_EXACT = MFMA_EXACT / (32 * 32);   // int8-chunk GEMM chu
 // thirds of the table reads (measured on attention-V: 9/16 of a full step's time, against
 // 8/16, 10/16 and 11/16); the 256 x 256 blocks weigh every step 1
 constexpr int64_t RW1_NARROW = 16, RW2_NARROW = 9;
+// ... and once only the first one does (RW3: one A read and two MFMAs per k-step, beside two B
+// reads; measured on attention-V: 5/16 against 3, 4, 7 and 9); the smallest of the three
+constexpr int64_t RW3_NARROW = 5;
 // The 256 x 64 blocks run two per CU, and the one dispatched first issues first: of the two
 // ranges of a CU's pair of blocks, the first one's is RLEAD_NARROW / 16 longer than the
 // average and the second one's as much shorter, so that both end together

@@ -434,6 +434,7 @@ __global__ __launch_bounds__(1024) void k_schedule(const int32_t *__restrict__ L
 // block runs, W2 per step once the 256 x 64 blocks run only the first half of each wave's
 // row blocks (from the group where sorted row 128 of the pair has ended: rows are sorted by
 // length, and the blocks {2, 3} and {6, 7} of the waves' row halves hold rows 128 .. 255),
+// W3 once they run only row block 0 (from the group where sorted row 32 has ended),
 // at least 1 (a tile of rows of length 0 still writes its zeros), plus E for its decode and
 // prologue (measured: 13.6 + 3.7 us against 3.6 us per step for 256 x 256 blocks; 13.4 us
 // against 1.65 us per step for 256 x 64 blocks, whose best E measured 5 steps of 3, 5 and 8).
@@ -452,29 +453,33 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *
     const int NTW = lay.NT / 2, npairs = lay.MT / 2, slots = lay.sk_slots;
     const int tiles = batch * npairs * NTW;
     const int64_t W1 = lay.narrow ? RW1_NARROW : 1, W2 = lay.narrow ? RW2_NARROW : 1;
+    const int64_t W3 = lay.narrow ? RW3_NARROW : 1;
     const int64_t E = 5 * W1;
-    // tile t's steps at weight W1 and at weight W2
-    auto steps = [&](int t) -> int2 {
+    // tile t's steps at weight W1, W2 and W3 (the 256 x 64 blocks: from the group after which
+    // sorted row 128, then row 32, of the pair has ended)
+    auto steps = [&](int t) -> int4 {
         const int tb = t / NTW, b = tb % batch, tp = tb / batch;
         uint8_t *wsb = ws + (size_t)b * lay.stride_batchA;
         const int g0 = (ws_ptr<int32_t>(wsb, lay.off_tileL)[2 * tp] + 31) / 32;
-        int g1 = g0;
+        int g1 = g0, g2 = g0;
         if (lay.narrow) {
-            const int r = tp * 256 + 128;
-            const int L1 = ws_ptr<int32_t>(wsb, lay.off_perm)[r] >= 0
-                               ? ws_ptr<int32_t>(wsb, lay.off_Ls)[r]
-                               : 0;
-            g1 = min((L1 + 31) / 32, g0);
+            auto ends = [&](int r) {
+                const int L1 = ws_ptr<int32_t>(wsb, lay.off_perm)[r] >= 0 ? ws_ptr<int32_t>(wsb, lay.off_Ls)[r] : 0;
+                return min((L1 + 31) / 32, g0);
+            };
+            g1 = ends(tp * 256 + 128);
+            g2 = max(ends(tp * 256 + 32), g1);
         }
-        return make_int2(g1 * lay.KC, (g0 - g1) * lay.KC);
+        return make_int4(g1 * lay.KC, (g2 - g1) * lay.KC, (g0 - g2) * lay.KC, 0);
     };
-    auto cost = [&](int2 n) -> int64_t {
-        const int64_t c = (int64_t)n.x * W1 + (int64_t)n.y * W2;
+    auto cost = [&](int4 n) -> int64_t {
+        const int64_t c = (int64_t)n.x * W1 + (int64_t)n.y * W2 + (int64_t)n.z * W3;
         return c > 0 ? c : 1;
     };
     // the steps whose cost ends at or before c (0 <= c <= cost(n); c = cost(n): every step)
-    auto step_at = [&](int2 n, int64_t c) -> int64_t {
-        return c < (int64_t)n.x * W1 ? c / W1 : n.x + (c - (int64_t)n.x * W1) / W2;
+    auto step_at = [&](int4 n, int64_t c) -> int64_t {
+        const int64_t c1 = (int64_t)n.x * W1, c2 = c1 + (int64_t)n.y * W2;
+        return c < c1 ? c / W1 : c < c2 ? n.x + (c - c1) / W2 : n.x + n.y + (c - c2) / W3;
     };
     int64_t W = 0;
     for (int c = 0; c < tiles; c += 1024) {
@@ -500,7 +505,7 @@ __global__ __launch_bounds__(1024) void k_units(Layout lay, int batch, uint8_t *
     int64_t ccarry = 0, ucarry = 0, pcarry = 0;
     for (int c = 0; c < tiles; c += 1024) {
         const int t = c + tid;
-        const int2 n = t < tiles ? steps(t) : make_int2(0, 0);
+        const int4 n = t < tiles ? steps(t) : make_int4(0, 0, 0, 0);
         const int64_t w = t < tiles ? cost(n) : 0, cw = t < tiles ? w + E : 0;
         int64_t ctot, utot, ptot;
         const int64_t C = ccarry + block_excl_scan_1024(cw, &ctot);
