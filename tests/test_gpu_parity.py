@@ -195,6 +195,24 @@ def test_split_partials_extreme(dev, oracle_mod, polarity):
     _compare(g, 0, rows, np.arange(N), out, cnt, oracle_mod, "extreme pol%d" % polarity)
 
 
+@pytest.mark.parametrize("polarity", [0, 1])
+def test_int16_partials_at_their_bound(dev, oracle_mod, polarity):
+    # 384 tiles of 256 x 256 on 256 CUs: the last 128 run in two parts of 31 chunk steps each
+    # (K = 992: 31 chunks, L = 64: 2 cycle groups), the most whose partial counts are stored as
+    # int16; constant operands give every part's counts the largest magnitude, 31 x 32 x 32 =
+    # 31744, of both signs across columns.  (With K = 1024 the parts hold 32 steps and int32.)
+    M, N, K, L = 6144, 4096, 992, 64
+    rng = np.random.default_rng(311 + polarity)
+    g = W.random_gemm(rng, 1, M, N, K, L, polarity, 311 + polarity, uniform_L=L)
+    g.A[:] = 127
+    g.B[:] = np.where(np.arange(N)[:, None] % 2 == 0, 127, -127).astype(np.int8)
+    _note("int16 partials at the bound polarity %d" % polarity)
+    out, cnt = _run(g, dev)
+    assert np.array_equal(cnt[0], np.broadcast_to(cnt[0][:1], cnt[0].shape))
+    rows = np.union1d(_sample(M, rng, 3), [0, 4095, 4096, 5000, 6143])
+    _compare(g, 0, rows, np.arange(N), out, cnt, oracle_mod, "int16 bound pol%d" % polarity)
+
+
 # --------------------------------------------------------------------------
 # 256 x 256 MFMA GEMM with comparator streams: fp4 fragments built from int8 chunks
 # through a table per 32-cycle group.  One variant masks every A fragment with its row's
