@@ -562,7 +562,8 @@ template <bool SKIP, int NB>
 __device__ __forceinline__ void store_part_r(const v16f (&acc)[4][NB], uint8_t *part, bool p16, int rh, int wc,
                                              int lane) {
     constexpr int PC = NB == 2 ? 64 : 256;
-    const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(part, 0, 256 * PC * (p16 ? 2 : 4), 0x00020000);
+    const __amdgpu_buffer_rsrc_t pr =
+        __builtin_amdgcn_make_buffer_rsrc(part, 0, 256 * PC * (p16 ? 2 : 4), 0x00020000);
     if (p16) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -1647,7 +1648,7 @@ __device__ __forceinline__ u4 r_half(const int8_t *xrow, int d0, int K, bool vec
         const uintptr_t end = reinterpret_cast<uintptr_t>(xrow + K);
         const u4 *w = reinterpret_cast<const u4 *>(p & ~(uintptr_t)15);
         const u4 lo = w[0];
-        const u4 hi = reinterpret_cast<uintptr_t>(w + 1) < end ? w[1] : u4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
+        const u4 hi = reinterpret_cast<uintptr_t>(w + 1) < end ? w[1] : v;   // (v: padding bytes)
         const uint32_t t[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         const uint32_t q = (uint32_t)(p >> 2) & 3u, sh = (uint32_t)(p & 3);
         // dwords q .. q + 4 of t, picked with selects (q differs between the rows of a wave)
@@ -2371,7 +2372,8 @@ __device__ __forceinline__ void rgemm_body(const MGemmArgs &g, const Layout &lay
     }
     if (split) {
         if (kh == 0)
-            store_part_r<SKIP, NB>(acc, ws_ptr<uint8_t>(ws, lay.off_part) + (size_t)v * 256 * lay.pcols * (lay.p16 ? 2 : 4),
+            store_part_r<SKIP, NB>(acc,
+                                   ws_ptr<uint8_t>(ws, lay.off_part) + (size_t)v * 256 * lay.pcols * (lay.p16 ? 2 : 4),
                                    lay.p16 != 0, rh, wc, lane);
         continue;
     }
