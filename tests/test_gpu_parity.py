@@ -240,6 +240,10 @@ RGEN = [
     # k-steps that reach them)
     (1, 700, 64, 108, 200, "random", 0, False, 85),
     (2, 333, 20, 99, 64, "random", 1, False, 87),
+    # last chunk of K holding one element (K % 32 = 1, as attention-V's K = 577) and nine (the
+    # k-half 1 waves then hold one of its k-steps): the chunk runs only those k-steps
+    (2, 300, 48, 33, 96, "random", 0, False, 89),
+    (1, 520, 40, 73, 64, "random", 1, False, 91),
 ]
 
 
