@@ -398,8 +398,12 @@ __device__ __forceinline__ void decode4_store(const float (&P)[4], const int32_t
 #pragma unroll
     for (int c = 0; c < 4; ++c) o[c] = (P[c] * f) * sBj[c];
     const size_t off = (size_t)b * g.strideO + (size_t)i * g.ldo + j0;
+    // (non-temporal: the outputs are not read again here; ViT-B fc1 with mixed lengths -0.9 %,
+    // the compensator -2 %)
+    typedef float f4nt __attribute__((ext_vector_type(4)));
+    typedef int i4nt __attribute__((ext_vector_type(4)));
     if (ncol == 4 && g.vec_out) {
-        *reinterpret_cast<float4 *>(g.out + off) = make_float4(o[0], o[1], o[2], o[3]);
+        __builtin_nontemporal_store(f4nt{o[0], o[1], o[2], o[3]}, reinterpret_cast<f4nt *>(g.out + off));
     } else {
         for (int c = 0; c < ncol; ++c) g.out[off + c] = o[c];
     }
@@ -412,7 +416,7 @@ __device__ __forceinline__ void decode4_store(const float (&P)[4], const int32_t
             cnt[c] = Li > 0 ? (BIP ? (KL + p) / 2 : p) : 0;
         }
         if (ncol == 4 && g.vec_cnt) {
-            *reinterpret_cast<int4 *>(g.counts + off) = make_int4(cnt[0], cnt[1], cnt[2], cnt[3]);
+            __builtin_nontemporal_store(i4nt{cnt[0], cnt[1], cnt[2], cnt[3]}, reinterpret_cast<i4nt *>(g.counts + off));
         } else {
             for (int c = 0; c < ncol; ++c) g.counts[off + c] = cnt[c];
         }
