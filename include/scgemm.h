@@ -156,7 +156,7 @@ int sc_gemm(const sc_gemm_desc *desc,
  * SC_NOALLOC_WORKSPACE_BYTES on each device the library runs on, held until the process
  * ends.  It calls no hipMalloc, hipFree or other allocating routine.
  *   Returns SC_ERR_WORKSPACE when sc_gemm_workspace_size(desc) exceeds
- *   SC_NOALLOC_WORKSPACE_BYTES (e.g. 6304 x 768 x 3072 at L = 128 needs 62 MiB), and the
+ *   SC_NOALLOC_WORKSPACE_BYTES (e.g. 6304 x 768 x 3072 at L = 128 needs 35 MiB), and the
  *   other codes as sc_gemm.
  *   status_out  NULLABLE device int32: after the call it holds the call's device status
  *               word, 0 when every L_i was in [0, L_max], nonzero (bit 0) otherwise.

@@ -50,7 +50,7 @@ def _both(g, dev):
 @pytest.mark.gpu
 def test_noalloc_matches_sc_gemm_twice(dev):
     import paper_2609_32922_amd as scg
-    w = W.vitb16_fc1_L128()                                   # 62 MiB of workspace
+    w = W.vitb16_fc1_L128()                                   # 35 MiB of workspace
     cases = [("vitb16_fc1_L128", w.gemms[0]),
              ("300x260x100 per-row L", W.random_gemm(np.random.default_rng(3), 1, 300, 260, 100, 96, 1, 33))]
     for name, g in cases:
